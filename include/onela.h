@@ -1,0 +1,210 @@
+/*
+ * onela.h -- C ABI of the MI355X (gfx950) large-beam Gated DeltaNet decode.
+ *
+ * The method is OneLA (arXiv 2609.12399): every live beam of a generative-
+ * recommendation beam search is represented by one shared post-prefill state
+ * S_ctx (Sec. 3.1) plus a short append-only chain of per-step transition
+ * records, found through a parent-pointer ancestry index (Sec. 3.3, Eq. 5).
+ * A decode step computes o_b = S_{t,b} q_b for every live beam b (Sec. 2.2,
+ * Eq. 1) without materialising any per-beam d_v x d_k state.
+ *
+ * Records.  This library stores the record of step t and beam slot b as the
+ * step's own inputs (k, v, alpha, beta) rather than the paper's
+ * (alpha, delta, k) of Sec. 3.2: with A_j = alpha_j (I - beta_j k_j k_j^T),
+ * Eq. 1 reads S_j = S_{j-1} A_j + beta_j v_j k_j^T, so the read-out
+ * S_t q_t can be evaluated by folding the query newest-to-oldest through the
+ * A_j, collecting the beta_j v_j k_j^T terms on the way, and applying S_ctx
+ * once at the end.  In exact arithmetic this is the same o_t as the paper's
+ * projection replay (Eqs. 3-4).
+ *
+ * Conventions for every entry point:
+ *   - Tensors are device pointers owned by the caller, dense, row-major, and
+ *     16-byte aligned.  The library allocates no device memory: all of its
+ *     device state lives in a caller-provided workspace.
+ *   - S is d_v x d_k (Sec. 2.2), stored [d_v][d_k].
+ *   - Value head hv uses query/key head hv / (H_V / H_K) (grouped heads).
+ *   - alpha, beta are fp32, one per (beam, value head).  q/k/v use the
+ *     context's io dtype (bf16 bits or fp32).  Outputs are fp32.
+ *   - Eq. 1 has no 1/sqrt(d_k) query scaling and none is applied.
+ *   - All device work is enqueued asynchronously on the context's stream;
+ *     no call synchronises except onela_get_device_status.  A context is
+ *     bound to one stream and is not thread-safe.
+ *   - An entry point that returns an error other than ONELA_EHIP has
+ *     enqueued nothing and left the context unchanged.
+ */
+#ifndef ONELA_H
+#define ONELA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct onela_ctx_s* onela_ctx_t;
+
+typedef enum {
+  ONELA_OK = 0,
+  ONELA_EINVAL = 1,    /* NULL or misaligned pointer, unsupported dimension */
+  ONELA_ESTEP = 2,     /* call out of the per-step protocol order */
+  ONELA_EPARENT = 3,   /* device-detected: a parent index was out of range */
+  ONELA_ECAPACITY = 4, /* width > max_beams, step >= max_steps, or a
+                          workspace smaller than required */
+  ONELA_EHIP = 5,      /* a HIP runtime call or kernel launch failed */
+  ONELA_ENOMEM = 6     /* host allocation of the context failed */
+} onela_status_t;
+
+typedef enum { ONELA_F32 = 0, ONELA_BF16 = 1 } onela_dtype_t;
+
+/* Shape of one decode context.  Supported: d_k == d_v in {32, 64, 128};
+ * io_dtype ONELA_BF16 or ONELA_F32; num_v_heads a multiple of num_qk_heads;
+ * 1 <= max_beams <= 65536; 1 <= max_steps <= 8 (the record chain of step t
+ * has t + 1 records). */
+typedef struct {
+  int32_t num_requests; /* R: independent requests, one S_ctx each */
+  int32_t num_qk_heads; /* H_K */
+  int32_t num_v_heads;  /* H_V */
+  int32_t d_k;
+  int32_t d_v;
+  int32_t max_beams;    /* W_max: upper bound on every W_t */
+  int32_t max_steps;    /* T_max: decode steps 0 .. T_max - 1 */
+  int32_t io_dtype;     /* onela_dtype_t of q, k, v */
+} onela_config_t;
+
+/* Human-readable name of a status code (static string). */
+const char* onela_status_str(onela_status_t status);
+
+/* Checks a configuration on the host (no HIP call).  ONELA_OK or
+ * ONELA_EINVAL. */
+onela_status_t onela_check_config(const onela_config_t* cfg);
+
+/* Bytes of device workspace onela_init needs for cfg (0 if cfg is invalid).
+ * Layout: status word, double-buffered ancestry index [2][R][W_max][T_max]
+ * int32, the split shared state (2 x bf16 per element of S_ctx), and the
+ * record arena: k [R][T_max][H_K][W_max][d_k], v [R][T_max][H_V][W_max][d_v]
+ * in the io dtype and (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs. */
+size_t onela_workspace_bytes(const onela_config_t* cfg);
+
+/* Creates a decode context and binds the shared post-prefill state
+ * (Sec. 3.1: S_ctx is stored once per request and shared by all beams).
+ *   s0        device, fp32 [R][H_V][d_v][d_k]; read only during this call
+ *             (it is split into bf16 high/low halves inside the workspace)
+ *   workspace device, >= onela_workspace_bytes(cfg), 256-byte aligned;
+ *             borrowed until onela_destroy, owned by the caller
+ *   stream    a hipStream_t (NULL: the default stream)
+ *   out       receives the context handle
+ * Errors: ONELA_EINVAL (bad cfg or pointers), ONELA_ECAPACITY (workspace too
+ * small), ONELA_ENOMEM, ONELA_EHIP. */
+onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
+                          void* workspace, size_t workspace_bytes, void* stream,
+                          onela_ctx_t* out);
+
+/* Starts a new beam search on the same S_ctx: forgets all records and the
+ * ancestry (host bookkeeping only; nothing is enqueued). */
+onela_status_t onela_reset(onela_ctx_t ctx);
+
+/* Ancestry index update of Sec. 3.3, Eq. 5, for decode step `step`:
+ *   h_t(b, j) = h_{t-1}(pi_t(b), j) for 0 <= j < t-1,  h_t(b, t-1) = pi_t(b).
+ * Global beam selection may reorder, duplicate or drop beams; only these
+ * integer indices change, never the stored records.
+ *   step       t; must be the next step (0 after init/reset)
+ *   width      W_t, 1 <= W_t <= max_beams
+ *   parents    device int32 [R][W_t], pi_t(b) in [0, W_{t-1}) indexing the
+ *              previous step's beams of the same request; must be NULL at
+ *              step 0 (every beam starts from S_ctx)
+ *   gather_out optional device int32 [R][W_t][t]: receives h_t (the record
+ *              slot of each beam's ancestor at steps 0..t-1); may be NULL
+ * A parent out of range is detected on the device: that beam's indices
+ * become -1 (its later outputs are unspecified but no out-of-bounds access
+ * happens) and onela_get_device_status reports ONELA_EPARENT.
+ * Host errors: ONELA_EINVAL, ONELA_ESTEP, ONELA_ECAPACITY, ONELA_EHIP. */
+onela_status_t onela_resolve_ancestry(onela_ctx_t ctx, int32_t step,
+                                      int32_t width, const int32_t* parents,
+                                      int32_t* gather_out);
+
+/* Appends the records of step `step` into the arena (Sec. 3.3: records are
+ * written once to the physical slots of the current step and never
+ * relocated).  Slot b of step t holds beam b's (k, v, alpha, beta).
+ *   k     device [R][W_t][H_K][d_k] io dtype
+ *   v     device [R][W_t][H_V][d_v] io dtype
+ *   alpha device fp32 [R][W_t][H_V]   (decay, Eq. 1)
+ *   beta  device fp32 [R][W_t][H_V]   (correction strength, Eq. 1)
+ * Must follow onela_resolve_ancestry(step) (which fixed W_t).  The inputs
+ * may be reused by the caller once the enqueued copy has run.
+ * Errors: ONELA_EINVAL, ONELA_ESTEP, ONELA_EHIP. */
+onela_status_t onela_append_records(onela_ctx_t ctx, int32_t step,
+                                    const void* k, const void* v,
+                                    const float* alpha, const float* beta);
+
+/* Decode step t: for every request r, live beam b < W_t and value head hv,
+ *   o[r][b][hv] = S_{t,b} q_b   (Eq. 1 read-out after the step-t update),
+ * where S_{t,b} is the state reached from S_ctx through the records at
+ * slots h_t(b, 0), ..., h_t(b, t-1) and the beam's own step-t record.
+ *   q device [R][W_t][H_K][d_k] io dtype
+ *   o device fp32 [R][W_t][H_V][d_v], written completely
+ * Must follow onela_append_records(step); may be repeated for the same
+ * step (it reads the context and writes only o).
+ * Errors: ONELA_EINVAL, ONELA_ESTEP, ONELA_EHIP. */
+onela_status_t onela_decode_step(onela_ctx_t ctx, int32_t step, const void* q,
+                                 float* o);
+
+/* Synchronises the context's stream, returns and clears the sticky device
+ * error (ONELA_OK or ONELA_EPARENT), or ONELA_EHIP. */
+onela_status_t onela_get_device_status(onela_ctx_t ctx);
+
+/* Frees the host-side context (the workspace stays the caller's). */
+void onela_destroy(onela_ctx_t ctx);
+
+/* ---- Setup helper: the post-prefill state S_ctx (Sec. 3.1) -------------
+ * Eq. 1 over a prompt of P tokens from S = 0, for every request and value
+ * head, fp32 state in registers.  Inputs [R][P][H_K][d_k] (k),
+ * [R][P][H_V][d_v] (v), fp32 [R][P][H_V] (alpha, beta); output fp32
+ * [R][H_V][d_v][d_k].  cfg supplies R, H_K, H_V, d_k, d_v and io_dtype.
+ * Errors: ONELA_EINVAL, ONELA_EHIP. */
+onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len,
+                                   const void* k, const void* v,
+                                   const float* alpha, const float* beta,
+                                   float* s0_out, void* stream);
+
+/* ---- Baseline: per-beam materialised states ("FullState", Sec. 2.3) ----
+ * Every live beam keeps a full fp32 d_v x d_k state per value head.  One
+ * call performs step t for all beams: copy the parent's state (S_ctx at
+ * t = 0), apply Eq. 1, store the child's state, read out o = S q.
+ * Workspace: [2][R][W_max][H_V][d_v][d_k] fp32 (double-buffered), see
+ * onela_fullstate_workspace_bytes.  parents as in onela_resolve_ancestry
+ * (NULL at step 0), prev_width = W_{t-1}.  Parents out of range are clamped
+ * to 0 on the device and reported through *status_word (device int32, set
+ * to nonzero; may be NULL).  Errors: ONELA_EINVAL, ONELA_ECAPACITY,
+ * ONELA_EHIP. */
+size_t onela_fullstate_workspace_bytes(const onela_config_t* cfg);
+onela_status_t onela_fullstate_step(const onela_config_t* cfg, int32_t step,
+                                    int32_t width, int32_t prev_width,
+                                    const int32_t* parents, const float* s0,
+                                    const void* q, const void* k, const void* v,
+                                    const float* alpha, const float* beta,
+                                    float* o, void* workspace,
+                                    size_t workspace_bytes, int32_t* status_word,
+                                    void* stream);
+
+/* ---- Capacity model (host only) -----------------------------------------
+ * Persistent recurrent-state bytes after `steps` decode steps for one GDN
+ * layer (Sec. 4.4): one S_ctx per request and value head (state_bytes per
+ * element) plus one record per (step, beam, value head).  record_bytes is
+ * the size of one record; the paper's (alpha fp32, delta 16-bit, k 16-bit)
+ * record at d_k = d_v = 128 is 516 bytes.  The FullState equivalent is
+ * onela_fullstate_capacity_bytes.  Return 0 on invalid arguments. */
+uint64_t onela_capacity_bytes(int32_t num_requests, int32_t num_v_heads,
+                              int32_t d_k, int32_t d_v, int32_t beams,
+                              int32_t steps, int32_t state_bytes,
+                              int32_t record_bytes);
+uint64_t onela_fullstate_capacity_bytes(int32_t num_requests,
+                                        int32_t num_v_heads, int32_t d_k,
+                                        int32_t d_v, int32_t beams,
+                                        int32_t state_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ONELA_H */

@@ -1,0 +1,65 @@
+// Internal declarations shared by the host side (onela_api.cpp) and the HIP
+// kernels of libonela.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace onela {
+
+// Maximum records in one beam's chain (decode steps 0 .. kMaxSteps-1).
+constexpr int kMaxSteps = 8;
+
+// Bits of the sticky device status word.
+constexpr int kStatusParent = 1;
+
+struct Shape {
+  int R, HK, HV, dk, dv;
+  int wmax, tmax;
+  bool bf16;  // q/k/v stored as bf16 bits (else fp32)
+  int io_bytes() const { return bf16 ? 2 : 4; }
+};
+
+// Device views carved out of the caller's workspace.
+struct Arena {
+  int* status;       // sticky error bits
+  int* anc[2];       // ancestry h_t, [R][wmax][tmax] int32, buffer t % 2
+  uint16_t* s_frag;  // S_ctx split into bf16 hi/lo, MFMA fragment order
+  void* k;           // [R][tmax][HK][wmax][dk] io dtype
+  void* v;           // [R][tmax][HV][wmax][dv] io dtype
+  float2* ab;        // [R][tmax][HV][wmax] (alpha, beta)
+};
+
+// Bytes of each region, in workspace order, each rounded up to 256.
+struct Layout {
+  size_t status, anc, s_frag, k, v, ab, total;
+};
+Layout layout_of(const Shape& s);
+
+// ---- launchers (each returns hipGetLastError() after the launch) ---------
+hipError_t launch_clear_status(int* status, hipStream_t st);
+hipError_t launch_split_state(const Shape& s, const float* s0, uint16_t* frag,
+                              hipStream_t st);
+hipError_t launch_resolve(const Shape& s, int step, int width, int prev_width,
+                          const int* parents, const int* anc_prev, int* anc_cur,
+                          int* gather_out, int* status, hipStream_t st);
+hipError_t launch_append(const Shape& s, int step, int width, const void* k,
+                         const void* v, const float* alpha, const float* beta,
+                         const Arena& a, hipStream_t st);
+hipError_t launch_decode(const Shape& s, int step, int width, const void* q,
+                         float* o, const Arena& a, hipStream_t st);
+hipError_t launch_prefill(const Shape& s, int prompt_len, const void* k,
+                          const void* v, const float* alpha, const float* beta,
+                          float* s0_out, hipStream_t st);
+hipError_t launch_fullstate(const Shape& s, int step, int width, int prev_width,
+                            const int* parents, const float* s0, const void* q,
+                            const void* k, const void* v, const float* alpha,
+                            const float* beta, float* o, const float* states_in,
+                            float* states_out, int* status, hipStream_t st);
+
+// True when the decode kernel has an instance for this shape.
+bool decode_supported(const Shape& s);
+
+}  // namespace onela

@@ -1,0 +1,273 @@
+// Host side of libonela: argument validation, workspace carving, per-step
+// protocol bookkeeping and kernel launches.  Every check that can fail runs
+// before anything is enqueued, so a rejected call leaves no device work and
+// no change in the context.
+#include <cstdint>
+#include <cstdlib>
+#include <new>
+
+#include "../../include/onela.h"
+#include "internal.h"
+
+using onela::Arena;
+using onela::Layout;
+using onela::Shape;
+
+struct onela_ctx_s {
+  Shape shape;
+  Arena arena;
+  hipStream_t stream;
+  int resolved;  // last step whose ancestry was resolved (-1: none)
+  int appended;  // last step whose records were appended (-1: none)
+  int widths[onela::kMaxSteps];
+};
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+onela_status_t shape_of(const onela_config_t* c, Shape* s) {
+  if (!c) return ONELA_EINVAL;
+  if (c->num_requests < 1 || c->num_qk_heads < 1 || c->num_v_heads < 1)
+    return ONELA_EINVAL;
+  if (c->num_v_heads % c->num_qk_heads) return ONELA_EINVAL;
+  if (c->max_beams < 1 || c->max_beams > 65536) return ONELA_EINVAL;
+  if (c->max_steps < 1 || c->max_steps > onela::kMaxSteps) return ONELA_EINVAL;
+  if (c->io_dtype != ONELA_F32 && c->io_dtype != ONELA_BF16) return ONELA_EINVAL;
+  Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads, c->d_k, c->d_v,
+          c->max_beams,    c->max_steps,    c->io_dtype == ONELA_BF16};
+  if (!onela::decode_supported(t)) return ONELA_EINVAL;
+  // every index the kernels form must fit in 32-bit element counts per region
+  const double big = double(t.R) * t.tmax * (t.HV > t.HK ? t.HV : t.HK) * t.wmax *
+                     (t.dv > t.dk ? t.dv : t.dk);
+  if (big >= 2147483647.0) return ONELA_EINVAL;
+  *s = t;
+  return ONELA_OK;
+}
+
+bool launch_ok(hipError_t e) { return e == hipSuccess; }
+
+}  // namespace
+
+namespace onela {
+
+Layout layout_of(const Shape& s) {
+  Layout l{};
+  const size_t R = s.R, T = s.tmax, W = s.wmax;
+  l.status = 256;
+  l.anc = round256(sizeof(int) * R * W * T);
+  l.s_frag = round256(sizeof(uint16_t) * 2 * R * s.HV * size_t(s.dv) * s.dk);
+  l.k = round256(size_t(s.io_bytes()) * R * T * s.HK * W * s.dk);
+  l.v = round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
+  l.ab = round256(sizeof(float2) * R * T * s.HV * W);
+  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab;
+  return l;
+}
+
+}  // namespace onela
+
+extern "C" {
+
+const char* onela_status_str(onela_status_t st) {
+  switch (st) {
+    case ONELA_OK: return "ok";
+    case ONELA_EINVAL: return "invalid argument";
+    case ONELA_ESTEP: return "call out of step order";
+    case ONELA_EPARENT: return "parent index out of range (device)";
+    case ONELA_ECAPACITY: return "capacity exceeded";
+    case ONELA_EHIP: return "HIP runtime error";
+    case ONELA_ENOMEM: return "host allocation failed";
+  }
+  return "unknown status";
+}
+
+onela_status_t onela_check_config(const onela_config_t* cfg) {
+  Shape s;
+  return shape_of(cfg, &s);
+}
+
+size_t onela_workspace_bytes(const onela_config_t* cfg) {
+  Shape s;
+  if (shape_of(cfg, &s) != ONELA_OK) return 0;
+  return onela::layout_of(s).total;
+}
+
+onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
+                          void* workspace, size_t workspace_bytes, void* stream,
+                          onela_ctx_t* out) {
+  Shape s;
+  onela_status_t rc = shape_of(cfg, &s);
+  if (rc != ONELA_OK) return rc;
+  if (!s0 || !workspace || !out || !aligned16(s0)) return ONELA_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return ONELA_EINVAL;
+  const Layout l = onela::layout_of(s);
+  if (workspace_bytes < l.total) return ONELA_ECAPACITY;
+
+  onela_ctx_s* c = new (std::nothrow) onela_ctx_s();
+  if (!c) return ONELA_ENOMEM;
+  c->shape = s;
+  c->stream = static_cast<hipStream_t>(stream);
+  c->resolved = -1;
+  c->appended = -1;
+  char* p = static_cast<char*>(workspace);
+  c->arena.status = reinterpret_cast<int*>(p);
+  p += l.status;
+  c->arena.anc[0] = reinterpret_cast<int*>(p);
+  p += l.anc;
+  c->arena.anc[1] = reinterpret_cast<int*>(p);
+  p += l.anc;
+  c->arena.s_frag = reinterpret_cast<uint16_t*>(p);
+  p += l.s_frag;
+  c->arena.k = p;
+  p += l.k;
+  c->arena.v = p;
+  p += l.v;
+  c->arena.ab = reinterpret_cast<float2*>(p);
+
+  if (!launch_ok(onela::launch_clear_status(c->arena.status, c->stream)) ||
+      !launch_ok(onela::launch_split_state(s, s0, c->arena.s_frag, c->stream))) {
+    delete c;
+    return ONELA_EHIP;
+  }
+  *out = c;
+  return ONELA_OK;
+}
+
+onela_status_t onela_reset(onela_ctx_t c) {
+  if (!c) return ONELA_EINVAL;
+  c->resolved = -1;
+  c->appended = -1;
+  return ONELA_OK;
+}
+
+onela_status_t onela_resolve_ancestry(onela_ctx_t c, int32_t step, int32_t width,
+                                      const int32_t* parents, int32_t* gather_out) {
+  if (!c) return ONELA_EINVAL;
+  const Shape& s = c->shape;
+  if (step != c->resolved + 1 || c->appended != c->resolved) return ONELA_ESTEP;
+  if (step >= s.tmax) return ONELA_ECAPACITY;
+  if (width < 1 || width > s.wmax) return ONELA_ECAPACITY;
+  if (step == 0 && parents) return ONELA_EINVAL;
+  if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
+  if (gather_out && !aligned4(gather_out)) return ONELA_EINVAL;
+  if (step > 0) {
+    hipError_t e = onela::launch_resolve(s, step, width, c->widths[step - 1], parents,
+                                         c->arena.anc[(step - 1) & 1],
+                                         c->arena.anc[step & 1], gather_out,
+                                         c->arena.status, c->stream);
+    if (!launch_ok(e)) return ONELA_EHIP;
+  }
+  c->widths[step] = width;
+  c->resolved = step;
+  return ONELA_OK;
+}
+
+onela_status_t onela_append_records(onela_ctx_t c, int32_t step, const void* k,
+                                    const void* v, const float* alpha,
+                                    const float* beta) {
+  if (!c) return ONELA_EINVAL;
+  if (step != c->resolved || step != c->appended + 1) return ONELA_ESTEP;
+  if (!k || !v || !alpha || !beta) return ONELA_EINVAL;
+  if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta))
+    return ONELA_EINVAL;
+  hipError_t e = onela::launch_append(c->shape, step, c->widths[step], k, v, alpha,
+                                      beta, c->arena, c->stream);
+  if (!launch_ok(e)) return ONELA_EHIP;
+  c->appended = step;
+  return ONELA_OK;
+}
+
+onela_status_t onela_decode_step(onela_ctx_t c, int32_t step, const void* q, float* o) {
+  if (!c) return ONELA_EINVAL;
+  if (step < 0 || step != c->resolved || step != c->appended) return ONELA_ESTEP;
+  if (!q || !o || !aligned16(q) || !aligned16(o)) return ONELA_EINVAL;
+  hipError_t e = onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
+                                      c->stream);
+  return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
+}
+
+onela_status_t onela_get_device_status(onela_ctx_t c) {
+  if (!c) return ONELA_EINVAL;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return ONELA_EHIP;
+  int word = 0;
+  if (hipMemcpy(&word, c->arena.status, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+    return ONELA_EHIP;
+  if (word == 0) return ONELA_OK;
+  if (!launch_ok(onela::launch_clear_status(c->arena.status, c->stream)) ||
+      hipStreamSynchronize(c->stream) != hipSuccess)
+    return ONELA_EHIP;
+  return ONELA_EPARENT;
+}
+
+void onela_destroy(onela_ctx_t c) { delete c; }
+
+onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len,
+                                   const void* k, const void* v, const float* alpha,
+                                   const float* beta, float* s0_out, void* stream) {
+  Shape s;
+  onela_status_t rc = shape_of(cfg, &s);
+  if (rc != ONELA_OK) return rc;
+  if (prompt_len < 0 || !s0_out || !aligned16(s0_out)) return ONELA_EINVAL;
+  if (prompt_len > 0 && (!k || !v || !alpha || !beta || !aligned16(k) || !aligned16(v) ||
+                         !aligned4(alpha) || !aligned4(beta)))
+    return ONELA_EINVAL;
+  hipError_t e = onela::launch_prefill(s, prompt_len, k, v, alpha, beta, s0_out,
+                                       static_cast<hipStream_t>(stream));
+  return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
+}
+
+size_t onela_fullstate_workspace_bytes(const onela_config_t* cfg) {
+  Shape s;
+  if (shape_of(cfg, &s) != ONELA_OK) return 0;
+  return 2 * sizeof(float) * size_t(s.R) * s.wmax * s.HV * size_t(s.dv) * s.dk;
+}
+
+onela_status_t onela_fullstate_step(const onela_config_t* cfg, int32_t step,
+                                    int32_t width, int32_t prev_width,
+                                    const int32_t* parents, const float* s0,
+                                    const void* q, const void* k, const void* v,
+                                    const float* alpha, const float* beta, float* o,
+                                    void* workspace, size_t workspace_bytes,
+                                    int32_t* status_word, void* stream) {
+  Shape s;
+  onela_status_t rc = shape_of(cfg, &s);
+  if (rc != ONELA_OK) return rc;
+  if (step < 0 || width < 1 || width > s.wmax) return ONELA_ECAPACITY;
+  if (step > 0 && (prev_width < 1 || prev_width > s.wmax)) return ONELA_ECAPACITY;
+  if (step == 0 && parents) return ONELA_EINVAL;
+  if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
+  if (!s0 || !q || !k || !v || !alpha || !beta || !o || !workspace) return ONELA_EINVAL;
+  if (!aligned16(s0) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+      !aligned4(alpha) || !aligned4(beta) || !aligned16(workspace))
+    return ONELA_EINVAL;
+  if (status_word && !aligned4(status_word)) return ONELA_EINVAL;
+  const size_t half = sizeof(float) * size_t(s.R) * s.wmax * s.HV * size_t(s.dv) * s.dk;
+  if (workspace_bytes < 2 * half) return ONELA_ECAPACITY;
+  float* base = static_cast<float*>(workspace);
+  float* buf[2] = {base, base + half / sizeof(float)};
+  hipError_t e = onela::launch_fullstate(s, step, width, prev_width, parents, s0, q, k, v,
+                                         alpha, beta, o, buf[(step + 1) & 1], buf[step & 1],
+                                         status_word, static_cast<hipStream_t>(stream));
+  return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
+}
+
+uint64_t onela_capacity_bytes(int32_t R, int32_t HV, int32_t dk, int32_t dv, int32_t beams,
+                              int32_t steps, int32_t state_bytes, int32_t record_bytes) {
+  if (R < 0 || HV < 0 || dk < 0 || dv < 0 || beams < 0 || steps < 0 || state_bytes < 0 ||
+      record_bytes < 0)
+    return 0;
+  const uint64_t ctx = uint64_t(R) * HV * uint64_t(dv) * dk * state_bytes;
+  const uint64_t rec = uint64_t(steps) * R * uint64_t(beams) * HV * record_bytes;
+  return ctx + rec;
+}
+
+uint64_t onela_fullstate_capacity_bytes(int32_t R, int32_t HV, int32_t dk, int32_t dv,
+                                        int32_t beams, int32_t state_bytes) {
+  if (R < 0 || HV < 0 || dk < 0 || dv < 0 || beams < 0 || state_bytes < 0) return 0;
+  return uint64_t(R) * beams * HV * uint64_t(dv) * dk * state_bytes;
+}
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, validates arguments on the host before any HIP call, and
+its capacity model reproduces the paper's printed accounting."""
+import ctypes
+import json
+import os
+import re
+from decimal import ROUND_HALF_UP, Decimal
+
+import pytest
+
+from paper_2609_12399_amd import onela as ab
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "onela.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ab.load_library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(onela_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = header_functions()
+    assert len(declared) >= 15
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(ab.EXPORTED) == declared
+
+
+def cfg(**kw):
+    base = dict(num_requests=1, num_qk_heads=16, num_v_heads=16, d_k=128, d_v=128,
+                max_beams=512, max_steps=4, io_dtype=ab.ONELA_BF16)
+    base.update(kw)
+    return ab.make_config(**base)
+
+
+def test_config_validation(lib):
+    assert ab.onela_check_config(cfg()) == ab.ONELA_OK
+    assert ab.onela_check_config(cfg(d_k=32, d_v=32, io_dtype=ab.ONELA_F32)) == ab.ONELA_OK
+    assert ab.onela_check_config(cfg(num_v_heads=32)) == ab.ONELA_OK
+    bad = [dict(num_v_heads=24, num_qk_heads=16), dict(d_k=96, d_v=96), dict(d_k=128, d_v=64),
+           dict(max_beams=0), dict(max_beams=65537), dict(max_steps=0), dict(max_steps=9),
+           dict(io_dtype=7), dict(num_requests=0), dict(num_qk_heads=0)]
+    for b in bad:
+        assert ab.onela_check_config(cfg(**b)) == ab.ONELA_EINVAL, b
+        assert ab.onela_workspace_bytes(cfg(**b)) == 0, b
+    assert lib.onela_check_config(None) == ab.ONELA_EINVAL
+
+
+def test_workspace_bytes_layout(lib):
+    n = ab.onela_workspace_bytes(cfg())
+    R, T, W, H, d = 1, 4, 512, 16, 128
+    expect = (256 + 2 * (W * T * 4) + 2 * 2 * H * d * d + 2 * T * H * W * d * 2
+              + T * H * W * 8)
+    assert n == expect
+    assert n % 256 == 0
+
+
+def test_host_errors_before_any_hip_call(lib):
+    c = cfg()
+    out = ctypes.c_void_p()
+    # NULL pointers / misaligned pointers / short workspace: rejected on the host
+    assert lib.onela_init(ctypes.byref(c), None, 256, 1 << 30, None, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert lib.onela_init(ctypes.byref(c), 4096, None, 1 << 30, None, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert lib.onela_init(ctypes.byref(c), 4100, 4096, 1 << 30, None, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert lib.onela_init(ctypes.byref(c), 4096, 4096 + 16, 1 << 30, None, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert lib.onela_init(ctypes.byref(c), 4096, 4096, 100, None, ctypes.byref(out)) == ab.ONELA_ECAPACITY
+    bad = cfg(d_k=100)
+    assert lib.onela_init(ctypes.byref(bad), 4096, 4096, 1 << 30, None, ctypes.byref(out)) == ab.ONELA_EINVAL
+    # calls on a NULL context
+    assert lib.onela_resolve_ancestry(None, 0, 4, None, None) == ab.ONELA_EINVAL
+    assert lib.onela_append_records(None, 0, 16, 16, 16, 16) == ab.ONELA_EINVAL
+    assert lib.onela_decode_step(None, 0, 16, 16) == ab.ONELA_EINVAL
+    assert lib.onela_reset(None) == ab.ONELA_EINVAL
+    assert lib.onela_get_device_status(None) == ab.ONELA_EINVAL
+    lib.onela_destroy(None)
+    # prefill / fullstate argument checks
+    assert lib.onela_prefill_state(ctypes.byref(c), -1, 16, 16, 16, 16, 16, None) == ab.ONELA_EINVAL
+    assert lib.onela_prefill_state(ctypes.byref(c), 4, None, 16, 16, 16, 16, None) == ab.ONELA_EINVAL
+    fs = lib.onela_fullstate_step
+    assert fs(ctypes.byref(c), 0, 513, 0, None, 16, 16, 16, 16, 16, 16, 16, 256, 1 << 40, None, None) == ab.ONELA_ECAPACITY
+    assert fs(ctypes.byref(c), 1, 8, 8, None, 16, 16, 16, 16, 16, 16, 16, 256, 1 << 40, None, None) == ab.ONELA_EINVAL
+    assert fs(ctypes.byref(c), 0, 8, 0, 64, 16, 16, 16, 16, 16, 16, 16, 256, 1 << 40, None, None) == ab.ONELA_EINVAL
+    assert fs(ctypes.byref(c), 0, 8, 0, None, 16, 16, 16, 16, 16, 16, 16, 256, 10, None, None) == ab.ONELA_ECAPACITY
+
+
+def test_status_strings(lib):
+    for code in range(7):
+        assert ab.onela_status_str(code)
+    assert ab.onela_status_str(99) == "unknown status"
+
+
+def sig3(x):
+    """x rounded half-up to 3 significant digits (the paper's printing)."""
+    d = Decimal(repr(float(x)))
+    q = Decimal(1).scaleb(d.adjusted() - 2)
+    return d.quantize(q, rounding=ROUND_HALF_UP)
+
+
+def test_capacity_model_matches_paper(lib):
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "capacity_e3.json")))
+    w = g["workload"]
+    MiB = float(1 << 20)
+    record = 4 + 2 * w["d_v"] + 2 * w["d_k"]  # alpha fp32 + delta 16-bit + k 16-bit
+    assert record == 516
+    full = ab.onela_fullstate_capacity_bytes(w["R"], w["H"], w["d_k"], w["d_v"], w["W"], 4)
+    for O in (3, 7):
+        T = O - 1
+        cap = ab.onela_capacity_bytes(w["R"], w["H"], w["d_k"], w["d_v"], w["W"], T, 4, record)
+        writes = ab.onela_capacity_bytes(w["R"], w["H"], w["d_k"], w["d_v"], w["W"], T, 0, record)
+        pr = g["printed"]
+        key = f"O={O}"
+        assert sig3(cap / MiB) == sig3(pr["capacity_mib"][key])
+        assert sig3(full / cap) == sig3(pr["capacity_reduction_vs_fullstate"][key])
+        assert sig3(writes / MiB) == sig3(pr["state_writes_mib"][key])
+        assert sig3(T * full / writes) == sig3(pr["write_reduction_vs_fullstate"][key])
+    assert ab.onela_capacity_bytes(-1, 1, 1, 1, 1, 1, 1, 1) == 0
+
+
+def test_binding_rejects_host_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        ab._dev(torch.zeros(4), "x")
+    assert ab._dev(None, "x", optional=True) is None
+    assert ab._dev(1234, "x") == 1234

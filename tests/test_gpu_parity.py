@@ -1,0 +1,233 @@
+"""Parity of the HIP decode path (through the C ABI) with the fp64 oracle.
+
+Ancestry and gather indices must be bit-exact; outputs within REL_TOL (max
+over output vectors of ||o_gpu - o_ref||_inf / ||o_ref||_inf).  Every
+workload is seeded and synthetic; S_ctx is the oracle's fp64 prefill rounded
+once to fp32 and fed to both sides.
+"""
+import numpy as np
+import pytest
+
+from paper_2609_12399_amd import onela as ab
+from paper_2609_12399_amd import runner
+from paper_2609_12399_amd import workload as W
+from tests.gpu_common import REL_TOL, cached_case, log, oracle_ancestry, oracle_outputs, \
+    oracle_s0, rel_err
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+DEV = "cuda:0"
+
+
+def run_gpu(wl, s0, with_gather=True):
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    dec = runner.Decoder(wl.spec, torch.from_numpy(s0).to(DEV), DEV)
+    gathers = None
+    if with_gather:
+        gathers = [torch.full((wl.spec.R, st.width, max(t, 1)), -7, dtype=torch.int32,
+                              device=DEV) for t, st in enumerate(dw.steps)]
+    outs = dec.run(dw, gathers=gathers)
+    assert dec.status() == ab.ONELA_OK
+    torch.cuda.synchronize()
+    o = [x.cpu().numpy() for x in outs]
+    g = None if gathers is None else [x.cpu().numpy()[:, :, :t] for t, x in enumerate(gathers)]
+    dec.close()
+    return o, g
+
+
+@pytest.mark.parametrize("name", list(W.SPECS))
+def test_decode_matches_oracle(name):
+    log(f"[parity] {name}")
+    wl, s0, ref = cached_case(name)
+    o, g = run_gpu(wl, s0)
+    anc = oracle_ancestry(wl)
+    for t in range(wl.spec.T):
+        assert np.array_equal(g[t], anc[t]), f"ancestry differs at t={t}"
+    errs = [rel_err(o[t], ref[t]) for t in range(wl.spec.T)]
+    log(f"[parity] {name} max rel err per step {['%.2e' % e for e in errs]}")
+    assert max(errs) <= REL_TOL
+
+
+@pytest.mark.parametrize("base,widths", [
+    ("tiny_h2_d32_w8", (5, 21, 17, 33)),
+    ("h16_d128_w128", (1, 3, 40, 7, 100)),
+    ("h16_d128_w128", (37, 129, 2)),
+])
+def test_ragged_and_changing_widths(base, widths):
+    log(f"[ragged] {base} {widths}")
+    spec = W.with_widths(base, widths, P=64, seed=77)
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    o, g = run_gpu(wl, s0)
+    anc = oracle_ancestry(wl)
+    for t in range(spec.T):
+        assert np.array_equal(g[t], anc[t])
+        assert rel_err(o[t], ref[t]) <= REL_TOL
+
+
+def _small(io="bf16", d=128, widths=(16, 16, 16), HK=2, HV=4, seed=5):
+    return W.WorkloadSpec("small", 1, HK, HV, d, d, 32, tuple(widths), io, "uniform", seed=seed)
+
+
+def _set(x: W.Tensor, values):
+    """Replace a workload tensor's values (rounded to its dtype)."""
+    v = np.broadcast_to(np.asarray(values, dtype=np.float64), x.shape).astype(np.float32)
+    x.dev = W.f32_to_bf16_bits(v) if x.dtype == "bf16" else v.copy()
+
+
+def test_identity_gates_read_context():
+    """alpha = 1, beta = 0: o = S_ctx q for every beam."""
+    wl = W.make_workload(_small())
+    for st in wl.steps:
+        _set(st.alpha, 1.0)
+        _set(st.beta, 0.0)
+    s0 = oracle_s0(wl)
+    o, _ = run_gpu(wl, s0)
+    G = wl.spec.HV // wl.spec.HK
+    for t, st in enumerate(wl.steps):
+        q = st.q.f64[0]
+        ref = np.einsum("hij,bhj->bhi", s0[0].astype(np.float64), np.repeat(q, G, axis=1))
+        assert rel_err(o[t][0], ref) <= 1e-4
+
+
+def test_zero_decay_and_delta_write_bit_exact():
+    """alpha = beta = 1 with k = q = e_i makes o_t = v_t exactly on the fold
+    path (c = 1, the folded query becomes exactly 0); alpha = 0 gives
+    o_t = beta_t (k_t . q_t) v_t."""
+    spec = _small(widths=(16, 16, 16, 16))
+    wl = W.make_workload(spec)
+    rng = np.random.default_rng(3)
+    t = 2
+    st = wl.steps[t]
+    e = np.zeros(st.k.shape)
+    cols = rng.integers(0, spec.dk, size=(spec.W, spec.HK))
+    for b in range(spec.W):
+        for h in range(spec.HK):
+            e[0, b, h, cols[b, h]] = 1.0
+    _set(st.k, e)
+    _set(st.q, e)
+    _set(st.alpha, 1.0)
+    _set(st.beta, 1.0)
+    st3 = wl.steps[3]
+    _set(st3.alpha, 0.0)
+    s0 = oracle_s0(wl)
+    o, _ = run_gpu(wl, s0)
+    G = spec.HV // spec.HK
+    v = st.v.dev
+    got = o[t][0]
+    exp = W.bf16_bits_to_f64(v[0]).astype(np.float32)
+    assert np.array_equal(got, exp), "delta-rule write not exact"
+    kq = np.sum(st3.k.f64[0] * st3.q.f64[0], axis=-1)  # [W][HK]
+    ref = st3.beta.f64[0][..., None] * np.repeat(kq, G, axis=1)[..., None] * st3.v.f64[0]
+    assert rel_err(o[3][0], ref) <= 1e-5
+
+
+def test_duplicated_parents_bitwise_identical():
+    """Siblings with the same parent and identical inputs get identical
+    outputs bit for bit (beam position in a tile does not matter)."""
+    spec = _small(widths=(8, 40, 40), seed=9)
+    wl = W.make_workload(spec)
+    par = wl.steps[1].parents
+    par[0, :] = 3
+    for st in wl.steps[1:]:
+        for x in (st.q, st.k, st.v, st.alpha, st.beta):
+            x.dev[0, 1:] = x.dev[0, :1]
+    wl.steps[2].parents[0, :] = np.arange(40) % 40
+    s0 = oracle_s0(wl)
+    o, _ = run_gpu(wl, s0)
+    for t in (1, 2):
+        assert all(np.array_equal(o[t][0, 0], o[t][0, b]) for b in range(1, 40)), t
+
+
+def test_run_to_run_deterministic():
+    wl, s0, _ = cached_case("h16_d128_w128")
+    o1, _ = run_gpu(wl, s0, with_gather=False)
+    o2, _ = run_gpu(wl, s0, with_gather=False)
+    for a, b in zip(o1, o2):
+        assert np.array_equal(a, b)
+
+
+def test_bad_parent_is_reported_and_contained():
+    spec = _small(widths=(16, 16, 16), seed=21)
+    wl = W.make_workload(spec)
+    bad_beam = 5
+    wl.steps[1].parents[0, bad_beam] = 16  # == W_0: out of range
+    good_wl = W.make_workload(spec)
+    good_wl.steps[1].parents[0, bad_beam] = 0
+    s0 = oracle_s0(good_wl)
+    ref, _ = oracle_outputs(good_wl, s0)
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    dec = runner.Decoder(spec, torch.from_numpy(s0).to(DEV), DEV)
+    outs = dec.run(dw)
+    assert dec.status() == ab.ONELA_EPARENT
+    assert dec.status() == ab.ONELA_OK  # cleared after reporting
+    o = [x.cpu().numpy() for x in outs]
+    # beams whose ancestry avoids the bad slot are still exact
+    par2 = wl.steps[2].parents[0]
+    ok2 = par2 != bad_beam
+    assert rel_err(o[1][0][np.arange(16) != bad_beam], ref[1][0][np.arange(16) != bad_beam]) <= REL_TOL
+    assert rel_err(o[2][0][ok2], ref[2][0][ok2]) <= REL_TOL
+    dec.close()
+
+
+def test_protocol_order_enforced():
+    wl = W.make_workload(_small())
+    s0 = oracle_s0(wl)
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    dec = runner.Decoder(wl.spec, torch.from_numpy(s0).to(DEV), DEV)
+    st0, st1 = dw.steps[0], dw.steps[1]
+    o = torch.empty((1, 16, wl.spec.HV, wl.spec.dv), device=DEV)
+    with pytest.raises(ab.OnelaError) as e:
+        ab.onela_decode_step(dec.ctx, 0, st0.q, o)
+    assert e.value.status == ab.ONELA_ESTEP
+    with pytest.raises(ab.OnelaError):
+        ab.onela_append_records(dec.ctx, 0, st0.k, st0.v, st0.alpha, st0.beta)
+    with pytest.raises(ab.OnelaError) as e:
+        ab.onela_resolve_ancestry(dec.ctx, 0, 16, st1.parents)  # parents at step 0
+    assert e.value.status == ab.ONELA_EINVAL
+    with pytest.raises(ab.OnelaError) as e:
+        ab.onela_resolve_ancestry(dec.ctx, 0, 17)  # wider than max_beams
+    assert e.value.status == ab.ONELA_ECAPACITY
+    dec.step(0, st0, o)
+    first = o.cpu().numpy().copy()
+    ab.onela_decode_step(dec.ctx, 0, st0.q, o)  # repeating a decode is allowed
+    assert np.array_equal(o.cpu().numpy(), first)
+    with pytest.raises(ab.OnelaError) as e:
+        ab.onela_resolve_ancestry(dec.ctx, 1, 16, None)  # parents required
+    assert e.value.status == ab.ONELA_EINVAL
+    with pytest.raises(ab.OnelaError) as e:
+        ab.onela_resolve_ancestry(dec.ctx, 2, 16, st1.parents)  # skipped a step
+    assert e.value.status == ab.ONELA_ESTEP
+    dec.reset()
+    outs = dec.run(dw)
+    assert np.array_equal(outs[0].cpu().numpy(), first)
+    dec.close()
+
+
+@pytest.mark.parametrize("name", ["tiny_h2_d32_w8", "h16_d128_w128"])
+def test_fullstate_baseline_matches_oracle(name):
+    log(f"[fullstate] {name}")
+    wl, s0, ref = cached_case(name)
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    base = runner.FullStateBaseline(wl.spec, torch.from_numpy(s0).to(DEV), DEV)
+    outs = base.run(dw)
+    torch.cuda.synchronize()
+    assert int(base.status_word[0].item()) == 0
+    for t in range(wl.spec.T):
+        assert rel_err(outs[t].cpu().numpy(), ref[t]) <= REL_TOL
+
+
+@pytest.mark.parametrize("name", ["tiny_h2_d32_w8", "h16_d128_w128"])
+def test_prefill_matches_oracle(name):
+    log(f"[prefill] {name}")
+    wl, s0, _ = cached_case(name)
+    spec = wl.spec
+    prompt = tuple(runner.device_tensor(x, DEV) for x in
+                   (wl.prompt_k, wl.prompt_v, wl.prompt_alpha, wl.prompt_beta))
+    got = runner.prefill_state(spec, prompt, DEV).cpu().numpy()
+    ref = oracle_s0(wl)
+    err = np.max(np.abs(got - ref)) / np.max(np.abs(ref))
+    log(f"[prefill] {name} rel err {err:.2e}")
+    assert err <= 1e-4
