@@ -1,9 +1,11 @@
 """Benchmark of the large-beam GDN decode hot path on one MI355X.
 
 One *step* is one pass of the whole hot path over one batch (one request
-group) of synthetic input: ``onela_init`` (bind + split S_ctx), then for every
-decode step t: ``onela_resolve_ancestry`` -> ``onela_append_records`` ->
-``onela_decode_step``.  The default workload is 1 GDN layer, 16 heads,
+group) of synthetic input: ``onela_init`` (binds S_ctx, enqueues nothing), then for every
+decode step t one ``onela_decode_step_fused`` (ancestry resolve, record append
+and decode in one launch).  The same step through the three separate calls
+(``onela_resolve_ancestry`` -> ``onela_append_records`` ->
+``onela_decode_step``) is timed too and reported beside it.  The default workload is 1 GDN layer, 16 heads,
 d_k = d_v = 128, bf16 inputs, a 4096-token prompt, 512 beams, 4 decode steps,
 Zipf(1.1) parents.
 
@@ -14,9 +16,10 @@ batch i % batches, so a batch's data was last touched far more than the
 captured graph per batch) so host launch cost does not pace the GPU.
 
 Printed: one JSON line with the whole-job throughput (beam-tokens/s), the
-per-kernel roofline of the decode kernel (algorithmic bytes / average kernel
-duration from HIP events on the kernels' stream), the per-beam FullState GPU
-baseline, and the fp64 CPU oracle timed on this host.
+per-kernel roofline of the fused step kernel (algorithmic bytes / average
+launch duration from HIP events around back-to-back launches on the kernels'
+stream), the separate-call path, the per-beam FullState GPU baseline, and the
+fp64 CPU oracle timed on this host.
 """
 from __future__ import annotations
 
@@ -57,13 +60,13 @@ def unique_record_slots(wl, t):
 
 
 def decode_alg_bytes(wl, t):
-    """Algorithmic HBM bytes of one decode launch at step t: split S_ctx once,
+    """Algorithmic HBM bytes of one decode launch at step t: S_ctx (fp32) once,
     q, o, the unique records referenced and the ancestry indices."""
     s = wl.spec
     io = 2 if s.io_dtype == "bf16" else 4
     W = s.widths[t]
     rec = s.HK * s.dk * io + s.HV * (s.dv * io + 8)  # one slot, all heads
-    b = s.R * s.HV * s.dv * s.dk * 4          # S_ctx hi + lo bf16
+    b = s.R * s.HV * s.dv * s.dk * 4          # S_ctx fp32
     b += s.R * W * s.HK * s.dk * io           # q
     b += s.R * W * s.HV * s.dv * 4            # o (fp32)
     b += sum(unique_record_slots(wl, t)) * rec
@@ -71,19 +74,43 @@ def decode_alg_bytes(wl, t):
     return b
 
 
-def step_alg_bytes(wl):
-    """Algorithmic bytes of one whole step: split (read fp32 S, write hi/lo),
-    per t: resolve (parents + h_{t-1} rows + h_t), append (read + write one
-    slab), decode."""
+def slab_bytes(wl, t):
     s = wl.spec
     io = 2 if s.io_dtype == "bf16" else 4
-    total = 2 * s.R * s.HV * s.dv * s.dk * 4
+    return s.R * s.widths[t] * (s.HK * s.dk * io + s.HV * (s.dv * io + 8))
+
+
+def unique_parents(wl, t):
+    return sum(len(np.unique(wl.steps[t].parents[r])) for r in range(wl.spec.R)) if t else 0
+
+
+def fused_alg_bytes(wl, t):
+    """Algorithmic HBM bytes of one fused step launch at step t: the decode's
+    bytes with the step-t records read from the caller instead of the arena,
+    plus writing them into the arena, the parents, the parents' rows of
+    h_{t-1} and the new h_t."""
+    s = wl.spec
+    W = s.widths[t]
+    b = decode_alg_bytes(wl, t) - s.R * W * t * 4   # h_t is written, not read
+    b += slab_bytes(wl, t)                          # arena write of the step-t records
+    if t > 0:
+        b += s.R * W * 4                            # parents
+        b += unique_parents(wl, t) * (t - 1) * 4    # parents' rows of h_{t-1}
+        b += s.R * W * t * 4                        # h_t
+    return b
+
+
+def step_alg_bytes(wl, fused=True):
+    """Algorithmic bytes of one whole step (T decode steps; init moves none)."""
+    s = wl.spec
+    total = 0
     for t, W in enumerate(s.widths):
-        slab = s.R * W * (s.HK * s.dk * io + s.HV * (s.dv * io + 8))
-        total += 2 * slab
-        if t > 0:
-            total += s.R * W * 4 + 2 * s.R * W * t * 4
-        total += decode_alg_bytes(wl, t)
+        if fused:
+            total += fused_alg_bytes(wl, t)
+        else:
+            total += 2 * slab_bytes(wl, t) + decode_alg_bytes(wl, t)
+            if t > 0:
+                total += s.R * W * 4 + unique_parents(wl, t) * (t - 1) * 4 + s.R * W * t * 4
     return total
 
 
@@ -121,7 +148,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--batches", type=int, default=16)
+    ap.add_argument("--batches", type=int, default=32)
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--skip-cpu", action="store_true")
@@ -174,74 +201,119 @@ def main():
                     [getattr(st, f) for st in b["steps"] for f in ("q", "k", "v", "alpha", "beta")])
     log(f"[bench] {NB} batches, {footprint / 2**20:.0f} MiB resident")
 
-    def one_step(b, events=None):
+    def init_ctx(b):
+        return ab.onela_init(cfg, b["s0"], b["ws"], ws_bytes, None)
+
+    def one_step(b, fused):
         """init + T x (resolve, append, decode) on the current stream."""
-        ctx = ab.onela_init(cfg, b["s0"], b["ws"], ws_bytes, None)
+        ctx = init_ctx(b)
         for t, st in enumerate(b["steps"]):
-            ab.onela_resolve_ancestry(ctx, t, st.width, st.parents, None)
-            ab.onela_append_records(ctx, t, st.k, st.v, st.alpha, st.beta)
-            if events is not None:
-                events[t][0].record()
-            ab.onela_decode_step(ctx, t, st.q, b["outs"][t])
-            if events is not None:
-                events[t][1].record()
+            if fused:
+                ab.onela_decode_step_fused(ctx, t, st.width, st.parents, st.k, st.v, st.alpha,
+                                           st.beta, st.q, b["outs"][t])
+            else:
+                ab.onela_resolve_ancestry(ctx, t, st.width, st.parents, None)
+                ab.onela_append_records(ctx, t, st.k, st.v, st.alpha, st.beta)
+                ab.onela_decode_step(ctx, t, st.q, b["outs"][t])
         ab.onela_destroy(ctx)
 
-    # ---- capture one graph per batch
-    graphs = None
-    if not args.no_graph:
-        graphs = []
-        for b in batches:
-            one_step(b)  # eager once before capture
+    def capture(fn):
+        fn()  # eager once before capture
         torch.cuda.synchronize()
-        for b in batches:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                one_step(b)
-            graphs.append(g)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
         torch.cuda.synchronize()
+        return g
 
-    def run_steps(n, start):
-        for i in range(n):
-            k = (start + i) % NB
-            if graphs is not None:
-                graphs[k].replay()
-            else:
-                one_step(batches[k])
+    def timed_steps(fused, K, warmup):
+        """Exactly K steps (step i on batch i % NB); returns ms per step."""
+        graphs = None
+        if not args.no_graph:
+            graphs = [capture(lambda b=b: one_step(b, fused)) for b in batches]
 
-    log(f"[bench] warmup {args.warmup}")
-    run_steps(args.warmup, 0)
-    torch.cuda.synchronize()
+        def run(n, start):
+            for i in range(n):
+                k = (start + i) % NB
+                if graphs is not None:
+                    graphs[k].replay()
+                else:
+                    one_step(batches[k], fused)
 
-    # ---- timed region: exactly K steps
+        run(warmup, 0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run(K, warmup)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
     K = args.steps
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_host = time.perf_counter()
-    e0.record()
-    run_steps(K, args.warmup)
-    e1.record()
-    torch.cuda.synchronize()
-    host_s = time.perf_counter() - t_host
-    ms_total = e0.elapsed_time(e1)
-    ms_per_step = ms_total / K
+    log(f"[bench] fused path: warmup {args.warmup}, {K} timed steps")
+    ms_per_step = timed_steps(True, K, args.warmup)
     beam_tokens_per_step = spec.R * sum(spec.widths)
-    value = beam_tokens_per_step * K / (ms_total / 1e3)
-    log(f"[bench] {K} steps: {ms_per_step * 1e3:.1f} us/step (host {host_s / K * 1e6:.1f} us/step)")
+    value = beam_tokens_per_step / (ms_per_step / 1e3)
+    log(f"[bench] fused: {ms_per_step * 1e3:.1f} us/step")
+    ms_sep = timed_steps(False, K, args.warmup)
+    log(f"[bench] separate calls: {ms_sep * 1e3:.1f} us/step")
 
-    # ---- decode-kernel roofline: events around every decode launch (eager)
-    n_roof = max(K // 4, 2 * NB)
+    # ---- dominant-kernel roofline: the fused step kernel.  Per decode step t
+    # one graph holds the fused launches of every batch back to back (batch b
+    # at step t), bracketed by HIP events on the same stream; a batch's data
+    # was last touched NB - 1 launches earlier.
+    ctxs = [None] * NB
+    rs = torch.cuda.Stream()  # contexts bound to the stream the graphs capture
+
+    def init_all():
+        for i, b in enumerate(batches):
+            ctxs[i] = ab.onela_init(cfg, b["s0"], b["ws"], ws_bytes, rs)
+
+    def fused_all(t):
+        for i, b in enumerate(batches):
+            st = b["steps"][t]
+            ab.onela_decode_step_fused(ctxs[i], t, st.width, st.parents, st.k, st.v,
+                                       st.alpha, st.beta, st.q, b["outs"][t])
+
+    # Graphs hold kernel arguments by value, so each one is captured with the
+    # host-side contexts already advanced to the step it replays; replaying
+    # g_init and then step_graphs[0..T-1] redoes the whole sequence on device.
+    def capture_on_rs(fn):
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=rs):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    g_init = capture_on_rs(init_all)
+    for c in ctxs:
+        ab.onela_destroy(c)
+    step_graphs = []
+    for t in range(T):
+        with torch.cuda.stream(rs):
+            init_all()
+            for tt in range(t):
+                fused_all(tt)
+        step_graphs.append(capture_on_rs(lambda t=t: fused_all(t)))
+        for c in ctxs:
+            ab.onela_destroy(c)
+    torch.cuda.synchronize()
+    n_roof = max(4, args.steps // 20)
     dec_ms = np.zeros((n_roof, T))
     for i in range(n_roof):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(T)]
-        one_step(batches[i % NB], ev)
+        g_init.replay()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
+        ev[0].record()
+        for t in range(T):
+            step_graphs[t].replay()
+            ev[t + 1].record()
         torch.cuda.synchronize()
-        dec_ms[i] = [a.elapsed_time(b) for a, b in ev]
-    dec_us = dec_ms[NB // 2:].mean(axis=0) * 1e3  # drop the first rotation
-    bytes_t = [decode_alg_bytes(wl, t) for t in range(T)]
+        dec_ms[i] = [ev[t].elapsed_time(ev[t + 1]) / NB for t in range(T)]
+    dec_us = dec_ms[1:].mean(axis=0) * 1e3
+    bytes_t = [fused_alg_bytes(wl, t) for t in range(T)]
     achieved = sum(bytes_t) / (dec_us.sum() * 1e-6) / 1e9
-    log(f"[bench] decode us per t: {np.round(dec_us, 2).tolist()}  "
+    log(f"[bench] fused kernel us per t: {np.round(dec_us, 2).tolist()}  "
         f"alg MB: {[round(b / 1e6, 2) for b in bytes_t]}  -> {achieved:.0f} GB/s")
 
     result = {
@@ -261,16 +333,25 @@ def main():
                    "v_heads": spec.HV, "d_k": spec.dk, "d_v": spec.dv, "prompt": spec.P,
                    "beams": spec.W, "decode_steps": T, "io_dtype": spec.io_dtype,
                    "parents": f"{spec.parents}{spec.zipf_s if spec.parents == 'zipf' else ''}",
-                   "step": "init + per t (resolve_ancestry, append_records, decode_step)",
-                   "contraction": "S_ctx.P on bf16 MFMA, hi/lo split, 3 products, fp32 accum",
-                   "graph": graphs is not None, "batches": NB},
+                   "step": "onela_init + per t onela_decode_step_fused (resolve + append "
+                           "+ decode in one launch)",
+                   "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
+                                  "fp32 accum",
+                   "graph": not args.no_graph, "batches": NB},
         "decode_step_us": {"per_t": [round(float(x), 3) for x in dec_us],
                            "mean": round(float(dec_us.mean()), 3)},
         "beam_tokens_per_step": beam_tokens_per_step,
-        "step_alg_bytes": step_alg_bytes(wl),
+        "step_alg_bytes": step_alg_bytes(wl, fused=True),
+        "separate_calls": {"ms_per_step": ms_sep,
+                           "beam_tokens_per_s": beam_tokens_per_step / (ms_sep / 1e3),
+                           "step": "onela_init + per t (resolve_ancestry, append_records, "
+                                   "decode_step)",
+                           "step_alg_bytes": step_alg_bytes(wl, fused=False)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "decode_kernel", "alg_bytes_per_t": bytes_t},
+                     "kernel": "decode_kernel<FUSED>", "alg_bytes_per_t": bytes_t,
+                     "us_per_t": [round(float(x), 3) for x in dec_us],
+                     "timing": f"HIP events around {NB} back-to-back launches per t"},
     }
 
     # ---- per-beam FullState GPU baseline
@@ -292,7 +373,7 @@ def main():
             "ms_per_step": fs_ms, "unit": "ms per T-step decode (all beams, all heads)",
             "beam_tokens_per_s": beam_tokens_per_step / (fs_ms / 1e3),
             "speedup_whole_step": fs_ms / ms_per_step,
-            "speedup_decode_kernels": fs_ms / (dec_us.sum() / 1e3)}
+            "speedup_fused_kernels": fs_ms / (dec_us.sum() / 1e3)}
         log(f"[bench] fullstate baseline {fs_ms:.3f} ms/step")
         del base
 

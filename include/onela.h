@@ -80,16 +80,19 @@ const char* onela_status_str(onela_status_t status);
 onela_status_t onela_check_config(const onela_config_t* cfg);
 
 /* Bytes of device workspace onela_init needs for cfg (0 if cfg is invalid).
- * Layout: status word, double-buffered ancestry index [2][R][W_max][T_max]
- * int32, the split shared state (2 x bf16 per element of S_ctx), and the
- * record arena: k [R][T_max][H_K][W_max][d_k], v [R][T_max][H_V][W_max][d_v]
- * in the io dtype and (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs. */
+ * Layout (each part 256-byte aligned): status word, double-buffered ancestry
+ * index [2][R][W_max][T_max] int32, S_ctx split into bf16 high/low halves
+ * (written by the step-0 launch, read by later steps), and the record arena:
+ * k [R][T_max][H_K][W_max][d_k], v [R][T_max][H_V][W_max][d_v] in the io
+ * dtype and (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs. */
 size_t onela_workspace_bytes(const onela_config_t* cfg);
 
 /* Creates a decode context and binds the shared post-prefill state
  * (Sec. 3.1: S_ctx is stored once per request and shared by all beams).
- *   s0        device, fp32 [R][H_V][d_v][d_k]; read only during this call
- *             (it is split into bf16 high/low halves inside the workspace)
+ * Host bookkeeping only: nothing is enqueued.
+ *   s0        device, fp32 [R][H_V][d_v][d_k]; borrowed until onela_destroy
+ *             (read by the step-0 launch of every beam search), owned by the
+ *             caller
  *   workspace device, >= onela_workspace_bytes(cfg), 256-byte aligned;
  *             borrowed until onela_destroy, owned by the caller
  *   stream    a hipStream_t (NULL: the default stream)
@@ -149,8 +152,25 @@ onela_status_t onela_append_records(onela_ctx_t ctx, int32_t step,
 onela_status_t onela_decode_step(onela_ctx_t ctx, int32_t step, const void* q,
                                  float* o);
 
+/* One whole decode step in a single launch: the ancestry update of
+ * onela_resolve_ancestry, the record append of onela_append_records and the
+ * read-out of onela_decode_step (Sec. 3.4 describes fusing the context
+ * projection, ancestry replay, current update and record append into one
+ * kernel).  Arguments have the meaning, layout and ownership given for those
+ * three calls; on success the context is in the same state as after them,
+ * so the two forms may be mixed from step to step.  Must be called for the
+ * next step (0 after init/reset).  A bad parent is handled as in
+ * onela_resolve_ancestry.
+ * Errors: ONELA_EINVAL, ONELA_ESTEP, ONELA_ECAPACITY, ONELA_EHIP. */
+onela_status_t onela_decode_step_fused(onela_ctx_t ctx, int32_t step, int32_t width,
+                                       const int32_t* parents, const void* k,
+                                       const void* v, const float* alpha,
+                                       const float* beta, const void* q, float* o,
+                                       int32_t* gather_out);
+
 /* Synchronises the context's stream, returns and clears the sticky device
- * error (ONELA_OK or ONELA_EPARENT), or ONELA_EHIP. */
+ * error (ONELA_OK or ONELA_EPARENT), or ONELA_EHIP.  The error covers the
+ * current beam search: the step-0 launch of each search zeroes it. */
 onela_status_t onela_get_device_status(onela_ctx_t ctx);
 
 /* Frees the host-side context (the workspace stays the caller's). */

@@ -12,6 +12,11 @@ namespace onela {
 // Maximum records in one beam's chain (decode steps 0 .. kMaxSteps-1).
 constexpr int kMaxSteps = 8;
 
+// Decode tiling: MFMA row blocks (16 state rows each) per wave and 16-beam
+// MFMA column blocks per workgroup.
+constexpr int kDecodeRowBlocks = 1;
+constexpr int kDecodeBeamBlocks = 2;
+
 // Bits of the sticky device status word.
 constexpr int kStatusParent = 1;
 
@@ -26,7 +31,8 @@ struct Shape {
 struct Arena {
   int* status;       // sticky error bits
   int* anc[2];       // ancestry h_t, [R][wmax][tmax] int32, buffer t % 2
-  uint16_t* s_frag;  // S_ctx split into bf16 hi/lo, MFMA fragment order
+  const float* s0;   // S_ctx fp32 [R][HV][dv][dk], borrowed from the caller
+  uint16_t* s_frag;  // S_ctx as bf16 hi/lo in MFMA A-fragment order (from step 0)
   void* k;           // [R][tmax][HK][wmax][dk] io dtype
   void* v;           // [R][tmax][HV][wmax][dv] io dtype
   float2* ab;        // [R][tmax][HV][wmax] (alpha, beta)
@@ -40,8 +46,6 @@ Layout layout_of(const Shape& s);
 
 // ---- launchers (each returns hipGetLastError() after the launch) ---------
 hipError_t launch_clear_status(int* status, hipStream_t st);
-hipError_t launch_split_state(const Shape& s, const float* s0, uint16_t* frag,
-                              hipStream_t st);
 hipError_t launch_resolve(const Shape& s, int step, int width, int prev_width,
                           const int* parents, const int* anc_prev, int* anc_cur,
                           int* gather_out, int* status, hipStream_t st);
@@ -50,6 +54,10 @@ hipError_t launch_append(const Shape& s, int step, int width, const void* k,
                          const Arena& a, hipStream_t st);
 hipError_t launch_decode(const Shape& s, int step, int width, const void* q,
                          float* o, const Arena& a, hipStream_t st);
+hipError_t launch_fused_step(const Shape& s, int step, int width, int prev_width,
+                             const int* parents, const void* k, const void* v,
+                             const float* alpha, const float* beta, const void* q, float* o,
+                             int* gather_out, const Arena& a, hipStream_t st);
 hipError_t launch_prefill(const Shape& s, int prompt_len, const void* k,
                           const void* v, const float* alpha, const float* beta,
                           float* s0_out, hipStream_t st);

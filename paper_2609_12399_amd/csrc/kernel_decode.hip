@@ -1,4 +1,4 @@
-// Fused large-beam GDN decode step for gfx950 (CDNA4).
+// Large-beam GDN decode step for gfx950 (CDNA4).
 //
 // For every request r, value head hv and live beam b, with the chain of
 // records (k_j, v_j, alpha_j, beta_j) at slots h_t(b, 0..t-1) of steps
@@ -10,26 +10,47 @@
 //     p <- q;  for j = t..0:  c = k_j . p;  g_j = beta_j c;
 //                             o += g_j v_j;  p <- alpha_j (p - g_j k_j)
 //     o += S_ctx p,
-// gives S_{t,b} q exactly (in exact arithmetic).  The only d_v x d_k work is
-// the final S_ctx p, which is a dense GEMM over all beams of a head:
-// O_h = S_ctx[h] . [p_1 .. p_W].  That contraction runs on MFMA; the fold and
-// the v-terms are vector work with 16-byte loads.
+// gives S_{t,b} q exactly (in exact arithmetic).  The fold is carried in
+// scaled form p = s p~ with s the running product of the alphas, so each
+// step costs one dot product and one axpy per element (p~ -= beta_j c~ k_j,
+// c~ = k_j . p~, g_j = s beta_j c~, s *= alpha_j; alpha_j = 0 simply zeroes
+// s).  The only d_v x d_k work is the final S_ctx p, a dense GEMM over all
+// beams of a head, O_h = S_ctx[h] . [p_1 .. p_W], which runs on MFMA; the
+// fold and the v-terms are vector work with 16-byte loads.
 //
-// Precision.  S_ctx is split once (at init) into bf16 hi + lo, p is split the
-// same way in registers, and O = S_hi P_hi + S_hi P_lo + S_lo P_hi is
+// Precision.  S_ctx (fp32) and p are split into bf16 hi + lo
+// (hi = bf16(x), lo = bf16(x - hi)), and O = S_hi P_hi + S_hi P_lo + S_lo P_hi is
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16 (about 16 significant bits
 // per product; the dropped S_lo P_lo term is ~2^-17 relative).
 //
 // Work decomposition.  One workgroup = (request, value head, 16*NBLK beams),
-// DV/32 waves.  Phase 1 (fold): LPB lanes per beam, each owning EPL
-// consecutive key elements; dot products are reduced across those lanes.
-// The folded queries are written, split into hi/lo, to LDS directly in MFMA
-// B-fragment order; the fold scalars g_j go to LDS too.  Phase 2 (contract):
-// wave w multiplies its 32 state rows (A fragments streamed from the
-// fragment-ordered split state, issued before the fold so they overlap it)
-// by the beams' B fragments.  Phase 3 (epilogue): each lane holds 8
-// consecutive output rows of one beam, adds sum_j g_j v_j[rows] (v prefetched
-// at kernel start) and stores 32 contiguous bytes.
+// DV/(16*MB) waves.  Phase 1 (fold): LPB lanes per beam, each owning EPL
+// consecutive key elements; dot products are reduced across those lanes with
+// DPP.  The folded queries are written, split into hi/lo, to LDS directly in
+// MFMA B-fragment order; the fold scalars g_j go to LDS too.  Phase 2
+// (contract): wave w multiplies its 16*MB state rows (A fragments: split in
+// registers from fp32 S_ctx at step 0, stored split in the workspace for
+// later steps) by the beams' B fragments.  Phase 3
+// (epilogue): each lane holds 4*MB consecutive output rows of one beam, adds
+// sum_j g_j v_j[rows] and stores them as 16-byte vectors.
+//
+// Why 32 beams and 16 rows per wave: every workgroup streams its head's
+// whole shared state (64 KiB at d = 128) through the CU's vector memory pipe
+// as MFMA A fragments, which is most of a CU's traffic; one 512-thread
+// workgroup per CU covering 32 beams moves half the state bytes per beam of
+// two 16-beam workgroups at the same occupancy.
+//
+// Two modes share the kernel.  DECODE reads h_t and the step-t records from
+// the context (after onela_resolve_ancestry and onela_append_records).
+// FUSED performs the whole step in one launch: it reads the parents and the
+// previous index h_{t-1} (Eq. 5: h_t(b, j) = h_{t-1}(pi(b), j), h_t(b, t-1) =
+// pi(b)), reads the step-t records from the caller's buffers, writes them
+// into the arena slab t (workgroups of value head 0 write h_t, those of the
+// first value head of each group write k), and decodes.
+//
+// Loads are issued in the order they are waited for (the vector memory
+// counter retires in order): indices first, then everything that does not
+// depend on them, then the ancestral records once the indices are back.
 //
 // Block order is XCD-aware: workgroups are dispatched round-robin over the 8
 // XCDs, so block id i runs on XCD i % 8; all beam tiles of a (request, head)
@@ -46,47 +67,78 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 struct DecodeParams {
   const void* q;
   float* o;
-  const uint4* s_frag;
-  const void* ak;
-  const void* av;
-  const float2* ab;
-  const int* anc;
-  int R, HK, HV, W, wmax, tmax;
+  // FUSED only: the step's inputs from the caller
+  const int* parents;
+  const void* k_in;
+  const void* v_in;
+  const float* alpha_in;
+  const float* beta_in;
+  int* gather_out;
+  int* status;
+  // context
+  const float* s0;  // shared state S_ctx, fp32 [R*HV][DV][DK] (read at step 0)
+  uint4* s_frag;    // S_ctx split into bf16 hi/lo, A-fragment order (written at step 0)
+  void* ak;
+  void* av;
+  float2* ab;
+  const int* anc_rd;  // h_t (DECODE) or h_{t-1} (FUSED)
+  int* anc_wr;        // FUSED: h_t
+  int R, HK, HV, G, W, W_prev, wmax, tmax;
   int ntiles;   // beam tiles per (request, value head)
   int xcd_map;  // 1: XCD-aware block order (units % 8 == 0)
 };
 
-// 8 consecutive io elements, raw.
-template <bool BF16>
-struct Raw8;
-template <>
-struct Raw8<true> {
-  uint4 u;
-  __device__ void load(const void* base, long elem) {
-    u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
+// Pointer to a byte offset from a base (32-bit offsets keep per-lane address
+// arithmetic in 32 bits; every region is smaller than 2 GiB).
+template <typename T>
+__device__ inline T* at(void* base, unsigned off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+__device__ inline const T* at(const void* base, unsigned off) {
+  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+// N consecutive io elements (bf16 bits or fp32), raw, moved as whole
+// vectors of 8, 16 or 32 bytes.
+template <bool BF16, int N>
+struct RawV {
+  static constexpr int kWords = BF16 ? N / 2 : N;
+  static constexpr int kBytes = kWords * 4;
+  static_assert(kWords == 2 || kWords == 4 || kWords == 8, "8, 16 or 32 bytes");
+  unsigned w[kWords];
+  __device__ void load(const void* base, unsigned off) {
+    if constexpr (kWords == 2) {
+      const uint2 u = *at<uint2>(base, off);
+      w[0] = u.x; w[1] = u.y;
+    } else {
+#pragma unroll
+      for (int i = 0; i < kWords / 4; ++i) {
+        const uint4 u = *at<uint4>(base, off + 16 * i);
+        w[4 * i] = u.x; w[4 * i + 1] = u.y; w[4 * i + 2] = u.z; w[4 * i + 3] = u.w;
+      }
+    }
+  }
+  __device__ void store(void* base, unsigned off) const {
+    if constexpr (kWords == 2) {
+      *at<uint2>(base, off) = make_uint2(w[0], w[1]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < kWords / 4; ++i)
+        *at<uint4>(base, off + 16 * i) =
+            make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
+    }
   }
   __device__ void to_float(float* x) const {
-    x[0] = __uint_as_float(u.x << 16);
-    x[1] = __uint_as_float(u.x & 0xffff0000u);
-    x[2] = __uint_as_float(u.y << 16);
-    x[3] = __uint_as_float(u.y & 0xffff0000u);
-    x[4] = __uint_as_float(u.z << 16);
-    x[5] = __uint_as_float(u.z & 0xffff0000u);
-    x[6] = __uint_as_float(u.w << 16);
-    x[7] = __uint_as_float(u.w & 0xffff0000u);
-  }
-};
-template <>
-struct Raw8<false> {
-  float4 a, b;
-  __device__ void load(const void* base, long elem) {
-    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(base) + elem);
-    a = p[0];
-    b = p[1];
-  }
-  __device__ void to_float(float* x) const {
-    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+#pragma unroll
+    for (int i = 0; i < kWords; ++i) {
+      if constexpr (BF16) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+      } else {
+        x[i] = __uint_as_float(w[i]);
+      }
+    }
   }
 };
 
@@ -110,20 +162,45 @@ __device__ inline void split8(const float* x, uint4& hi, uint4& lo) {
   lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
+template <int CTRL>
+__device__ inline float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
+                                                               CTRL, 0xF, 0xF, false));
+}
+
+// Sum over an aligned group of G consecutive lanes, result in every lane of
+// the group.  Within a 16-lane row the exchanges are DPP moves: swap
+// neighbours, swap pairs (quad permutes), then mirror within half-rows and
+// within the row; wider groups finish with cross-row shuffles.
+template <int G>
+__device__ inline float group_sum(float x) {
+  if constexpr (G >= 2) x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  if constexpr (G >= 4) x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  if constexpr (G >= 8) x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (G >= 16) x += dpp<0x140>(x); // row_mirror
+  if constexpr (G >= 32) x += __shfl_xor(x, 16);
+  if constexpr (G >= 64) x += __shfl_xor(x, 32);
+  return x;
+}
+
 __device__ inline f32x4 mfma_bf16(const uint4& a, const uint4& b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <int DK, int DV, int NBLK, int CHAIN, bool BF16>
-__global__ __launch_bounds__(DV * 2) void decode_kernel(DecodeParams p) {
-  constexpr int NW = DV / 32;        // waves per workgroup
+template <int DK, int DV, int MB, int NBLK, int CHAIN, bool BF16, bool FUSED>
+__global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
+  constexpr int NW = DV / (16 * MB); // waves per workgroup (16*MB state rows each)
+  constexpr int RPL = 4 * MB;        // consecutive output rows per epilogue lane
   constexpr int NT = NW * 64;        // threads per workgroup
   constexpr int BEAMS = 16 * NBLK;   // beams per workgroup
   constexpr int LPB = NT / BEAMS;    // fold lanes per beam
   constexpr int EPL = DK / LPB;      // key elements per fold lane
   constexpr int C8 = EPL / 8;        // 8-element chunks per fold lane
   constexpr int KS = DK / 32;        // MFMA k-steps
+  constexpr int NA = CHAIN - 1;      // ancestral records (= step t)
+  constexpr int NAX = NA > 0 ? NA : 1;
+  constexpr unsigned IOB = BF16 ? 2 : 4;
   static_assert(EPL % 8 == 0 && EPL >= 8, "fold lanes must own 8-element chunks");
   static_assert(LPB <= 64 && (LPB & (LPB - 1)) == 0, "fold lane group within a wave");
 
@@ -133,6 +210,12 @@ __global__ __launch_bounds__(DV * 2) void decode_kernel(DecodeParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+
+  // A new beam search starts at step 0: no parent can be flagged yet, so the
+  // step-0 launch zeroes the sticky status word.
+  if constexpr (NA == 0) {
+    if (blockIdx.x == 0 && tid == 0) p.status[0] = 0;
+  }
 
   int unit, tile;
   if (p.xcd_map) {
@@ -145,130 +228,253 @@ __global__ __launch_bounds__(DV * 2) void decode_kernel(DecodeParams p) {
   }
   const int r = unit / p.HV;
   const int hv = unit - r * p.HV;
-  const int hk = hv / (p.HV / p.HK);
+  const int hk = hv / p.G;
   const int b0 = tile * BEAMS;
   const int W = p.W;
+  const int wmax = p.wmax, tmax = p.tmax;
 
-  // ---- A fragments of this wave's 32 state rows (independent of the beams)
-  uint4 A[KS][2][2];
-  {
-    const uint4* sf = p.s_frag + (long(unit) * NW + w) * (KS * 4 * 64) + lane;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int hl = 0; hl < 2; ++hl) A[ks][mb][hl] = sf[((ks * 2 + mb) * 2 + hl) * 64];
-  }
-
-  // ---- fold-phase lane mapping and chain slots
+  // fold lanes: beam fb of the tile, key elements [li*EPL, li*EPL + EPL)
   const int fb = tid / LPB;
   const int li = tid - fb * LPB;
   const int fbeam = b0 + fb;
-  const int fbc = fbeam < W ? fbeam : 0;
-  int fslot[CHAIN];
-  bool fok[CHAIN];
-  {
-    const int* arow = p.anc + (long(r) * p.wmax + fbc) * p.tmax;
-#pragma unroll
-    for (int j = 0; j < CHAIN - 1; ++j) {
-      const int s = arow[j];
-      fok[j] = unsigned(s) < unsigned(p.wmax);
-      fslot[j] = fok[j] ? s : 0;
-    }
-    fslot[CHAIN - 1] = fbc;
-    fok[CHAIN - 1] = true;
-  }
-
-  // ---- epilogue lane mapping and chain slots (one beam per lane and block)
-  const int g4 = lane >> 4;  // 8-row group of this lane within the wave's rows
-  int sslot[NBLK][CHAIN];
+  const bool fvalid = fbeam < W;
+  const int fbc = fvalid ? fbeam : 0;
+  // epilogue lanes: beam (lane & 15) of block nb, rows row0 + [0, RPL)
+  const int g4 = lane >> 4;
+  const unsigned row0 = 16 * MB * w + RPL * g4;
+  int sbc[NBLK];
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
     const int sb = b0 + nb * 16 + (lane & 15);
-    const int sbc = sb < W ? sb : 0;
-    const int* arow = p.anc + (long(r) * p.wmax + sbc) * p.tmax;
-#pragma unroll
-    for (int j = 0; j < CHAIN - 1; ++j) {
-      const int s = arow[j];
-      sslot[nb][j] = unsigned(s) < unsigned(p.wmax) ? s : 0;
-    }
-    sslot[nb][CHAIN - 1] = sbc;
+    sbc[nb] = sb < W ? sb : 0;
   }
 
-  // ---- issue every beam-side load up front
-  Raw8<BF16> qr[C8];
-  Raw8<BF16> kr[CHAIN][C8];
+  // uniform bases (per workgroup)
+  const int* anc_r = p.anc_rd + long(r) * wmax * tmax;
+  const unsigned kslot = DK * IOB, vslot = DV * IOB;
+  auto k_slab = [&](int j) {  // arena k rows of (r, j, hk)
+    return static_cast<char*>(p.ak) + ((long(r) * tmax + j) * p.HK + hk) * wmax * long(kslot);
+  };
+  auto v_slab = [&](int j) {
+    return static_cast<char*>(p.av) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
+  };
+  auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
+
+  // ---- round 1: indices (parents in FUSED mode, h_t otherwise)
+  int fsrc[NAX], ssrc[NBLK][NAX];
+  bool fpok = true, spok[NBLK];
+  int fpar = 0, spar[NBLK];
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) spok[nb] = true;
+  if constexpr (NA > 0) {
+    if constexpr (FUSED) {
+      const int* prow = p.parents + long(r) * W;
+      fpar = prow[fbc];
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) spar[nb] = prow[sbc[nb]];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+        for (int j = 0; j < NA; ++j) ssrc[nb][j] = anc_r[sbc[nb] * tmax + j];
+    }
+  }
+
+  // ---- loads that need no index: query, the step-t record, shared state
+  using K8 = RawV<BF16, 8>;
+  using VR = RawV<BF16, RPL>;
+  K8 qr[C8];
+  K8 kr[CHAIN][C8];
   float2 abr[CHAIN];
-  Raw8<BF16> vr[NBLK][CHAIN];
+  VR vr[NBLK][CHAIN];
   {
-    const long qbase = ((long(r) * W + fbc) * p.HK + hk) * DK + li * EPL;
+    const unsigned qoff = ((unsigned(r) * W + fbc) * p.HK + hk) * kslot + li * EPL * IOB;
 #pragma unroll
-    for (int c = 0; c < C8; ++c) qr[c].load(p.q, qbase + 8 * c);
+    for (int c = 0; c < C8; ++c) qr[c].load(p.q, qoff + c * K8::kBytes);
+    if constexpr (FUSED) {
 #pragma unroll
-    for (int j = 0; j < CHAIN; ++j) {
-      const long slab = long(r) * p.tmax + j;
-      const long kbase = ((slab * p.HK + hk) * p.wmax + fslot[j]) * DK + li * EPL;
+      for (int c = 0; c < C8; ++c) kr[NA][c].load(p.k_in, qoff + c * K8::kBytes);
+      const unsigned gi = (unsigned(r) * W + fbc) * p.HV + hv;
+      abr[NA] = make_float2(p.alpha_in[gi], p.beta_in[gi]);
 #pragma unroll
-      for (int c = 0; c < C8; ++c) kr[j][c].load(p.ak, kbase + 8 * c);
-      abr[j] = p.ab[(slab * p.HV + hv) * p.wmax + fslot[j]];
+      for (int nb = 0; nb < NBLK; ++nb)
+        vr[nb][NA].load(p.v_in, ((unsigned(r) * W + sbc[nb]) * p.HV + hv) * vslot + row0 * IOB);
+    } else {
+      const char* ks = k_slab(NA);
+#pragma unroll
+      for (int c = 0; c < C8; ++c)
+        kr[NA][c].load(ks, fbc * kslot + li * EPL * IOB + c * K8::kBytes);
+      abr[NA] = ab_slab(NA)[fbc];
+      const char* vs = v_slab(NA);
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) vr[nb][NA].load(vs, sbc[nb] * vslot + row0 * IOB);
     }
+  }
+  // This wave's shared-state rows in MFMA A-fragment order: lane l holds
+  // row 16 MB w + 4 MB (m/4) + 4 mb + (m%4) (m = l % 16) and columns
+  // 32 ks + 8 (l/16) + [0, 8); the row permutation makes a lane's
+  // accumulator rows consecutive state rows.  Step 0 reads fp32 S_ctx and
+  // splits it into bf16 hi/lo in registers (and tile-0 workgroups store the
+  // split fragments in the workspace); later steps read the stored
+  // fragments, 1 KiB contiguous per wave-wide load.
+  float4 Araw[NA == 0 ? KS : 1][MB][2];
+  uint4 A[KS][MB][2];
+  uint4* const frag = p.s_frag + (long(unit) * NW + w) * (KS * MB * 2 * 64) + lane;
+  if constexpr (NA == 0) {
+    const int m = lane & 15;
 #pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int j = 0; j < CHAIN; ++j) {
-        const long slab = long(r) * p.tmax + j;
-        vr[nb][j].load(p.av, ((slab * p.HV + hv) * p.wmax + sslot[nb][j]) * DV + 32 * w + 8 * g4);
+      for (int mb = 0; mb < MB; ++mb) {
+        const unsigned row = 16 * MB * w + 4 * MB * (m >> 2) + 4 * mb + (m & 3);
+        const unsigned col = 32 * ks + 8 * (lane >> 4);
+        const unsigned off = ((unsigned(unit) * DV + row) * DK + col) * 4u;
+        Araw[ks][mb][0] = *at<float4>(p.s0, off);
+        Araw[ks][mb][1] = *at<float4>(p.s0, off + 16);
       }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int hl = 0; hl < 2; ++hl) A[ks][mb][hl] = frag[((ks * MB + mb) * 2 + hl) * 64];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- round 2 (FUSED): the parents' rows of h_{t-1}
+  if constexpr (FUSED && NA > 0) {
+    fpok = unsigned(fpar) < unsigned(p.W_prev);
+    const int pf = fpok ? fpar : 0;
+#pragma unroll
+    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+    fsrc[NA - 1] = pf;
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
+      const int ps = spok[nb] ? spar[nb] : 0;
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps * tmax + j];
+      ssrc[nb][NA - 1] = ps;
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
 
-  // ---- phase 1: fold the query newest -> oldest
-  float pv[EPL];
+  // ---- ancestral records
+  bool fok[CHAIN];
+  fok[NA] = true;
 #pragma unroll
-  for (int c = 0; c < C8; ++c) qr[c].to_float(pv + 8 * c);
+  for (int j = 0; j < NA; ++j) {
+    fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
+    const int slot = fok[j] ? fsrc[j] : 0;
+    const char* ks = k_slab(j);
 #pragma unroll
-  for (int j = CHAIN - 1; j >= 0; --j) {
+    for (int c = 0; c < C8; ++c)
+      kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
+    abr[j] = ab_slab(j)[slot];
+  }
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
+      vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+    }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 1: fold the query newest -> oldest (scaled form)
+  float pt[EPL];
+#pragma unroll
+  for (int c = 0; c < C8; ++c) qr[c].to_float(pt + 8 * c);
+  float scale = 1.f;
+#pragma unroll
+  for (int j = NA; j >= 0; --j) {
     float kf[EPL];
 #pragma unroll
     for (int c = 0; c < C8; ++c) kr[j][c].to_float(kf + 8 * c);
     float c0 = 0.f, c1 = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; e += 2) {
-      c0 = fmaf(kf[e], pv[e], c0);
-      c1 = fmaf(kf[e + 1], pv[e + 1], c1);
+      c0 = fmaf(kf[e], pt[e], c0);
+      c1 = fmaf(kf[e + 1], pt[e + 1], c1);
     }
-    float cdot = c0 + c1;
-#pragma unroll
-    for (int m = 1; m < LPB; m <<= 1) cdot += __shfl_xor(cdot, m);
+    const float cdot = group_sum<LPB>(c0 + c1);
     const float alpha = fok[j] ? abr[j].x : 1.f;
     const float beta = fok[j] ? abr[j].y : 0.f;
-    const float gj = beta * cdot;
-    if (li == 0) g_lds[fb][j] = gj;
+    const float gt = beta * cdot;
+    if (li == 0) g_lds[fb][j] = scale * gt;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) pv[e] = alpha * fmaf(-gj, kf[e], pv[e]);
+    for (int e = 0; e < EPL; ++e) pt[e] = fmaf(-gt, kf[e], pt[e]);
+    scale *= alpha;
   }
 #pragma unroll
   for (int c = 0; c < C8; ++c) {
     const int k0 = li * EPL + 8 * c;
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = scale * pt[8 * c + e];
     uint4 hi, lo;
-    split8(pv + 8 * c, hi, lo);
+    split8(x, hi, lo);
     p_lds[0][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = hi;
     p_lds[1][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = lo;
+  }
+
+  // ---- FUSED: index h_t and the step-t record into the context
+  if constexpr (FUSED) {
+    if (fvalid) {
+      if (hv == 0 && li == 0 && NA > 0) {
+        int* dst = p.anc_wr + (long(r) * wmax + fbeam) * tmax;
+        int* g = p.gather_out ? p.gather_out + (long(r) * W + fbeam) * NA : nullptr;
+#pragma unroll
+        for (int j = 0; j < NA; ++j) {
+          const int h = fpok ? fsrc[j] : -1;
+          dst[j] = h;
+          if (g) g[j] = h;
+        }
+        if (!fpok) atomicOr(p.status, kStatusParent);
+      }
+      if (hv % p.G == 0) {
+        char* ks = k_slab(NA);
+#pragma unroll
+        for (int c = 0; c < C8; ++c)
+          kr[NA][c].store(ks, fbeam * kslot + li * EPL * IOB + c * K8::kBytes);
+      }
+      if (li == 0) ab_slab(NA)[fbeam] = abr[NA];
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+      if (b0 + nb * 16 + (lane & 15) < W) vr[nb][NA].store(v_slab(NA), sbc[nb] * vslot + row0 * IOB);
   }
   __syncthreads();
 
   // ---- phase 2: O = S_ctx . P on MFMA (three bf16 products per block)
-  f32x4 acc[NBLK][2];
+  if constexpr (NA == 0) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float x[8] = {Araw[ks][mb][0].x, Araw[ks][mb][0].y, Araw[ks][mb][0].z,
+                            Araw[ks][mb][0].w, Araw[ks][mb][1].x, Araw[ks][mb][1].y,
+                            Araw[ks][mb][1].z, Araw[ks][mb][1].w};
+        split8(x, A[ks][mb][0], A[ks][mb][1]);
+        if (tile == 0)
+#pragma unroll
+          for (int hl = 0; hl < 2; ++hl) frag[((ks * MB + mb) * 2 + hl) * 64] = A[ks][mb][hl];
+      }
+  }
+  f32x4 acc[NBLK][MB];
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
-    acc[nb][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-    acc[nb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const uint4 bh = p_lds[0][nb][ks][g4][lane & 15];
       const uint4 bl = p_lds[1][nb][ks][g4][lane & 15];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < MB; ++mb) {
         acc[nb][mb] = mfma_bf16(A[ks][mb][1], bh, acc[nb][mb]);
         acc[nb][mb] = mfma_bf16(A[ks][mb][0], bl, acc[nb][mb]);
         acc[nb][mb] = mfma_bf16(A[ks][mb][0], bh, acc[nb][mb]);
@@ -276,38 +482,39 @@ __global__ __launch_bounds__(DV * 2) void decode_kernel(DecodeParams p) {
     }
   }
 
-  // ---- phase 3: add the v-terms and store 8 consecutive rows per lane
+  // ---- phase 3: add the v-terms and store RPL consecutive rows per lane
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
     const int bl = nb * 16 + (lane & 15);
     const int sb = b0 + bl;
-    float ov[8];
+    float ov[RPL];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ov[e] = acc[nb][e >> 2][e & 3];
+    for (int e = 0; e < RPL; ++e) ov[e] = acc[nb][e >> 2][e & 3];
 #pragma unroll
     for (int j = 0; j < CHAIN; ++j) {
       const float gj = g_lds[bl][j];
-      float vf[8];
+      float vf[RPL];
       vr[nb][j].to_float(vf);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ov[e] = fmaf(gj, vf[e], ov[e]);
+      for (int e = 0; e < RPL; ++e) ov[e] = fmaf(gj, vf[e], ov[e]);
     }
     if (sb < W) {
-      float4* dst = reinterpret_cast<float4*>(p.o + ((long(r) * W + sb) * p.HV + hv) * DV +
-                                              32 * w + 8 * g4);
-      dst[0] = make_float4(ov[0], ov[1], ov[2], ov[3]);
-      dst[1] = make_float4(ov[4], ov[5], ov[6], ov[7]);
+      float4* dst = at<float4>(p.o, (((unsigned(r) * W + sb) * p.HV + hv) * DV + row0) * 4u);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+        dst[i] = make_float4(ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]);
     }
   }
 }
 
-template <int D, int NBLK, bool BF16>
+template <int D, int NBLK, bool BF16, bool FUSED>
 hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hipStream_t st) {
-  constexpr int threads = D * 2;
+  constexpr int MB = kDecodeRowBlocks;
+  constexpr int threads = 4 * D / MB;
   switch (chain) {
-#define ONELA_CHAIN_CASE(C)                                                          \
-  case C:                                                                           \
-    decode_kernel<D, D, NBLK, C, BF16><<<blocks, threads, 0, st>>>(prm);            \
+#define ONELA_CHAIN_CASE(C)                                                        \
+  case C:                                                                         \
+    decode_kernel<D, D, MB, NBLK, C, BF16, FUSED><<<blocks, threads, 0, st>>>(prm); \
     break;
     ONELA_CHAIN_CASE(1)
     ONELA_CHAIN_CASE(2)
@@ -324,6 +531,49 @@ hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hip
   return hipGetLastError();
 }
 
+template <bool FUSED>
+hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsigned blocks,
+                       hipStream_t st) {
+  constexpr int NBLK = kDecodeBeamBlocks;
+  const int chain = step + 1;
+  if (s.dk == 128)
+    return s.bf16 ? launch_chain<128, NBLK, true, FUSED>(chain, prm, blocks, st)
+                  : launch_chain<128, NBLK, false, FUSED>(chain, prm, blocks, st);
+  if (s.dk == 64)
+    return s.bf16 ? launch_chain<64, NBLK, true, FUSED>(chain, prm, blocks, st)
+                  : launch_chain<64, NBLK, false, FUSED>(chain, prm, blocks, st);
+  if (s.dk == 32)
+    return s.bf16 ? launch_chain<32, NBLK, true, FUSED>(chain, prm, blocks, st)
+                  : launch_chain<32, NBLK, false, FUSED>(chain, prm, blocks, st);
+  return hipErrorInvalidValue;
+}
+
+DecodeParams base_params(const Shape& s, int width, const void* q, float* o, const Arena& a,
+                         unsigned* blocks) {
+  constexpr int BEAMS = 16 * kDecodeBeamBlocks;
+  DecodeParams prm = {};
+  prm.q = q;
+  prm.o = o;
+  prm.s0 = a.s0;
+  prm.s_frag = reinterpret_cast<uint4*>(a.s_frag);
+  prm.ak = a.k;
+  prm.av = a.v;
+  prm.ab = a.ab;
+  prm.status = a.status;
+  prm.R = s.R;
+  prm.HK = s.HK;
+  prm.HV = s.HV;
+  prm.G = s.HV / s.HK;
+  prm.W = width;
+  prm.wmax = s.wmax;
+  prm.tmax = s.tmax;
+  prm.ntiles = (width + BEAMS - 1) / BEAMS;
+  const int units = s.R * s.HV;
+  prm.xcd_map = (units % 8 == 0) ? 1 : 0;
+  *blocks = unsigned(units) * unsigned(prm.ntiles);
+  return prm;
+}
+
 }  // namespace
 
 bool decode_supported(const Shape& s) {
@@ -332,36 +582,28 @@ bool decode_supported(const Shape& s) {
 
 hipError_t launch_decode(const Shape& s, int step, int width, const void* q, float* o,
                          const Arena& a, hipStream_t st) {
-  constexpr int NBLK = 1;
-  DecodeParams prm;
-  prm.q = q;
-  prm.o = o;
-  prm.s_frag = reinterpret_cast<const uint4*>(a.s_frag);
-  prm.ak = a.k;
-  prm.av = a.v;
-  prm.ab = a.ab;
-  prm.anc = a.anc[step & 1];
-  prm.R = s.R;
-  prm.HK = s.HK;
-  prm.HV = s.HV;
-  prm.W = width;
-  prm.wmax = s.wmax;
-  prm.tmax = s.tmax;
-  prm.ntiles = (width + 16 * NBLK - 1) / (16 * NBLK);
-  const int units = s.R * s.HV;
-  prm.xcd_map = (units % 8 == 0) ? 1 : 0;
-  const unsigned blocks = unsigned(units) * unsigned(prm.ntiles);
-  const int chain = step + 1;
-  if (s.dk == 128)
-    return s.bf16 ? launch_chain<128, NBLK, true>(chain, prm, blocks, st)
-                  : launch_chain<128, NBLK, false>(chain, prm, blocks, st);
-  if (s.dk == 64)
-    return s.bf16 ? launch_chain<64, NBLK, true>(chain, prm, blocks, st)
-                  : launch_chain<64, NBLK, false>(chain, prm, blocks, st);
-  if (s.dk == 32)
-    return s.bf16 ? launch_chain<32, NBLK, true>(chain, prm, blocks, st)
-                  : launch_chain<32, NBLK, false>(chain, prm, blocks, st);
-  return hipErrorInvalidValue;
+  unsigned blocks;
+  DecodeParams prm = base_params(s, width, q, o, a, &blocks);
+  prm.anc_rd = a.anc[step & 1];
+  return launch_mode<false>(s, step, prm, blocks, st);
+}
+
+hipError_t launch_fused_step(const Shape& s, int step, int width, int prev_width,
+                             const int* parents, const void* k, const void* v,
+                             const float* alpha, const float* beta, const void* q, float* o,
+                             int* gather_out, const Arena& a, hipStream_t st) {
+  unsigned blocks;
+  DecodeParams prm = base_params(s, width, q, o, a, &blocks);
+  prm.parents = parents;
+  prm.k_in = k;
+  prm.v_in = v;
+  prm.alpha_in = alpha;
+  prm.beta_in = beta;
+  prm.gather_out = gather_out;
+  prm.W_prev = prev_width;
+  prm.anc_rd = a.anc[(step + 1) & 1];
+  prm.anc_wr = a.anc[step & 1];
+  return launch_mode<true>(s, step, prm, blocks, st);
 }
 
 }  // namespace onela

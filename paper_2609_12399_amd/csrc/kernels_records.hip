@@ -1,7 +1,6 @@
-// Record store, ancestry index and shared-state split kernels (gfx950).
+// Record store and ancestry index kernels (gfx950).
 //
 //   clear_status  zero the sticky device status word
-//   split_state   S_ctx fp32 -> (hi, lo) bf16 pair in MFMA A-fragment order
 //   resolve       ancestry index update, Sec. 3.3 Eq. 5 (integer, exact)
 //   append        records of one step -> head-major arena slab (Sec. 3.3:
 //                 written once into the current step's slots, never moved)
@@ -12,54 +11,6 @@ namespace {
 
 __global__ void clear_status_kernel(int* status) {
   if (threadIdx.x == 0) status[0] = 0;
-}
-
-// Fragment order of the split state.  For request r and value head hv the
-// d_v rows are served by d_v/32 waves of the decode kernel; wave w owns rows
-// [32w, 32w + 32) as two 16-row MFMA blocks mb.  MFMA row m (0..15) of block
-// mb is state row 32w + 8(m/4) + 4mb + (m%4): with that permutation a lane's
-// four accumulator rows of both blocks are 8 consecutive state rows, so the
-// decode epilogue reads v and writes o with 16-byte vectors.  Lane l of the
-// A fragment for k-step ks holds columns 32ks + 8(l/16) + [0, 8).
-// Storage: [R*HV][dv/32][dk/32][mb 2][hi/lo 2][64 lanes][8 bf16].
-__global__ void split_state_kernel(const float* __restrict__ s0, uint4* __restrict__ frag,
-                                   int units, int dk, int dv) {
-  const int nw = dv / 32, ks_n = dk / 32;
-  const long total = long(units) * nw * ks_n * 2 * 64;
-  const long i = long(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= total) return;
-  const int lane = int(i % 64);
-  long rest = i / 64;
-  const int mb = int(rest % 2);
-  rest /= 2;
-  const int ks = int(rest % ks_n);
-  rest /= ks_n;
-  const int w = int(rest % nw);
-  const long unit = rest / nw;
-  const int m = lane & 15;
-  const int row = 32 * w + 8 * (m >> 2) + 4 * mb + (m & 3);
-  const int col = 32 * ks + 8 * (lane >> 4);
-  const float* src = s0 + (unit * dv + row) * long(dk) + col;
-  unsigned short hi[8], lo[8];
-  for (int e = 0; e < 8; ++e) {
-    const float x = src[e];
-    const __bf16 h = static_cast<__bf16>(x);
-    const __bf16 l = static_cast<__bf16>(x - static_cast<float>(h));
-    hi[e] = __builtin_bit_cast(unsigned short, h);
-    lo[e] = __builtin_bit_cast(unsigned short, l);
-  }
-  uint4 vh, vl;
-  vh.x = hi[0] | (unsigned(hi[1]) << 16);
-  vh.y = hi[2] | (unsigned(hi[3]) << 16);
-  vh.z = hi[4] | (unsigned(hi[5]) << 16);
-  vh.w = hi[6] | (unsigned(hi[7]) << 16);
-  vl.x = lo[0] | (unsigned(lo[1]) << 16);
-  vl.y = lo[2] | (unsigned(lo[3]) << 16);
-  vl.z = lo[4] | (unsigned(lo[5]) << 16);
-  vl.w = lo[6] | (unsigned(lo[7]) << 16);
-  const long base = (((unit * nw + w) * ks_n + ks) * 2 + mb) * 2 * 64;
-  frag[base + lane] = vh;
-  frag[base + 64 + lane] = vl;
 }
 
 // Eq. 5: h_t(b, j) = h_{t-1}(pi_t(b), j) for j < t-1, h_t(b, t-1) = pi_t(b).
@@ -157,15 +108,6 @@ unsigned blocks_for(long n, int threads) { return unsigned((n + threads - 1) / t
 
 hipError_t launch_clear_status(int* status, hipStream_t st) {
   clear_status_kernel<<<1, 64, 0, st>>>(status);
-  return hipGetLastError();
-}
-
-hipError_t launch_split_state(const Shape& s, const float* s0, uint16_t* frag,
-                              hipStream_t st) {
-  const int units = s.R * s.HV;
-  const long total = long(units) * (s.dv / 32) * (s.dk / 32) * 2 * 64;
-  split_state_kernel<<<blocks_for(total, 256), 256, 0, st>>>(
-      s0, reinterpret_cast<uint4*>(frag), units, s.dk, s.dv);
   return hipGetLastError();
 }
 

@@ -18,6 +18,7 @@ struct onela_ctx_s {
   Arena arena;
   hipStream_t stream;
   int resolved;  // last step whose ancestry was resolved (-1: none)
+  bool status_live;  // a step-0 launch (which zeroes the status word) was enqueued
   int appended;  // last step whose records were appended (-1: none)
   int widths[onela::kMaxSteps];
 };
@@ -40,10 +41,12 @@ onela_status_t shape_of(const onela_config_t* c, Shape* s) {
   Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads, c->d_k, c->d_v,
           c->max_beams,    c->max_steps,    c->io_dtype == ONELA_BF16};
   if (!onela::decode_supported(t)) return ONELA_EINVAL;
-  // every index the kernels form must fit in 32-bit element counts per region
+  // the kernels form 32-bit byte offsets: every region must stay below 2 GiB
   const double big = double(t.R) * t.tmax * (t.HV > t.HK ? t.HV : t.HK) * t.wmax *
-                     (t.dv > t.dk ? t.dv : t.dk);
-  if (big >= 2147483647.0) return ONELA_EINVAL;
+                     (t.dv > t.dk ? t.dv : t.dk) * t.io_bytes();
+  const double outb = double(t.R) * t.wmax * t.HV * t.dv * 4.0;
+  const double s0b = double(t.R) * t.HV * t.dv * t.dk * 4.0;
+  if (big >= 2147483648.0 || outb >= 2147483648.0 || s0b >= 2147483648.0) return ONELA_EINVAL;
   *s = t;
   return ONELA_OK;
 }
@@ -119,6 +122,7 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   p += l.anc;
   c->arena.anc[1] = reinterpret_cast<int*>(p);
   p += l.anc;
+  c->arena.s0 = s0;
   c->arena.s_frag = reinterpret_cast<uint16_t*>(p);
   p += l.s_frag;
   c->arena.k = p;
@@ -127,11 +131,7 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   p += l.v;
   c->arena.ab = reinterpret_cast<float2*>(p);
 
-  if (!launch_ok(onela::launch_clear_status(c->arena.status, c->stream)) ||
-      !launch_ok(onela::launch_split_state(s, s0, c->arena.s_frag, c->stream))) {
-    delete c;
-    return ONELA_EHIP;
-  }
+  c->status_live = false;
   *out = c;
   return ONELA_OK;
 }
@@ -186,12 +186,42 @@ onela_status_t onela_decode_step(onela_ctx_t c, int32_t step, const void* q, flo
   if (!q || !o || !aligned16(q) || !aligned16(o)) return ONELA_EINVAL;
   hipError_t e = onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
                                       c->stream);
-  return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
+  if (!launch_ok(e)) return ONELA_EHIP;
+  if (step == 0) c->status_live = true;
+  return ONELA_OK;
+}
+
+onela_status_t onela_decode_step_fused(onela_ctx_t c, int32_t step, int32_t width,
+                                       const int32_t* parents, const void* k, const void* v,
+                                       const float* alpha, const float* beta, const void* q,
+                                       float* o, int32_t* gather_out) {
+  if (!c) return ONELA_EINVAL;
+  const Shape& s = c->shape;
+  if (step != c->resolved + 1 || c->appended != c->resolved) return ONELA_ESTEP;
+  if (step >= s.tmax) return ONELA_ECAPACITY;
+  if (width < 1 || width > s.wmax) return ONELA_ECAPACITY;
+  if (step == 0 && parents) return ONELA_EINVAL;
+  if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
+  if (gather_out && !aligned4(gather_out)) return ONELA_EINVAL;
+  if (!k || !v || !alpha || !beta || !q || !o) return ONELA_EINVAL;
+  if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta) || !aligned16(q) ||
+      !aligned16(o))
+    return ONELA_EINVAL;
+  hipError_t e = onela::launch_fused_step(s, step, width, step > 0 ? c->widths[step - 1] : 0,
+                                          parents, k, v, alpha, beta, q, o, gather_out,
+                                          c->arena, c->stream);
+  if (!launch_ok(e)) return ONELA_EHIP;
+  c->widths[step] = width;
+  c->resolved = step;
+  c->appended = step;
+  if (step == 0) c->status_live = true;
+  return ONELA_OK;
 }
 
 onela_status_t onela_get_device_status(onela_ctx_t c) {
   if (!c) return ONELA_EINVAL;
   if (hipStreamSynchronize(c->stream) != hipSuccess) return ONELA_EHIP;
+  if (!c->status_live) return ONELA_OK;  // no step has run: nothing was flagged
   int word = 0;
   if (hipMemcpy(&word, c->arena.status, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
     return ONELA_EHIP;

@@ -27,7 +27,7 @@ STATUS_NAMES = {0: "ONELA_OK", 1: "ONELA_EINVAL", 2: "ONELA_ESTEP", 3: "ONELA_EP
 # every symbol declared in include/onela.h
 EXPORTED = ["onela_status_str", "onela_check_config", "onela_workspace_bytes", "onela_init",
             "onela_reset", "onela_resolve_ancestry", "onela_append_records",
-            "onela_decode_step", "onela_get_device_status", "onela_destroy",
+            "onela_decode_step", "onela_decode_step_fused", "onela_get_device_status", "onela_destroy",
             "onela_prefill_state", "onela_fullstate_workspace_bytes", "onela_fullstate_step",
             "onela_capacity_bytes", "onela_fullstate_capacity_bytes"]
 
@@ -77,6 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "onela_resolve_ancestry": ([_P, _I32, _I32, _P, _P], _I32),
         "onela_append_records": ([_P, _I32, _P, _P, _P, _P], _I32),
         "onela_decode_step": ([_P, _I32, _P, _P], _I32),
+        "onela_decode_step_fused": ([_P, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P], _I32),
         "onela_get_device_status": ([_P], _I32),
         "onela_destroy": ([_P], None),
         "onela_prefill_state": ([cfgp, _I32, _P, _P, _P, _P, _P, _P], _I32),
@@ -165,6 +166,14 @@ def onela_append_records(ctx, step: int, k, v, alpha, beta):
 def onela_decode_step(ctx, step: int, q, o):
     _check(load_library().onela_decode_step(ctx, step, _dev(q, "q"), _dev(o, "o")),
            "onela_decode_step")
+
+
+def onela_decode_step_fused(ctx, step: int, width: int, parents, k, v, alpha, beta, q, o,
+                            gather_out=None):
+    _check(load_library().onela_decode_step_fused(
+        ctx, step, width, _dev(parents, "parents", optional=True), _dev(k, "k"), _dev(v, "v"),
+        _dev(alpha, "alpha"), _dev(beta, "beta"), _dev(q, "q"), _dev(o, "o"),
+        _dev(gather_out, "gather_out", optional=True)), "onela_decode_step_fused")
 
 
 def onela_get_device_status(ctx) -> int:

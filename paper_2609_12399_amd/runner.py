@@ -95,9 +95,14 @@ class Decoder:
             raise ab.OnelaError(ab.ONELA_EINVAL, "onela_workspace_bytes")
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         self.stream = stream
+        self.s0 = s0  # borrowed by the context until close()
         self.ctx = ab.onela_init(self.cfg, s0, self.workspace, self.ws_bytes, stream)
 
-    def step(self, t: int, st: DeviceStep, o, gather_out=None):
+    def step(self, t: int, st: DeviceStep, o, gather_out=None, fused: bool = False):
+        if fused:
+            ab.onela_decode_step_fused(self.ctx, t, st.width, st.parents, st.k, st.v, st.alpha,
+                                       st.beta, st.q, o, gather_out)
+            return
         ab.onela_resolve_ancestry(self.ctx, t, st.width, st.parents, gather_out)
         ab.onela_append_records(self.ctx, t, st.k, st.v, st.alpha, st.beta)
         ab.onela_decode_step(self.ctx, t, st.q, o)
@@ -108,11 +113,13 @@ class Decoder:
         return [torch.empty((s.R, st.width, s.HV, s.dv), dtype=torch.float32,
                             device=self.workspace.device) for st in dw.steps]
 
-    def run(self, dw: DeviceWorkload, outs=None, gathers=None):
+    def run(self, dw: DeviceWorkload, outs=None, gathers=None, fused=False):
+        """Run every step; ``fused`` is a bool or a per-step list of bools."""
         if outs is None:
             outs = self.alloc_outputs(dw)
         for t, st in enumerate(dw.steps):
-            self.step(t, st, outs[t], None if gathers is None else gathers[t])
+            f = fused[t] if isinstance(fused, (list, tuple)) else fused
+            self.step(t, st, outs[t], None if gathers is None else gathers[t], f)
         return outs
 
     def reset(self):

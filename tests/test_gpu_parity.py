@@ -20,14 +20,14 @@ torch = pytest.importorskip("torch")
 DEV = "cuda:0"
 
 
-def run_gpu(wl, s0, with_gather=True):
+def run_gpu(wl, s0, with_gather=True, fused=False):
     dw = runner.to_device(wl, DEV, with_prompt=False)
     dec = runner.Decoder(wl.spec, torch.from_numpy(s0).to(DEV), DEV)
     gathers = None
     if with_gather:
         gathers = [torch.full((wl.spec.R, st.width, max(t, 1)), -7, dtype=torch.int32,
                               device=DEV) for t, st in enumerate(dw.steps)]
-    outs = dec.run(dw, gathers=gathers)
+    outs = dec.run(dw, gathers=gathers, fused=fused)
     assert dec.status() == ab.ONELA_OK
     torch.cuda.synchronize()
     o = [x.cpu().numpy() for x in outs]
@@ -49,6 +49,33 @@ def test_decode_matches_oracle(name):
     assert max(errs) <= REL_TOL
 
 
+@pytest.mark.parametrize("name", list(W.SPECS))
+def test_fused_step_matches_oracle(name):
+    """onela_decode_step_fused (resolve + append + decode in one launch)."""
+    log(f"[fused] {name}")
+    wl, s0, ref = cached_case(name)
+    o, g = run_gpu(wl, s0, fused=True)
+    anc = oracle_ancestry(wl)
+    for t in range(wl.spec.T):
+        assert np.array_equal(g[t], anc[t]), f"ancestry differs at t={t}"
+    errs = [rel_err(o[t], ref[t]) for t in range(wl.spec.T)]
+    log(f"[fused] {name} max rel err per step {['%.2e' % e for e in errs]}")
+    assert max(errs) <= REL_TOL
+
+
+@pytest.mark.parametrize("pattern", [[True, False, True, False], [False, True, True, False, True]])
+def test_fused_and_separate_steps_mix(pattern):
+    """Both forms leave the context in the same state, so they can alternate;
+    outputs are bitwise equal to the all-separate run."""
+    name = "h16_d128_w512" if len(pattern) == 4 else "gqa_h16x32_d128_w1024"
+    wl, s0, ref = cached_case(name)
+    o_sep, g_sep = run_gpu(wl, s0)
+    o_mix, g_mix = run_gpu(wl, s0, fused=pattern)
+    for t in range(wl.spec.T):
+        assert np.array_equal(g_sep[t], g_mix[t])
+        assert np.array_equal(o_sep[t], o_mix[t]), f"t={t}"
+
+
 @pytest.mark.parametrize("base,widths", [
     ("tiny_h2_d32_w8", (5, 21, 17, 33)),
     ("h16_d128_w128", (1, 3, 40, 7, 100)),
@@ -60,11 +87,12 @@ def test_ragged_and_changing_widths(base, widths):
     wl = W.make_workload(spec)
     s0 = oracle_s0(wl)
     ref, _ = oracle_outputs(wl, s0)
-    o, g = run_gpu(wl, s0)
     anc = oracle_ancestry(wl)
-    for t in range(spec.T):
-        assert np.array_equal(g[t], anc[t])
-        assert rel_err(o[t], ref[t]) <= REL_TOL
+    for fused in (False, True):
+        o, g = run_gpu(wl, s0, fused=fused)
+        for t in range(spec.T):
+            assert np.array_equal(g[t], anc[t])
+            assert rel_err(o[t], ref[t]) <= REL_TOL
 
 
 def _small(io="bf16", d=128, widths=(16, 16, 16), HK=2, HV=4, seed=5):
@@ -149,7 +177,8 @@ def test_run_to_run_deterministic():
         assert np.array_equal(a, b)
 
 
-def test_bad_parent_is_reported_and_contained():
+@pytest.mark.parametrize("fused", [False, True])
+def test_bad_parent_is_reported_and_contained(fused):
     spec = _small(widths=(16, 16, 16), seed=21)
     wl = W.make_workload(spec)
     bad_beam = 5
@@ -160,8 +189,11 @@ def test_bad_parent_is_reported_and_contained():
     ref, _ = oracle_outputs(good_wl, s0)
     dw = runner.to_device(wl, DEV, with_prompt=False)
     dec = runner.Decoder(spec, torch.from_numpy(s0).to(DEV), DEV)
-    outs = dec.run(dw)
+    gathers = [torch.zeros((1, 16, max(t, 1)), dtype=torch.int32, device=DEV) for t in range(3)]
+    outs = dec.run(dw, gathers=gathers, fused=fused)
     assert dec.status() == ab.ONELA_EPARENT
+    g1 = gathers[1].cpu().numpy()[0, :, :1]
+    assert g1[bad_beam, 0] == -1 and np.all(np.delete(g1[:, 0], bad_beam) >= 0)
     assert dec.status() == ab.ONELA_OK  # cleared after reporting
     o = [x.cpu().numpy() for x in outs]
     # beams whose ancestry avoids the bad slot are still exact
