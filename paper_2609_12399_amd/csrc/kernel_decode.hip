@@ -260,7 +260,9 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
   };
   auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
 
-  // ---- round 1: indices (parents in FUSED mode, h_t otherwise)
+  // ---- round 1: indices (parents in FUSED mode, h_t otherwise), then every
+  // load that needs no index: the query and the beam's own step-t record
+  // (fold operands first, the v rows for the epilogue after them).
   int fsrc[NAX], ssrc[NBLK][NAX];
   bool fpok = true, spok[NBLK];
   int fpar = 0, spar[NBLK];
@@ -282,7 +284,6 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
     }
   }
 
-  // ---- loads that need no index: query, the step-t record, shared state
   using K8 = RawV<BF16, 8>;
   using VR = RawV<BF16, RPL>;
   K8 qr[C8];
@@ -312,11 +313,75 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
       for (int nb = 0; nb < NBLK; ++nb) vr[nb][NA].load(vs, sbc[nb] * vslot + row0 * IOB);
     }
   }
-  // This wave's shared-state rows in MFMA A-fragment order: lane l holds
-  // row 16 MB w + 4 MB (m/4) + 4 mb + (m%4) (m = l % 16) and columns
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- ancestral records.  DECODE: all of them once h_t is back.  FUSED:
+  // the parent's own step-(t-1) record as soon as the parent index is back
+  // (it needs no ancestry row), together with the parent's row of h_{t-1};
+  // then the records of steps <= t-2 once that row is back.
+  bool fok[CHAIN];
+  fok[NA] = true;
+  auto load_fold_record = [&](int j, int slot) {
+    const char* ks = k_slab(j);
+#pragma unroll
+    for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
+    abr[j] = ab_slab(j)[slot];
+  };
+  if constexpr (FUSED && NA > 0) {
+    fpok = unsigned(fpar) < unsigned(p.W_prev);
+    const int pf = fpok ? fpar : 0;
+    fsrc[NA - 1] = pf;
+    fok[NA - 1] = fpok;
+    load_fold_record(NA - 1, pf);
+    int ps[NBLK];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
+      ps[nb] = spok[nb] ? spar[nb] : 0;
+      ssrc[nb][NA - 1] = ps[nb];
+      vr[nb][NA - 1].load(v_slab(NA - 1), ps[nb] * vslot + row0 * IOB);
+    }
+#pragma unroll
+    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps[nb] * tmax + j];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < NA - 1; ++j) {
+      fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
+      load_fold_record(j, fok[j] ? fsrc[j] : 0);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) {
+        const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
+        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+      }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      fok[j] = unsigned(fsrc[j]) < unsigned(wmax);
+      load_fold_record(j, fok[j] ? fsrc[j] : 0);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA; ++j) {
+        const bool ok = unsigned(ssrc[nb][j]) < unsigned(wmax);
+        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+      }
+  }
+
+  // ---- shared-state rows of this wave in MFMA A-fragment order, issued
+  // last: they are needed only after the fold and the barrier, and are L2
+  // hits for all but the first workgroup of a head on each XCD.  Lane l
+  // holds row 16 MB w + 4 MB (m/4) + 4 mb + (m%4) (m = l % 16) and columns
   // 32 ks + 8 (l/16) + [0, 8); the row permutation makes a lane's
   // accumulator rows consecutive state rows.  Step 0 reads fp32 S_ctx and
-  // splits it into bf16 hi/lo in registers (and tile-0 workgroups store the
+  // splits it into bf16 hi/lo in registers (tile-0 workgroups store the
   // split fragments in the workspace); later steps read the stored
   // fragments, 1 KiB contiguous per wave-wide load.
   float4 Araw[NA == 0 ? KS : 1][MB][2];
@@ -342,46 +407,6 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int hl = 0; hl < 2; ++hl) A[ks][mb][hl] = frag[((ks * MB + mb) * 2 + hl) * 64];
   }
-  __builtin_amdgcn_sched_barrier(0);
-
-  // ---- round 2 (FUSED): the parents' rows of h_{t-1}
-  if constexpr (FUSED && NA > 0) {
-    fpok = unsigned(fpar) < unsigned(p.W_prev);
-    const int pf = fpok ? fpar : 0;
-#pragma unroll
-    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
-    fsrc[NA - 1] = pf;
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb) {
-      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
-      const int ps = spok[nb] ? spar[nb] : 0;
-#pragma unroll
-      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps * tmax + j];
-      ssrc[nb][NA - 1] = ps;
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
-
-  // ---- ancestral records
-  bool fok[CHAIN];
-  fok[NA] = true;
-#pragma unroll
-  for (int j = 0; j < NA; ++j) {
-    fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
-    const int slot = fok[j] ? fsrc[j] : 0;
-    const char* ks = k_slab(j);
-#pragma unroll
-    for (int c = 0; c < C8; ++c)
-      kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
-    abr[j] = ab_slab(j)[slot];
-  }
-#pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
-      vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
-    }
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- phase 1: fold the query newest -> oldest (scaled form)
@@ -464,22 +489,33 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
           for (int hl = 0; hl < 2; ++hl) frag[((ks * MB + mb) * 2 + hl) * 64] = A[ks][mb][hl];
       }
   }
-  f32x4 acc[NBLK][MB];
+  // Two accumulator chains per output block (hi*hi, and the two cross
+  // terms) and the beam blocks interleaved keep several independent MFMAs
+  // in flight.
+  f32x4 acc[NBLK][MB], acx[NBLK][MB];
 #pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb) {
+  for (int nb = 0; nb < NBLK; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const uint4 bh = p_lds[0][nb][ks][g4][lane & 15];
-      const uint4 bl = p_lds[1][nb][ks][g4][lane & 15];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        acc[nb][mb] = mfma_bf16(A[ks][mb][1], bh, acc[nb][mb]);
-        acc[nb][mb] = mfma_bf16(A[ks][mb][0], bl, acc[nb][mb]);
-        acc[nb][mb] = mfma_bf16(A[ks][mb][0], bh, acc[nb][mb]);
-      }
+    for (int mb = 0; mb < MB; ++mb) {
+      acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acx[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint4 bh[NBLK], bl[NBLK];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+      bh[nb] = p_lds[0][nb][ks][g4][lane & 15];
+      bl[nb] = p_lds[1][nb][ks][g4][lane & 15];
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) {
+        acx[nb][mb] = mfma_bf16(A[ks][mb][1], bh[nb], acx[nb][mb]);
+        acc[nb][mb] = mfma_bf16(A[ks][mb][0], bh[nb], acc[nb][mb]);
+        acx[nb][mb] = mfma_bf16(A[ks][mb][0], bl[nb], acx[nb][mb]);
+      }
   }
 
   // ---- phase 3: add the v-terms and store RPL consecutive rows per lane
@@ -489,7 +525,7 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
     const int sb = b0 + bl;
     float ov[RPL];
 #pragma unroll
-    for (int e = 0; e < RPL; ++e) ov[e] = acc[nb][e >> 2][e & 3];
+    for (int e = 0; e < RPL; ++e) ov[e] = acx[nb][e >> 2][e & 3] + acc[nb][e >> 2][e & 3];
 #pragma unroll
     for (int j = 0; j < CHAIN; ++j) {
       const float gj = g_lds[bl][j];

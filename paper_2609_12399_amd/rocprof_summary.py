@@ -1,0 +1,134 @@
+"""Summaries of rocprofv3 output for this library's kernels.
+
+    python -m paper_2609_12399_amd.rocprof_summary trace <dir-or-file>
+    python -m paper_2609_12399_amd.rocprof_summary pmc <FETCH_SIZE dir> <WRITE_SIZE dir>
+
+``trace`` reads a ``--kernel-trace`` result (``*_kernel_trace.csv`` or a
+``*_results.db``) and prints one markdown row per kernel instance (calls,
+average / median / min duration).  ``pmc`` reads two ``--pmc FETCH_SIZE`` and
+``--pmc WRITE_SIZE`` runs (``*_counter_collection.csv``) and prints the
+average KiB per dispatch of each counter and kernel, raw and scaled by the
+factors a plain copy of known size gives (the largest device copy in the
+same runs, whose true read and write sizes equal its byte count).
+"""
+from __future__ import annotations
+
+import csv
+import glob
+import hashlib
+import os
+import re
+import sqlite3
+import statistics
+import sys
+from collections import defaultdict
+
+DECODE_RE = re.compile(r"decode_kernel<(\d+), (\d+), (\d+), (\d+), (\d+), (true|false), "
+                       r"(true|false)>")
+
+
+def short_name(name: str) -> str:
+    m = DECODE_RE.search(name)
+    if m:
+        dk, dv, mb, nblk, chain, bf16, fused = m.groups()
+        mode = "fused" if fused == "true" else "decode"
+        return f"decode_kernel<{mode}, d={dk}, chain={chain}, {'bf16' if bf16 == 'true' else 'f32'}>"
+    for k in ("resolve_kernel", "append_kernel", "prefill_kernel", "fullstate_kernel",
+              "clear_status_kernel"):
+        if k in name:
+            return k
+    name = re.sub(r"\(.*", "", name).replace("void ", "")
+    return name[:60]
+
+
+def source_sha256(path: str) -> str:
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def _find(path: str, pattern: str) -> list:
+    if os.path.isfile(path):
+        return [path]
+    return sorted(glob.glob(os.path.join(path, "**", pattern), recursive=True))
+
+
+def trace_rows(path: str):
+    """(name, grid, workgroup, duration_ns) per dispatch."""
+    csvs = _find(path, "*kernel_trace.csv")
+    if csvs:
+        for f in csvs:
+            for r in csv.DictReader(open(f)):
+                dur = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+                yield (r["Kernel_Name"], int(r.get("Grid_Size_X", r.get("Grid_Size", 0))),
+                       int(r.get("Workgroup_Size_X", r.get("Workgroup_Size", 0))), dur)
+        return
+    for f in _find(path, "*results.db"):
+        db = sqlite3.connect(f)
+        for name, dur, gx, wx in db.execute(
+                "select name, duration, grid_x, workgroup_x from kernels order by start"):
+            yield name, gx, wx, dur
+
+
+def summarize_trace(path: str) -> str:
+    d = defaultdict(list)
+    for name, grid, wg, dur in trace_rows(path):
+        d[(short_name(name), grid // max(wg, 1), wg)].append(dur / 1e3)
+    out = ["| kernel | workgroups | threads | calls | avg us | median us | min us |",
+           "|---|---|---|---|---|---|---|"]
+    for (name, g, w), v in sorted(d.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| {name} | {g} | {w} | {len(v)} | {sum(v) / len(v):.2f} | "
+                   f"{statistics.median(v):.2f} | {min(v):.2f} |")
+    return "\n".join(out)
+
+
+def pmc_rows(path: str):
+    for f in _find(path, "*counter_collection.csv"):
+        for r in csv.DictReader(open(f)):
+            yield r["Kernel_Name"], int(r["Grid_Size"]), int(r["Workgroup_Size"]), \
+                r["Counter_Name"], float(r["Counter_Value"])
+
+
+def copy_calibration(rows) -> float:
+    """Bytes-per-KiB-reported factor from the largest device copy dispatch."""
+    best = None
+    for name, grid, wg, cname, val in rows:
+        if "copyBuffer" in name and (best is None or val > best):
+            best = val
+    return best
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, copy_bytes: int | None = None) -> str:
+    frows = list(pmc_rows(fetch_dir))
+    wrows = list(pmc_rows(write_dir))
+    fmax, wmax = copy_calibration(frows), copy_calibration(wrows)
+    # the largest copy reads and writes the same number of bytes; WRITE_SIZE
+    # of a copy counts exactly its size, so it calibrates FETCH_SIZE too
+    kib = copy_bytes / 1024 if copy_bytes else wmax
+    ff, wf = kib / fmax, kib / wmax
+    out = [f"calibration: largest device copy = {kib:.0f} KiB read and written; "
+           f"FETCH_SIZE reads {fmax:.1f} KiB (factor {ff:.4f}), "
+           f"WRITE_SIZE reads {wmax:.1f} KiB (factor {wf:.4f})", "",
+           "| kernel | workgroups | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | "
+           "read MB (scaled) | written MB (scaled) | total MB |",
+           "|---|---|---|---|---|---|---|---|"]
+    acc = defaultdict(lambda: [[], []])
+    for rows, i in ((frows, 0), (wrows, 1)):
+        for name, grid, wg, cname, val in rows:
+            acc[(short_name(name), grid // max(wg, 1))][i].append(val)
+    for (name, g), (fv, wv) in sorted(acc.items(), key=lambda kv: -sum(kv[1][0])):
+        if not fv or not wv:
+            continue
+        f, w = sum(fv) / len(fv), sum(wv) / len(wv)
+        rd, wr = f * ff * 1024 / 1e6, w * wf * 1024 / 1e6
+        out.append(f"| {name} | {g} | {len(fv)} | {f:.1f} | {w:.1f} | {rd:.2f} | {wr:.2f} | "
+                   f"{rd + wr:.2f} |")
+    return "\n".join(out)
+
+
+if __name__ == "__main__":
+    if len(sys.argv) >= 3 and sys.argv[1] == "trace":
+        print(summarize_trace(sys.argv[2]))
+    elif len(sys.argv) >= 4 and sys.argv[1] == "pmc":
+        print(summarize_pmc(sys.argv[2], sys.argv[3]))
+    else:
+        print(__doc__)
+        sys.exit(2)
