@@ -57,8 +57,9 @@ typedef enum {
 
 typedef enum { ONELA_F32 = 0, ONELA_BF16 = 1 } onela_dtype_t;
 
-/* Shape of one decode context.  Supported: d_k == d_v in {32, 64, 128};
- * io_dtype ONELA_BF16 or ONELA_F32; num_v_heads a multiple of num_qk_heads;
+/* Shape of one decode context.  Supported (d_k, d_v): (32, 32), (64, 64),
+ * (128, 128) with io_dtype ONELA_BF16 or ONELA_F32, and (128, 256), (128, 512),
+ * (256, 256), (256, 512) with ONELA_BF16; num_v_heads a multiple of num_qk_heads;
  * 1 <= max_beams <= 65536; 1 <= max_steps <= 8 (the record chain of step t
  * has t + 1 records). */
 typedef struct {

@@ -12,9 +12,7 @@ namespace onela {
 // Maximum records in one beam's chain (decode steps 0 .. kMaxSteps-1).
 constexpr int kMaxSteps = 8;
 
-// Decode tiling: MFMA row blocks (16 state rows each) per wave and 16-beam
-// MFMA column blocks per workgroup.
-constexpr int kDecodeRowBlocks = 1;
+// Decode tiling: 16-beam MFMA column blocks per workgroup.
 constexpr int kDecodeBeamBlocks = 2;
 
 // Bits of the sticky device status word.

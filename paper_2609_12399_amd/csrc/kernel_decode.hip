@@ -23,8 +23,9 @@
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16 (about 16 significant bits
 // per product; the dropped S_lo P_lo term is ~2^-17 relative).
 //
-// Work decomposition.  One workgroup = (request, value head, 16*NBLK beams),
-// DV/(16*MB) waves.  Phase 1 (fold): LPB lanes per beam, each owning EPL
+// Work decomposition.  One workgroup = (request, value head, row slice of DVW
+// state rows, 16*NBLK beams), d_k/16 waves of 16*MB rows each (MB = DVW/d_k;
+// wide d_v is split into row slices, each folding its beams again).  Phase 1 (fold): LPB lanes per beam, each owning EPL
 // consecutive key elements; dot products are reduced across those lanes with
 // DPP.  The folded queries are written, split into hi/lo, to LDS directly in
 // MFMA B-fragment order; the fold scalars g_j go to LDS too.  Phase 2
@@ -188,10 +189,14 @@ __device__ inline f32x4 mfma_bf16(const uint4& a, const uint4& b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <int DK, int DV, int MB, int NBLK, int CHAIN, bool BF16, bool FUSED>
-__global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
-  constexpr int NW = DV / (16 * MB); // waves per workgroup (16*MB state rows each)
+template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED>
+__global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
+  constexpr int MB = DVW / DK;       // 16-row MFMA blocks per wave
+  constexpr int NS = DV / DVW;       // row slices (workgroups) per (request, head, tile)
+  constexpr int NW = DVW / (16 * MB);// waves per workgroup (= DK / 16)
   constexpr int RPL = 4 * MB;        // consecutive output rows per epilogue lane
+  static_assert(MB * DK == DVW && NS * DVW == DV && (MB == 1 || MB == 2 || MB == 4),
+                "state rows per workgroup must be 1, 2 or 4 times d_k");
   constexpr int NT = NW * 64;        // threads per workgroup
   constexpr int BEAMS = 16 * NBLK;   // beams per workgroup
   constexpr int LPB = NT / BEAMS;    // fold lanes per beam
@@ -217,15 +222,20 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
     if (blockIdx.x == 0 && tid == 0) p.status[0] = 0;
   }
 
-  int unit, tile;
+  // block -> (unit = request*HV + head, row slice, beam tile); all slices and
+  // tiles of a unit share an XCD when the unit count is a multiple of 8
+  int unit, st;
+  const int nst = NS * p.ntiles;
   if (p.xcd_map) {
     const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    unit = x + 8 * (slot / p.ntiles);
-    tile = slot % p.ntiles;
+    unit = x + 8 * (slot / nst);
+    st = slot % nst;
   } else {
-    unit = blockIdx.x / p.ntiles;
-    tile = blockIdx.x % p.ntiles;
+    unit = blockIdx.x / nst;
+    st = blockIdx.x % nst;
   }
+  const int slice = st / p.ntiles;
+  const int tile = st - slice * p.ntiles;
   const int r = unit / p.HV;
   const int hv = unit - r * p.HV;
   const int hk = hv / p.G;
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
   const int fbc = fvalid ? fbeam : 0;
   // epilogue lanes: beam (lane & 15) of block nb, rows row0 + [0, RPL)
   const int g4 = lane >> 4;
-  const unsigned row0 = 16 * MB * w + RPL * g4;
+  const unsigned row0 = DVW * slice + 16 * MB * w + RPL * g4;
   int sbc[NBLK];
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
@@ -386,14 +396,15 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
   // fragments, 1 KiB contiguous per wave-wide load.
   float4 Araw[NA == 0 ? KS : 1][MB][2];
   uint4 A[KS][MB][2];
-  uint4* const frag = p.s_frag + (long(unit) * NW + w) * (KS * MB * 2 * 64) + lane;
+  uint4* const frag =
+      p.s_frag + ((long(unit) * NS + slice) * NW + w) * (KS * MB * 2 * 64) + lane;
   if constexpr (NA == 0) {
     const int m = lane & 15;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const unsigned row = 16 * MB * w + 4 * MB * (m >> 2) + 4 * mb + (m & 3);
+        const unsigned row = DVW * slice + 16 * MB * w + 4 * MB * (m >> 2) + 4 * mb + (m & 3);
         const unsigned col = 32 * ks + 8 * (lane >> 4);
         const unsigned off = ((unsigned(unit) * DV + row) * DK + col) * 4u;
         Araw[ks][mb][0] = *at<float4>(p.s0, off);
@@ -448,7 +459,7 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
 
   // ---- FUSED: index h_t and the step-t record into the context
   if constexpr (FUSED) {
-    if (fvalid) {
+    if (fvalid && slice == 0) {
       if (hv == 0 && li == 0 && NA > 0) {
         int* dst = p.anc_wr + (long(r) * wmax + fbeam) * tmax;
         int* g = p.gather_out ? p.gather_out + (long(r) * W + fbeam) * NA : nullptr;
@@ -543,14 +554,14 @@ __global__ __launch_bounds__(4 * DV / MB) void decode_kernel(DecodeParams p) {
   }
 }
 
-template <int D, int NBLK, bool BF16, bool FUSED>
+template <int DK, int DV, int DVW, bool BF16, bool FUSED>
 hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hipStream_t st) {
-  constexpr int MB = kDecodeRowBlocks;
-  constexpr int threads = 4 * D / MB;
+  constexpr int NBLK = kDecodeBeamBlocks;
+  constexpr int threads = 4 * DK;
   switch (chain) {
-#define ONELA_CHAIN_CASE(C)                                                        \
-  case C:                                                                         \
-    decode_kernel<D, D, MB, NBLK, C, BF16, FUSED><<<blocks, threads, 0, st>>>(prm); \
+#define ONELA_CHAIN_CASE(C)                                                              \
+  case C:                                                                               \
+    decode_kernel<DK, DV, DVW, NBLK, C, BF16, FUSED><<<blocks, threads, 0, st>>>(prm);  \
     break;
     ONELA_CHAIN_CASE(1)
     ONELA_CHAIN_CASE(2)
@@ -567,25 +578,37 @@ hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hip
   return hipGetLastError();
 }
 
+// Supported (d_k, d_v) pairs and the state rows one workgroup covers:
+// DVW = min(d_v, 256) rows in 16*MB-row blocks per wave, MB = DVW / d_k.
 template <bool FUSED>
-hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsigned blocks,
+hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsigned units,
                        hipStream_t st) {
-  constexpr int NBLK = kDecodeBeamBlocks;
   const int chain = step + 1;
-  if (s.dk == 128)
-    return s.bf16 ? launch_chain<128, NBLK, true, FUSED>(chain, prm, blocks, st)
-                  : launch_chain<128, NBLK, false, FUSED>(chain, prm, blocks, st);
-  if (s.dk == 64)
-    return s.bf16 ? launch_chain<64, NBLK, true, FUSED>(chain, prm, blocks, st)
-                  : launch_chain<64, NBLK, false, FUSED>(chain, prm, blocks, st);
-  if (s.dk == 32)
-    return s.bf16 ? launch_chain<32, NBLK, true, FUSED>(chain, prm, blocks, st)
-                  : launch_chain<32, NBLK, false, FUSED>(chain, prm, blocks, st);
+#define ONELA_SHAPE(DK, DV, DVW)                                                          \
+  if (s.dk == DK && s.dv == DV) {                                                        \
+    const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
+    return s.bf16 ? launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st)      \
+                  : launch_chain<DK, DV, DVW, false, FUSED>(chain, prm, blocks, st);    \
+  }
+#define ONELA_SHAPE_BF16(DK, DV, DVW)                                                     \
+  if (s.dk == DK && s.dv == DV && s.bf16) {                                              \
+    const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
+    return launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st);               \
+  }
+  ONELA_SHAPE(32, 32, 32)
+  ONELA_SHAPE(64, 64, 64)
+  ONELA_SHAPE(128, 128, 128)
+  ONELA_SHAPE_BF16(128, 256, 256)
+  ONELA_SHAPE_BF16(128, 512, 256)
+  ONELA_SHAPE_BF16(256, 256, 256)
+  ONELA_SHAPE_BF16(256, 512, 256)
+#undef ONELA_SHAPE
+#undef ONELA_SHAPE_BF16
   return hipErrorInvalidValue;
 }
 
 DecodeParams base_params(const Shape& s, int width, const void* q, float* o, const Arena& a,
-                         unsigned* blocks) {
+                         unsigned* units_out) {
   constexpr int BEAMS = 16 * kDecodeBeamBlocks;
   DecodeParams prm = {};
   prm.q = q;
@@ -606,30 +629,33 @@ DecodeParams base_params(const Shape& s, int width, const void* q, float* o, con
   prm.ntiles = (width + BEAMS - 1) / BEAMS;
   const int units = s.R * s.HV;
   prm.xcd_map = (units % 8 == 0) ? 1 : 0;
-  *blocks = unsigned(units) * unsigned(prm.ntiles);
+  *units_out = unsigned(units);
   return prm;
 }
 
 }  // namespace
 
 bool decode_supported(const Shape& s) {
-  return s.dk == s.dv && (s.dk == 32 || s.dk == 64 || s.dk == 128);
+  const int dk = s.dk, dv = s.dv;
+  if ((dk == 32 && dv == 32) || (dk == 64 && dv == 64) || (dk == 128 && dv == 128)) return true;
+  if (!s.bf16) return false;
+  return (dk == 128 && (dv == 256 || dv == 512)) || (dk == 256 && (dv == 256 || dv == 512));
 }
 
 hipError_t launch_decode(const Shape& s, int step, int width, const void* q, float* o,
                          const Arena& a, hipStream_t st) {
-  unsigned blocks;
-  DecodeParams prm = base_params(s, width, q, o, a, &blocks);
+  unsigned units;
+  DecodeParams prm = base_params(s, width, q, o, a, &units);
   prm.anc_rd = a.anc[step & 1];
-  return launch_mode<false>(s, step, prm, blocks, st);
+  return launch_mode<false>(s, step, prm, units, st);
 }
 
 hipError_t launch_fused_step(const Shape& s, int step, int width, int prev_width,
                              const int* parents, const void* k, const void* v,
                              const float* alpha, const float* beta, const void* q, float* o,
                              int* gather_out, const Arena& a, hipStream_t st) {
-  unsigned blocks;
-  DecodeParams prm = base_params(s, width, q, o, a, &blocks);
+  unsigned units;
+  DecodeParams prm = base_params(s, width, q, o, a, &units);
   prm.parents = parents;
   prm.k_in = k;
   prm.v_in = v;
@@ -639,7 +665,7 @@ hipError_t launch_fused_step(const Shape& s, int step, int width, int prev_width
   prm.W_prev = prev_width;
   prm.anc_rd = a.anc[(step + 1) & 1];
   prm.anc_wr = a.anc[step & 1];
-  return launch_mode<true>(s, step, prm, blocks, st);
+  return launch_mode<true>(s, step, prm, units, st);
 }
 
 }  // namespace onela

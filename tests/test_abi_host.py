@@ -45,6 +45,12 @@ def test_config_validation(lib):
     assert ab.onela_check_config(cfg()) == ab.ONELA_OK
     assert ab.onela_check_config(cfg(d_k=32, d_v=32, io_dtype=ab.ONELA_F32)) == ab.ONELA_OK
     assert ab.onela_check_config(cfg(num_v_heads=32)) == ab.ONELA_OK
+    for dk, dv in ((128, 256), (128, 512), (256, 256), (256, 512), (64, 64)):
+        assert ab.onela_check_config(cfg(d_k=dk, d_v=dv)) == ab.ONELA_OK, (dk, dv)
+    for dk, dv in ((128, 256), (256, 512)):  # wide shapes are bf16-only
+        assert ab.onela_check_config(cfg(d_k=dk, d_v=dv, io_dtype=ab.ONELA_F32)) == ab.ONELA_EINVAL
+    for dk, dv in ((256, 128), (128, 1024), (512, 512), (128, 384)):
+        assert ab.onela_check_config(cfg(d_k=dk, d_v=dv)) == ab.ONELA_EINVAL, (dk, dv)
     bad = [dict(num_v_heads=24, num_qk_heads=16), dict(d_k=96, d_v=96), dict(d_k=128, d_v=64),
            dict(max_beams=0), dict(max_beams=65537), dict(max_steps=0), dict(max_steps=9),
            dict(io_dtype=7), dict(num_requests=0), dict(num_qk_heads=0)]

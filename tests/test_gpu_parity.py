@@ -263,3 +263,41 @@ def test_prefill_matches_oracle(name):
     err = np.max(np.abs(got - ref)) / np.max(np.abs(ref))
     log(f"[prefill] {name} rel err {err:.2e}")
     assert err <= 1e-4
+
+
+# The paper's wider GDN geometries (d_k up to 256, d_v up to 512, grouped
+# heads), at sizes the oracle finishes in seconds, with ragged widths.
+WIDE = [
+    W.WorkloadSpec("k128_v256_gqa", 1, 4, 8, 128, 256, 48, (48, 40, 48), "bf16", "zipf", 1.1, seed=31),
+    W.WorkloadSpec("k128_v512", 2, 2, 4, 128, 512, 48, (40, 33, 40), "bf16", "uniform", seed=32),
+    W.WorkloadSpec("k256_v256", 1, 4, 4, 256, 256, 48, (32, 64, 50), "bf16", "zipf", 1.5, seed=33),
+    W.WorkloadSpec("k256_v512_gqa", 1, 2, 4, 256, 512, 48, (32, 20, 32, 17), "bf16", "uniform",
+                   seed=34),
+    W.WorkloadSpec("k64_v64_f32", 2, 2, 4, 64, 64, 48, (24, 30, 24), "f32", "uniform", seed=35),
+]
+
+
+@pytest.mark.parametrize("spec", WIDE, ids=[s.name for s in WIDE])
+def test_wide_geometries_match_oracle(spec):
+    log(f"[wide] {spec.name}")
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    anc = oracle_ancestry(wl)
+    for fused in (False, True):
+        o, g = run_gpu(wl, s0, fused=fused)
+        for t in range(spec.T):
+            assert np.array_equal(g[t], anc[t])
+        errs = [rel_err(o[t], ref[t]) for t in range(spec.T)]
+        log(f"[wide] {spec.name} fused={fused} max rel err {max(errs):.2e}")
+        assert max(errs) <= REL_TOL
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    base = runner.FullStateBaseline(spec, torch.from_numpy(s0).to(DEV), DEV)
+    outs = base.run(dw)
+    torch.cuda.synchronize()
+    for t in range(spec.T):
+        assert rel_err(outs[t].cpu().numpy(), ref[t]) <= REL_TOL
+    prompt = tuple(runner.device_tensor(x, DEV) for x in
+                   (wl.prompt_k, wl.prompt_v, wl.prompt_alpha, wl.prompt_beta))
+    got = runner.prefill_state(spec, prompt, DEV).cpu().numpy()
+    assert np.max(np.abs(got - s0)) / np.max(np.abs(s0)) <= 1e-4
