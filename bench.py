@@ -121,6 +121,32 @@ def fused_alg_bytes(wl, t):
     return b
 
 
+def fused_alg_bytes_delta(wl, t):
+    """Algorithmic HBM bytes of one fused step launch with transition records
+    (alpha, delta, k): S_ctx, q, o, the step's inputs read from the caller,
+    the key, gates and new delta written to the arena, the distinct ancestral
+    records (key, gates, delta) and the ancestry indices."""
+    s = wl.spec
+    io = 2 if s.io_dtype == "bf16" else 4
+    W = s.widths[t]
+    rec = s.HK * s.dk * io + s.HV * (s.dv * io + 8)  # key + delta + (alpha, beta) per slot
+    b = s.R * s.HV * s.dv * s.dk * 4                 # S_ctx
+    b += s.R * W * s.HK * s.dk * io                  # q
+    b += s.R * W * s.HV * s.dv * 4                   # o
+    b += slab_bytes(wl, t)                           # k_t, v_t, alpha_t, beta_t read
+    b += s.R * W * rec                               # k_t, delta_t, (alpha_t, beta_t) written
+    b += (sum(unique_record_slots(wl, t)) - s.R * W) * rec  # ancestral records
+    if t == 0:
+        b += s.R * s.HV * s.dv * s.dk * 4            # S_ctx split write
+    if t > 0:
+        b += s.R * W * 4 + unique_parents(wl, t) * (t - 1) * 4 + s.R * W * t * 4
+    return b
+
+
+def kernel_alg_bytes(wl, t, records):
+    return fused_alg_bytes(wl, t) if records == "inputs" else fused_alg_bytes_delta(wl, t)
+
+
 def step_alg_bytes(wl, fused=True):
     """Algorithmic bytes of one whole step (T decode steps; init moves none)."""
     s = wl.spec
@@ -187,6 +213,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--skip-fullstate", action="store_true")
+    ap.add_argument("--records", choices=("inputs", "delta"), default="inputs",
+                    help="record kind of the headline path (the other is timed as an A/B)")
+    ap.add_argument("--skip-ab", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -217,8 +246,8 @@ def main():
     s0 = runner.prefill_state(spec, dw0.prompt, dev, stream)
     torch.cuda.synchronize()
     NB = args.batches
-    cfg = runner.config_for(spec)
-    ws_bytes = ab.onela_workspace_bytes(cfg)
+    cfgs = {kind: runner.config_for(spec, records=kind) for kind in ("inputs", "delta")}
+    ws_bytes = max(ab.onela_workspace_bytes(c) for c in cfgs.values())
     batches = []
     for i in range(NB):
         steps = [runner.DeviceStep(st.q.clone(), st.k.clone(), st.v.clone(), st.alpha.clone(),
@@ -235,12 +264,9 @@ def main():
                     [getattr(st, f) for st in b["steps"] for f in ("q", "k", "v", "alpha", "beta")])
     log(f"[bench] {NB} batches, {footprint / 2**20:.0f} MiB resident")
 
-    def init_ctx(b):
-        return ab.onela_init(cfg, b["s0"], b["ws"], ws_bytes, None)
-
-    def one_step(b, fused):
+    def one_step(b, fused, kind):
         """init + T x (resolve, append, decode) on the current stream."""
-        ctx = init_ctx(b)
+        ctx = ab.onela_init(cfgs[kind], b["s0"], b["ws"], ws_bytes, None)
         for t, st in enumerate(b["steps"]):
             if fused:
                 ab.onela_decode_step_fused(ctx, t, st.width, st.parents, st.k, st.v, st.alpha,
@@ -260,11 +286,11 @@ def main():
         torch.cuda.synchronize()
         return g
 
-    def timed_steps(fused, K, warmup):
+    def timed_steps(fused, K, warmup, kind):
         """Exactly K steps (step i on batch i % NB); returns ms per step."""
         graphs = None
         if not args.no_graph:
-            graphs = [capture(lambda b=b: one_step(b, fused)) for b in batches]
+            graphs = [capture(lambda b=b: one_step(b, fused, kind)) for b in batches]
 
         def run(n, start):
             for i in range(n):
@@ -272,7 +298,7 @@ def main():
                 if graphs is not None:
                     graphs[k].replay()
                 else:
-                    one_step(batches[k], fused)
+                    one_step(batches[k], fused, kind)
 
         run(warmup, 0)
         torch.cuda.synchronize()
@@ -284,12 +310,13 @@ def main():
         return e0.elapsed_time(e1) / K
 
     K = args.steps
-    log(f"[bench] fused path: warmup {args.warmup}, {K} timed steps")
-    ms_per_step = timed_steps(True, K, args.warmup)
+    kind = args.records
+    log(f"[bench] fused path ({kind} records): warmup {args.warmup}, {K} timed steps")
+    ms_per_step = timed_steps(True, K, args.warmup, kind)
     beam_tokens_per_step = spec.R * sum(spec.widths)
     value = beam_tokens_per_step / (ms_per_step / 1e3)
     log(f"[bench] fused: {ms_per_step * 1e3:.1f} us/step")
-    ms_sep = timed_steps(False, K, args.warmup)
+    ms_sep = timed_steps(False, K, args.warmup, kind)
     log(f"[bench] separate calls: {ms_sep * 1e3:.1f} us/step")
 
     # ---- dominant-kernel roofline: the fused step kernel.  Per decode step t
@@ -299,20 +326,6 @@ def main():
     ctxs = [None] * NB
     rs = torch.cuda.Stream()  # contexts bound to the stream the graphs capture
 
-    def init_all():
-        for i, b in enumerate(batches):
-            ctxs[i] = ab.onela_init(cfg, b["s0"], b["ws"], ws_bytes, rs)
-
-    def fused_all(t):
-        for i, b in enumerate(batches):
-            st = b["steps"][t]
-            ab.onela_decode_step_fused(ctxs[i], t, st.width, st.parents, st.k, st.v,
-                                       st.alpha, st.beta, st.q, b["outs"][t])
-
-    # Graphs hold kernel arguments by value, so each one is captured with the
-    # host-side contexts already advanced to the step it replays; replaying
-    # step_graphs[0..T-1] redoes the whole sequence on the device (onela_init
-    # enqueues nothing).
     def capture_on_rs(fn):
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
@@ -321,28 +334,47 @@ def main():
         torch.cuda.synchronize()
         return g
 
-    step_graphs = []
-    for t in range(T):
-        with torch.cuda.stream(rs):
-            init_all()
-            for tt in range(t):
-                fused_all(tt)
-        step_graphs.append(capture_on_rs(lambda t=t: fused_all(t)))
-        for c in ctxs:
-            ab.onela_destroy(c)
-    torch.cuda.synchronize()
-    n_roof = max(4, args.steps // 20)
-    dec_ms = np.zeros((n_roof, T))
-    for i in range(n_roof):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
-        ev[0].record()
+    def fused_kernel_us(kind):
+        """Average fused-launch duration per decode step t (events around
+        NB back-to-back launches held in one graph per t)."""
+        def init_all():
+            for i, b in enumerate(batches):
+                ctxs[i] = ab.onela_init(cfgs[kind], b["s0"], b["ws"], ws_bytes, rs)
+
+        def fused_all(t):
+            for i, b in enumerate(batches):
+                st = b["steps"][t]
+                ab.onela_decode_step_fused(ctxs[i], t, st.width, st.parents, st.k, st.v,
+                                           st.alpha, st.beta, st.q, b["outs"][t])
+
+        # Graphs hold kernel arguments by value, so each one is captured with
+        # the host-side contexts already advanced to the step it replays;
+        # replaying step_graphs[0..T-1] redoes the whole sequence on the
+        # device (onela_init enqueues nothing).
+        step_graphs = []
         for t in range(T):
-            step_graphs[t].replay()
-            ev[t + 1].record()
+            with torch.cuda.stream(rs):
+                init_all()
+                for tt in range(t):
+                    fused_all(tt)
+            step_graphs.append(capture_on_rs(lambda t=t: fused_all(t)))
+            for c in ctxs:
+                ab.onela_destroy(c)
         torch.cuda.synchronize()
-        dec_ms[i] = [ev[t].elapsed_time(ev[t + 1]) / NB for t in range(T)]
-    dec_us = dec_ms[1:].mean(axis=0) * 1e3
-    bytes_t = [fused_alg_bytes(wl, t) for t in range(T)]
+        n_roof = max(4, args.steps // 20)
+        dec_ms = np.zeros((n_roof, T))
+        for i in range(n_roof):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
+            ev[0].record()
+            for t in range(T):
+                step_graphs[t].replay()
+                ev[t + 1].record()
+            torch.cuda.synchronize()
+            dec_ms[i] = [ev[t].elapsed_time(ev[t + 1]) / NB for t in range(T)]
+        return dec_ms[1:].mean(axis=0) * 1e3
+
+    dec_us = fused_kernel_us(kind)
+    bytes_t = [kernel_alg_bytes(wl, t, kind) for t in range(T)]
     achieved = sum(bytes_t) / (dec_us.sum() * 1e-6) / 1e9
     log(f"[bench] fused kernel us per t: {np.round(dec_us, 2).tolist()}  "
         f"alg MB: {[round(b / 1e6, 2) for b in bytes_t]}  -> {achieved:.0f} GB/s")
@@ -366,6 +398,7 @@ def main():
                    "parents": f"{spec.parents}{spec.zipf_s if spec.parents == 'zipf' else ''}",
                    "step": "onela_init + per t onela_decode_step_fused (resolve + append "
                            "+ decode in one launch)",
+                   "records": kind,
                    "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
                                   "fp32 accum",
                    "graph": not args.no_graph, "batches": NB},
@@ -380,10 +413,29 @@ def main():
                            "step_alg_bytes": step_alg_bytes(wl, fused=False)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "decode_kernel<FUSED>", "alg_bytes_per_t": bytes_t,
+                     "kernel": ("decode_kernel<FUSED>" if kind == "inputs"
+                                else "replay_kernel<FUSED>"),
+                     "alg_bytes_per_t": bytes_t,
                      "us_per_t": [round(float(x), 3) for x in dec_us],
                      "timing": f"HIP events around {NB} back-to-back launches per t"},
     }
+
+    # ---- A/B: the other record kind (inputs: k, v, alpha, beta with the
+    # backward query fold; delta: the paper's (alpha, delta, k) with forward
+    # replay), same workload and protocol
+    if not args.skip_ab:
+        other = "delta" if kind == "inputs" else "inputs"
+        ms_o = timed_steps(True, K, args.warmup, other)
+        us_o = fused_kernel_us(other)
+        bytes_o = [kernel_alg_bytes(wl, t, other) for t in range(T)]
+        result["record_kind_ab"] = {
+            "records": other, "ms_per_step": ms_o,
+            "beam_tokens_per_s": beam_tokens_per_step / (ms_o / 1e3),
+            "fused_kernel_us_per_t": [round(float(x), 3) for x in us_o],
+            "alg_bytes_per_t": bytes_o,
+            "achieved_GBs": sum(bytes_o) / (us_o.sum() * 1e-6) / 1e9}
+        log(f"[bench] A/B {other} records: {ms_o * 1e3:.1f} us/step, kernel us per t "
+            f"{np.round(us_o, 2).tolist()}")
 
     # ---- per-beam FullState GPU baseline
     if not args.skip_fullstate:
@@ -432,7 +484,7 @@ def main():
         del src, dst
     result["copy_ceiling"] = ceil
     result["roofline"]["frac_of_copy_ceiling_same_size"] = achieved / ceil["same_size"]["GB/s"]
-    traffic = measured_traffic(name)
+    traffic = measured_traffic(name) if kind == "inputs" else None
     if traffic is not None:
         result["roofline"]["traffic"] = float(np.mean(traffic))
         result["roofline"]["traffic_per_t"] = traffic

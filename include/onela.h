@@ -57,6 +57,16 @@ typedef enum {
 
 typedef enum { ONELA_F32 = 0, ONELA_BF16 = 1 } onela_dtype_t;
 
+/* What one record of the arena holds.
+ * ONELA_RECORD_INPUTS: the step's own inputs (k, v, alpha, beta); the decode
+ *   folds the query newest-to-oldest and applies S_ctx once (see above).
+ * ONELA_RECORD_DELTA: the paper's GDN transition record (alpha, delta, k) of
+ *   Sec. 3.2 (Eq. 2), delta_t = beta_t (v_t - alpha_t S_{t-1} k_t), computed
+ *   and appended by the decode step, which replays the ancestral records on
+ *   the two projections S_ctx q_t and S_ctx k_t (Eqs. 3-4).  delta is stored
+ *   in fp16 for bf16 io (fp32 for fp32 io). */
+typedef enum { ONELA_RECORD_INPUTS = 0, ONELA_RECORD_DELTA = 1 } onela_record_kind_t;
+
 /* Shape of one decode context.  Supported (d_k, d_v): (32, 32), (64, 64),
  * (128, 128) with io_dtype ONELA_BF16 or ONELA_F32, and (128, 256), (128, 512),
  * (256, 256), (256, 512) with ONELA_BF16; num_v_heads a multiple of num_qk_heads;
@@ -71,6 +81,7 @@ typedef struct {
   int32_t max_beams;    /* W_max: upper bound on every W_t */
   int32_t max_steps;    /* T_max: decode steps 0 .. T_max - 1 */
   int32_t io_dtype;     /* onela_dtype_t of q, k, v */
+  int32_t record_kind;  /* onela_record_kind_t */
 } onela_config_t;
 
 /* Human-readable name of a status code (static string). */
@@ -85,7 +96,8 @@ onela_status_t onela_check_config(const onela_config_t* cfg);
  * index [2][R][W_max][T_max] int32, S_ctx split into bf16 high/low halves
  * (written by the step-0 launch, read by later steps), and the record arena:
  * k [R][T_max][H_K][W_max][d_k], v [R][T_max][H_V][W_max][d_v] in the io
- * dtype and (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs. */
+ * dtype, (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs and, for
+ * ONELA_RECORD_DELTA, delta [R][T_max][H_V][W_max][d_v] (fp16 / fp32). */
 size_t onela_workspace_bytes(const onela_config_t* cfg);
 
 /* Creates a decode context and binds the shared post-prefill state

@@ -22,6 +22,7 @@ struct Shape {
   int R, HK, HV, dk, dv;
   int wmax, tmax;
   bool bf16;  // q/k/v stored as bf16 bits (else fp32)
+  bool delta;  // records are (alpha, delta, k) transition records (else step inputs)
   int io_bytes() const { return bf16 ? 2 : 4; }
 };
 
@@ -34,11 +35,12 @@ struct Arena {
   void* k;           // [R][tmax][HK][wmax][dk] io dtype
   void* v;           // [R][tmax][HV][wmax][dv] io dtype
   float2* ab;        // [R][tmax][HV][wmax] (alpha, beta)
+  void* d;           // delta records [R][tmax][HV][wmax][dv], fp16 (bf16 io) / fp32; or null
 };
 
 // Bytes of each region, in workspace order, each rounded up to 256.
 struct Layout {
-  size_t status, anc, s_frag, k, v, ab, total;
+  size_t status, anc, s_frag, k, v, ab, d, total;
 };
 Layout layout_of(const Shape& s);
 
@@ -56,6 +58,12 @@ hipError_t launch_fused_step(const Shape& s, int step, int width, int prev_width
                              const int* parents, const void* k, const void* v,
                              const float* alpha, const float* beta, const void* q, float* o,
                              int* gather_out, const Arena& a, hipStream_t st);
+hipError_t launch_replay_decode(const Shape& s, int step, int width, const void* q, float* o,
+                                const Arena& a, hipStream_t st);
+hipError_t launch_replay_fused(const Shape& s, int step, int width, int prev_width,
+                               const int* parents, const void* k, const void* v,
+                               const float* alpha, const float* beta, const void* q, float* o,
+                               int* gather_out, const Arena& a, hipStream_t st);
 hipError_t launch_prefill(const Shape& s, int prompt_len, const void* k,
                           const void* v, const float* alpha, const float* beta,
                           float* s0_out, hipStream_t st);

@@ -57,13 +57,12 @@
 // XCDs, so block id i runs on XCD i % 8; all beam tiles of a (request, head)
 // are mapped to one XCD so that head's shared state and records stay in that
 // XCD's L2.
+#include "device_common.h"
 #include "internal.h"
 
 namespace onela {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct DecodeParams {
   const void* q;
@@ -88,106 +87,6 @@ struct DecodeParams {
   int ntiles;   // beam tiles per (request, value head)
   int xcd_map;  // 1: XCD-aware block order (units % 8 == 0)
 };
-
-// Pointer to a byte offset from a base (32-bit offsets keep per-lane address
-// arithmetic in 32 bits; every region is smaller than 2 GiB).
-template <typename T>
-__device__ inline T* at(void* base, unsigned off) {
-  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
-}
-template <typename T>
-__device__ inline const T* at(const void* base, unsigned off) {
-  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
-}
-
-// N consecutive io elements (bf16 bits or fp32), raw, moved as whole
-// vectors of 8, 16 or 32 bytes.
-template <bool BF16, int N>
-struct RawV {
-  static constexpr int kWords = BF16 ? N / 2 : N;
-  static constexpr int kBytes = kWords * 4;
-  static_assert(kWords == 2 || kWords == 4 || kWords == 8, "8, 16 or 32 bytes");
-  unsigned w[kWords];
-  __device__ void load(const void* base, unsigned off) {
-    if constexpr (kWords == 2) {
-      const uint2 u = *at<uint2>(base, off);
-      w[0] = u.x; w[1] = u.y;
-    } else {
-#pragma unroll
-      for (int i = 0; i < kWords / 4; ++i) {
-        const uint4 u = *at<uint4>(base, off + 16 * i);
-        w[4 * i] = u.x; w[4 * i + 1] = u.y; w[4 * i + 2] = u.z; w[4 * i + 3] = u.w;
-      }
-    }
-  }
-  __device__ void store(void* base, unsigned off) const {
-    if constexpr (kWords == 2) {
-      *at<uint2>(base, off) = make_uint2(w[0], w[1]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < kWords / 4; ++i)
-        *at<uint4>(base, off + 16 * i) =
-            make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
-    }
-  }
-  __device__ void to_float(float* x) const {
-#pragma unroll
-    for (int i = 0; i < kWords; ++i) {
-      if constexpr (BF16) {
-        x[2 * i] = __uint_as_float(w[i] << 16);
-        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-      } else {
-        x[i] = __uint_as_float(w[i]);
-      }
-    }
-  }
-};
-
-__device__ inline unsigned pack_bf16x2(float a, float b) {
-  return unsigned(__builtin_bit_cast(unsigned short, static_cast<__bf16>(a))) |
-         (unsigned(__builtin_bit_cast(unsigned short, static_cast<__bf16>(b))) << 16);
-}
-
-__device__ inline float bf16_lo_to_float(unsigned u) { return __uint_as_float(u << 16); }
-__device__ inline float bf16_hi_to_float(unsigned u) { return __uint_as_float(u & 0xffff0000u); }
-
-// Split 8 floats into bf16 hi and lo vectors: hi = bf16(x), lo = bf16(x - hi).
-__device__ inline void split8(const float* x, uint4& hi, uint4& lo) {
-  unsigned h[4], l[4];
-  for (int i = 0; i < 4; ++i) {
-    h[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
-    l[i] = pack_bf16x2(x[2 * i] - bf16_lo_to_float(h[i]),
-                       x[2 * i + 1] - bf16_hi_to_float(h[i]));
-  }
-  hi = make_uint4(h[0], h[1], h[2], h[3]);
-  lo = make_uint4(l[0], l[1], l[2], l[3]);
-}
-
-template <int CTRL>
-__device__ inline float dpp(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
-                                                               CTRL, 0xF, 0xF, false));
-}
-
-// Sum over an aligned group of G consecutive lanes, result in every lane of
-// the group.  Within a 16-lane row the exchanges are DPP moves: swap
-// neighbours, swap pairs (quad permutes), then mirror within half-rows and
-// within the row; wider groups finish with cross-row shuffles.
-template <int G>
-__device__ inline float group_sum(float x) {
-  if constexpr (G >= 2) x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
-  if constexpr (G >= 4) x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
-  if constexpr (G >= 8) x += dpp<0x141>(x);  // row_half_mirror
-  if constexpr (G >= 16) x += dpp<0x140>(x); // row_mirror
-  if constexpr (G >= 32) x += __shfl_xor(x, 16);
-  if constexpr (G >= 64) x += __shfl_xor(x, 32);
-  return x;
-}
-
-__device__ inline f32x4 mfma_bf16(const uint4& a, const uint4& b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
 
 template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED>
 __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {

@@ -1,0 +1,578 @@
+// Large-beam GDN decode step with the paper's transition records (gfx950).
+//
+// Records are the GDN transition records of Sec. 3.2, r_j = (alpha_j, delta_j,
+// k_j) with delta_j = beta_j (v_j - alpha_j S_{j-1} k_j) (Eq. 2), stored once
+// per (step, slot) and never moved.  A decode step replays the beam's
+// ancestral records onto the two projections it needs (Eq. 3):
+//     u_q = S_ctx q_t,  u_k = S_ctx k_t;
+//     for j = 0..t-1:  u_q <- alpha_j u_q + delta_j (k_j . q_t)
+//                      u_k <- alpha_j u_k + delta_j (k_j . k_t)
+// and evaluates the step (Eq. 4):
+//     delta_t = beta_t (v_t - alpha_t u_k),  o_t = alpha_t u_q + delta_t (k_t . q_t),
+// appending r_t = (alpha_t, delta_t, k_t).  Unrolled, u = (prod_j alpha_j) S x
+// + sum_j w_j delta_j with w_j = (k_j . x) prod_{i>j} alpha_i, so every record
+// contributes independently: one dot product per (record, projection) and one
+// weighted d_v-vector per record.
+//
+// Layout of the work is the one of the input-record decode kernel (one
+// workgroup = request, value head, row slice, 32 beams; d_k/16 waves of 16*MB
+// state rows; XCD-aware block order; shared state split into bf16 hi/lo,
+// stored split by step 0).  The difference is the order of dependencies:
+// the contraction S_ctx [q_t | k_t] needs no record, so after one barrier
+// (the B fragments of q_t and k_t staged in LDS) the MFMAs run while the
+// ancestral records are still arriving; the record dots follow, a second
+// barrier publishes the per-beam scalars, and the epilogue applies Eq. 4.
+//
+// delta is stored in fp16 for bf16 inputs (fp32 for fp32 inputs): the paper's
+// record is a 32-bit decay with 16-bit delta and key vectors; bf16 would cost
+// ~8x more error.  MODE: DECODE reads the step-t record from the arena (after
+// onela_append_records); FUSED reads it from the caller and performs the
+// ancestry update and the append in the same launch.
+#include "device_common.h"
+#include "internal.h"
+
+namespace onela {
+namespace {
+
+struct ReplayParams {
+  const void* q;
+  float* o;
+  const int* parents;  // FUSED
+  const void* k_in;    // FUSED: the step's inputs
+  const void* v_in;
+  const float* alpha_in;
+  const float* beta_in;
+  int* gather_out;
+  int* status;
+  const float* s0;
+  uint4* s_frag;
+  void* ak;    // arena keys [R][tmax][HK][wmax][dk] io dtype
+  void* av;    // arena step inputs v (DECODE mode reads step t from here)
+  float2* ab;  // arena (alpha, beta)
+  void* ad;    // arena delta [R][tmax][HV][wmax][dv], fp16 (bf16 io) or fp32
+  const int* anc_rd;
+  int* anc_wr;
+  int R, HK, HV, G, W, W_prev, wmax, tmax;
+  int ntiles;
+  int xcd_map;
+};
+
+// delta rows: fp16 words for bf16 inputs, fp32 otherwise (same byte sizes as
+// the input rows, so RawV moves them).
+template <bool F16>
+__device__ inline void delta_to_float(const unsigned* w, float* x, int n) {
+  for (int i = 0; i < (F16 ? n / 2 : n); ++i) {
+    if constexpr (F16) {
+      x[2 * i] = float(__builtin_bit_cast(_Float16, static_cast<unsigned short>(w[i] & 0xffffu)));
+      x[2 * i + 1] = float(__builtin_bit_cast(_Float16, static_cast<unsigned short>(w[i] >> 16)));
+    } else {
+      x[i] = __uint_as_float(w[i]);
+    }
+  }
+}
+
+template <bool F16>
+__device__ inline void float_to_delta(const float* x, unsigned* w, int n) {
+  for (int i = 0; i < (F16 ? n / 2 : n); ++i) {
+    if constexpr (F16) {
+      const unsigned lo = __builtin_bit_cast(unsigned short, static_cast<_Float16>(x[2 * i]));
+      const unsigned hi = __builtin_bit_cast(unsigned short, static_cast<_Float16>(x[2 * i + 1]));
+      w[i] = lo | (hi << 16);
+    } else {
+      w[i] = __float_as_uint(x[i]);
+    }
+  }
+}
+
+template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED>
+__global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
+  constexpr int MB = DVW / DK;
+  constexpr int NS = DV / DVW;
+  constexpr int NW = DVW / (16 * MB);
+  constexpr int RPL = 4 * MB;
+  constexpr int NT = NW * 64;
+  constexpr int BEAMS = 16 * NBLK;
+  constexpr int LPB = NT / BEAMS;    // fold lanes per beam
+  constexpr int EPL = DK / LPB;      // key elements per fold lane
+  constexpr int C8 = EPL / 8;
+  constexpr int KS = DK / 32;
+  constexpr int NA = CHAIN - 1;
+  constexpr int NAX = NA > 0 ? NA : 1;
+  constexpr unsigned IOB = BF16 ? 2 : 4;
+  constexpr int HL = BF16 ? 1 : 2;   // bf16 inputs are exact in bf16: no low half
+  static_assert(MB * DK == DVW && NS * DVW == DV && EPL % 8 == 0, "tiling");
+  static_assert(LPB <= 64 && (LPB & (LPB - 1)) == 0, "fold lane group within a wave");
+
+  __shared__ uint4 b_lds[2][HL][NBLK][KS][4][16];  // [q | k_t][hi | lo] B fragments
+  constexpr int NSC = 4 + 2 * NAX;
+  __shared__ float sc_lds[BEAMS][NSC];             // decay, alpha_t, beta_t, k_t.q, w_q[], w_k[]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  if constexpr (NA == 0) {
+    if (blockIdx.x == 0 && tid == 0) p.status[0] = 0;
+  }
+
+  int unit, st;
+  const int nst = NS * p.ntiles;
+  if (p.xcd_map) {
+    const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    unit = x + 8 * (slot / nst);
+    st = slot % nst;
+  } else {
+    unit = blockIdx.x / nst;
+    st = blockIdx.x % nst;
+  }
+  const int slice = st / p.ntiles;
+  const int tile = st - slice * p.ntiles;
+  const int r = unit / p.HV;
+  const int hv = unit - r * p.HV;
+  const int hk = hv / p.G;
+  const int b0 = tile * BEAMS;
+  const int W = p.W;
+  const int wmax = p.wmax, tmax = p.tmax;
+
+  const int fb = tid / LPB;
+  const int li = tid - fb * LPB;
+  const int fbeam = b0 + fb;
+  const bool fvalid = fbeam < W;
+  const int fbc = fvalid ? fbeam : 0;
+  const int g4 = lane >> 4;
+  const unsigned row0 = DVW * slice + 16 * MB * w + RPL * g4;
+  int sbc[NBLK];
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) {
+    const int sb = b0 + nb * 16 + (lane & 15);
+    sbc[nb] = sb < W ? sb : 0;
+  }
+
+  const int* anc_r = p.anc_rd + long(r) * wmax * tmax;
+  const unsigned kslot = DK * IOB, vslot = DV * IOB;
+  auto k_slab = [&](int j) {
+    return static_cast<char*>(p.ak) + ((long(r) * tmax + j) * p.HK + hk) * wmax * long(kslot);
+  };
+  auto v_slab = [&](int j) {
+    return static_cast<char*>(p.av) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
+  };
+  auto d_slab = [&](int j) {  // delta rows use the input row size (fp16 / fp32)
+    return static_cast<char*>(p.ad) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
+  };
+  auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
+
+  // ---- round 1: indices, then query and the beam's step-t inputs
+  int fsrc[NAX], ssrc[NBLK][NAX];
+  bool fpok = true, spok[NBLK];
+  int fpar = 0, spar[NBLK];
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) spok[nb] = true;
+  if constexpr (NA > 0) {
+    if constexpr (FUSED) {
+      const int* prow = p.parents + long(r) * W;
+      fpar = prow[fbc];
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) spar[nb] = prow[sbc[nb]];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+        for (int j = 0; j < NA; ++j) ssrc[nb][j] = anc_r[sbc[nb] * tmax + j];
+    }
+  }
+  using K8 = RawV<BF16, 8>;
+  using VR = RawV<BF16, RPL>;
+  K8 qr[C8], kt[C8];
+  K8 kr[NAX][C8];
+  float alr[NAX];
+  float2 abt;
+  VR vt[NBLK];
+  VR dr[NBLK][NAX];
+  {
+    const unsigned qoff = ((unsigned(r) * W + fbc) * p.HK + hk) * kslot + li * EPL * IOB;
+#pragma unroll
+    for (int c = 0; c < C8; ++c) qr[c].load(p.q, qoff + c * K8::kBytes);
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int c = 0; c < C8; ++c) kt[c].load(p.k_in, qoff + c * K8::kBytes);
+      const unsigned gi = (unsigned(r) * W + fbc) * p.HV + hv;
+      abt = make_float2(p.alpha_in[gi], p.beta_in[gi]);
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb)
+        vt[nb].load(p.v_in, ((unsigned(r) * W + sbc[nb]) * p.HV + hv) * vslot + row0 * IOB);
+    } else {
+      const char* ks = k_slab(NA);
+#pragma unroll
+      for (int c = 0; c < C8; ++c)
+        kt[c].load(ks, fbc * kslot + li * EPL * IOB + c * K8::kBytes);
+      abt = ab_slab(NA)[fbc];
+      const char* vs = v_slab(NA);
+#pragma unroll
+      for (int nb = 0; nb < NBLK; ++nb) vt[nb].load(vs, sbc[nb] * vslot + row0 * IOB);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- ancestral records: keys and decays for the dots (fold lanes), delta
+  // rows for the epilogue.  FUSED: the parent's own step-(t-1) record first.
+  bool fok[NAX];
+  auto load_rec = [&](int j, int slot) {
+    const char* ks = k_slab(j);
+#pragma unroll
+    for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
+    alr[j] = ab_slab(j)[slot].x;
+  };
+  if constexpr (FUSED && NA > 0) {
+    fpok = unsigned(fpar) < unsigned(p.W_prev);
+    const int pf = fpok ? fpar : 0;
+    fsrc[NA - 1] = pf;
+    fok[NA - 1] = fpok;
+    load_rec(NA - 1, pf);
+    int ps[NBLK];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
+      ps[nb] = spok[nb] ? spar[nb] : 0;
+      ssrc[nb][NA - 1] = ps[nb];
+      dr[nb][NA - 1].load(d_slab(NA - 1), ps[nb] * vslot + row0 * IOB);
+    }
+#pragma unroll
+    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps[nb] * tmax + j];
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < NA - 1; ++j) {
+      fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
+      load_rec(j, fok[j] ? fsrc[j] : 0);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) {
+        const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
+        dr[nb][j].load(d_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+      }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      fok[j] = unsigned(fsrc[j]) < unsigned(wmax);
+      load_rec(j, fok[j] ? fsrc[j] : 0);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+      for (int j = 0; j < NA; ++j) {
+        const bool ok = unsigned(ssrc[nb][j]) < unsigned(wmax);
+        dr[nb][j].load(d_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+      }
+  }
+
+  // ---- shared-state rows (A fragments), as in the input-record kernel
+  float4 Araw[NA == 0 ? KS : 1][MB][2];
+  uint4 A[KS][MB][2];
+  uint4* const frag =
+      p.s_frag + ((long(unit) * NS + slice) * NW + w) * (KS * MB * 2 * 64) + lane;
+  if constexpr (NA == 0) {
+    const int m = lane & 15;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const unsigned row = DVW * slice + 16 * MB * w + 4 * MB * (m >> 2) + 4 * mb + (m & 3);
+        const unsigned off = ((unsigned(unit) * DV + row) * DK + 32 * ks + 8 * (lane >> 4)) * 4u;
+        Araw[ks][mb][0] = *at<float4>(p.s0, off);
+        Araw[ks][mb][1] = *at<float4>(p.s0, off + 16);
+      }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int hl = 0; hl < 2; ++hl) A[ks][mb][hl] = frag[((ks * MB + mb) * 2 + hl) * 64];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 1: stage q_t and k_t as MFMA B fragments
+  float qf[EPL], kf[EPL];
+#pragma unroll
+  for (int c = 0; c < C8; ++c) {
+    qr[c].to_float(qf + 8 * c);
+    kt[c].to_float(kf + 8 * c);
+    const int k0 = li * EPL + 8 * c;
+    uint4 hi, lo;
+    split8(qf + 8 * c, hi, lo);
+    b_lds[0][0][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = hi;
+    if constexpr (HL == 2) b_lds[0][1][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = lo;
+    split8(kf + 8 * c, hi, lo);
+    b_lds[1][0][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = hi;
+    if constexpr (HL == 2) b_lds[1][1][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = lo;
+  }
+  if constexpr (NA == 0) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float x[8] = {Araw[ks][mb][0].x, Araw[ks][mb][0].y, Araw[ks][mb][0].z,
+                            Araw[ks][mb][0].w, Araw[ks][mb][1].x, Araw[ks][mb][1].y,
+                            Araw[ks][mb][1].z, Araw[ks][mb][1].w};
+        split8(x, A[ks][mb][0], A[ks][mb][1]);
+        if (tile == 0)
+#pragma unroll
+          for (int hl = 0; hl < 2; ++hl) frag[((ks * MB + mb) * 2 + hl) * 64] = A[ks][mb][hl];
+      }
+  }
+  __syncthreads();
+
+  // ---- phase 2: u_q = S_ctx q_t, u_k = S_ctx k_t on MFMA (no record needed)
+  f32x4 accq[NBLK][MB], acck[NBLK][MB];
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      accq[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acck[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+    for (int nb = 0; nb < NBLK; ++nb) {
+      const uint4 bq = b_lds[0][0][nb][ks][g4][lane & 15];
+      const uint4 bk = b_lds[1][0][nb][ks][g4][lane & 15];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        accq[nb][mb] = mfma_bf16(A[ks][mb][1], bq, accq[nb][mb]);
+        acck[nb][mb] = mfma_bf16(A[ks][mb][1], bk, acck[nb][mb]);
+        if constexpr (HL == 2) {
+          const uint4 bql = b_lds[0][1][nb][ks][g4][lane & 15];
+          const uint4 bkl = b_lds[1][1][nb][ks][g4][lane & 15];
+          accq[nb][mb] = mfma_bf16(A[ks][mb][0], bql, accq[nb][mb]);
+          acck[nb][mb] = mfma_bf16(A[ks][mb][0], bkl, acck[nb][mb]);
+        }
+        accq[nb][mb] = mfma_bf16(A[ks][mb][0], bq, accq[nb][mb]);
+        acck[nb][mb] = mfma_bf16(A[ks][mb][0], bk, acck[nb][mb]);
+      }
+    }
+  }
+
+  // ---- phase 3: record dots and per-beam scalars (independent across j)
+  {
+    float c0 = 0.f, c1 = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; e += 2) {
+      c0 = fmaf(kf[e], qf[e], c0);
+      c1 = fmaf(kf[e + 1], qf[e + 1], c1);
+    }
+    const float cqt = group_sum<LPB>(c0 + c1);
+    float cq[NAX], ck[NAX];
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      float kj[EPL];
+#pragma unroll
+      for (int c = 0; c < C8; ++c) kr[j][c].to_float(kj + 8 * c);
+      float a0 = 0.f, a1 = 0.f, b0v = 0.f, b1v = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; e += 2) {
+        a0 = fmaf(kj[e], qf[e], a0);
+        a1 = fmaf(kj[e + 1], qf[e + 1], a1);
+        b0v = fmaf(kj[e], kf[e], b0v);
+        b1v = fmaf(kj[e + 1], kf[e + 1], b1v);
+      }
+      cq[j] = group_sum<LPB>(a0 + a1);
+      ck[j] = group_sum<LPB>(b0v + b1v);
+    }
+    if (li == 0) {
+      float decay = 1.f;  // prod of the decays of records newer than j
+#pragma unroll
+      for (int j = NA - 1; j >= 0; --j) {
+        const float aj = fok[j] ? alr[j] : 1.f;
+        sc_lds[fb][4 + j] = fok[j] ? decay * cq[j] : 0.f;
+        sc_lds[fb][4 + NAX + j] = fok[j] ? decay * ck[j] : 0.f;
+        decay *= aj;
+      }
+      sc_lds[fb][0] = decay;
+      sc_lds[fb][1] = abt.x;
+      sc_lds[fb][2] = abt.y;
+      sc_lds[fb][3] = cqt;
+    }
+  }
+
+  // ---- FUSED: index h_t and the step-t key and gates into the context
+  if constexpr (FUSED) {
+    if (fvalid && slice == 0) {
+      if (hv == 0 && li == 0 && NA > 0) {
+        int* dst = p.anc_wr + (long(r) * wmax + fbeam) * tmax;
+        int* g = p.gather_out ? p.gather_out + (long(r) * W + fbeam) * NA : nullptr;
+#pragma unroll
+        for (int j = 0; j < NA; ++j) {
+          const int h = fpok ? fsrc[j] : -1;
+          dst[j] = h;
+          if (g) g[j] = h;
+        }
+        if (!fpok) atomicOr(p.status, kStatusParent);
+      }
+      if (hv % p.G == 0) {
+        char* ks = k_slab(NA);
+#pragma unroll
+        for (int c = 0; c < C8; ++c)
+          kt[c].store(ks, fbeam * kslot + li * EPL * IOB + c * K8::kBytes);
+      }
+      if (li == 0) ab_slab(NA)[fbeam] = abt;
+    }
+  }
+  __syncthreads();
+
+  // ---- phase 4: Eq. 4 per output row; append delta_t
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) {
+    const int bl = nb * 16 + (lane & 15);
+    const int sb = b0 + bl;
+    const float decay = sc_lds[bl][0], at_ = sc_lds[bl][1], bt = sc_lds[bl][2],
+                cqt = sc_lds[bl][3];
+    float uq[RPL], uk[RPL];
+#pragma unroll
+    for (int e = 0; e < RPL; ++e) {
+      uq[e] = decay * accq[nb][e >> 2][e & 3];
+      uk[e] = decay * acck[nb][e >> 2][e & 3];
+    }
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      const float wq = sc_lds[bl][4 + j], wk = sc_lds[bl][4 + NAX + j];
+      float dj[RPL];
+      delta_to_float<BF16>(dr[nb][j].w, dj, RPL);
+#pragma unroll
+      for (int e = 0; e < RPL; ++e) {
+        uq[e] = fmaf(wq, dj[e], uq[e]);
+        uk[e] = fmaf(wk, dj[e], uk[e]);
+      }
+    }
+    float vf[RPL], dt[RPL], ov[RPL];
+    vt[nb].to_float(vf);
+#pragma unroll
+    for (int e = 0; e < RPL; ++e) {
+      dt[e] = bt * (vf[e] - at_ * uk[e]);
+      ov[e] = fmaf(dt[e], cqt, at_ * uq[e]);
+    }
+    if (sb < W) {
+      float4* dst = at<float4>(p.o, (((unsigned(r) * W + sb) * p.HV + hv) * DV + row0) * 4u);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+        dst[i] = make_float4(ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]);
+      VR dw;
+      float_to_delta<BF16>(dt, dw.w, RPL);
+      dw.store(d_slab(NA), sb * vslot + row0 * IOB);
+    }
+  }
+}
+
+template <int DK, int DV, int DVW, bool BF16, bool FUSED>
+hipError_t launch_chain(int chain, const ReplayParams& prm, unsigned blocks, hipStream_t st) {
+  constexpr int NBLK = kDecodeBeamBlocks;
+  constexpr int threads = 4 * DK;
+  switch (chain) {
+#define ONELA_CHAIN_CASE(C)                                                              \
+  case C:                                                                               \
+    replay_kernel<DK, DV, DVW, NBLK, C, BF16, FUSED><<<blocks, threads, 0, st>>>(prm);  \
+    break;
+    ONELA_CHAIN_CASE(1)
+    ONELA_CHAIN_CASE(2)
+    ONELA_CHAIN_CASE(3)
+    ONELA_CHAIN_CASE(4)
+    ONELA_CHAIN_CASE(5)
+    ONELA_CHAIN_CASE(6)
+    ONELA_CHAIN_CASE(7)
+    ONELA_CHAIN_CASE(8)
+#undef ONELA_CHAIN_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <bool FUSED>
+hipError_t launch_mode(const Shape& s, int step, const ReplayParams& prm, unsigned units,
+                       hipStream_t st) {
+  const int chain = step + 1;
+#define ONELA_SHAPE(DK, DV, DVW)                                                          \
+  if (s.dk == DK && s.dv == DV) {                                                        \
+    const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
+    return s.bf16 ? launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st)      \
+                  : launch_chain<DK, DV, DVW, false, FUSED>(chain, prm, blocks, st);    \
+  }
+#define ONELA_SHAPE_BF16(DK, DV, DVW)                                                     \
+  if (s.dk == DK && s.dv == DV && s.bf16) {                                              \
+    const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
+    return launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st);               \
+  }
+  ONELA_SHAPE(32, 32, 32)
+  ONELA_SHAPE(64, 64, 64)
+  ONELA_SHAPE(128, 128, 128)
+  ONELA_SHAPE_BF16(128, 256, 256)
+  ONELA_SHAPE_BF16(128, 512, 256)
+  ONELA_SHAPE_BF16(256, 256, 256)
+  ONELA_SHAPE_BF16(256, 512, 256)
+#undef ONELA_SHAPE
+#undef ONELA_SHAPE_BF16
+  return hipErrorInvalidValue;
+}
+
+ReplayParams base_params(const Shape& s, int width, const void* q, float* o, const Arena& a,
+                         unsigned* units_out) {
+  constexpr int BEAMS = 16 * kDecodeBeamBlocks;
+  ReplayParams prm = {};
+  prm.q = q;
+  prm.o = o;
+  prm.s0 = a.s0;
+  prm.s_frag = reinterpret_cast<uint4*>(a.s_frag);
+  prm.ak = a.k;
+  prm.av = a.v;
+  prm.ab = a.ab;
+  prm.ad = a.d;
+  prm.status = a.status;
+  prm.R = s.R;
+  prm.HK = s.HK;
+  prm.HV = s.HV;
+  prm.G = s.HV / s.HK;
+  prm.W = width;
+  prm.wmax = s.wmax;
+  prm.tmax = s.tmax;
+  prm.ntiles = (width + BEAMS - 1) / BEAMS;
+  const int units = s.R * s.HV;
+  prm.xcd_map = (units % 8 == 0) ? 1 : 0;
+  *units_out = unsigned(units);
+  return prm;
+}
+
+}  // namespace
+
+hipError_t launch_replay_decode(const Shape& s, int step, int width, const void* q, float* o,
+                                const Arena& a, hipStream_t st) {
+  unsigned units;
+  ReplayParams prm = base_params(s, width, q, o, a, &units);
+  prm.anc_rd = a.anc[step & 1];
+  return launch_mode<false>(s, step, prm, units, st);
+}
+
+hipError_t launch_replay_fused(const Shape& s, int step, int width, int prev_width,
+                               const int* parents, const void* k, const void* v,
+                               const float* alpha, const float* beta, const void* q, float* o,
+                               int* gather_out, const Arena& a, hipStream_t st) {
+  unsigned units;
+  ReplayParams prm = base_params(s, width, q, o, a, &units);
+  prm.parents = parents;
+  prm.k_in = k;
+  prm.v_in = v;
+  prm.alpha_in = alpha;
+  prm.beta_in = beta;
+  prm.gather_out = gather_out;
+  prm.W_prev = prev_width;
+  prm.anc_rd = a.anc[(step + 1) & 1];
+  prm.anc_wr = a.anc[step & 1];
+  return launch_mode<true>(s, step, prm, units, st);
+}
+
+}  // namespace onela

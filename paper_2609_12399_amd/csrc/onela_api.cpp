@@ -38,8 +38,11 @@ onela_status_t shape_of(const onela_config_t* c, Shape* s) {
   if (c->max_beams < 1 || c->max_beams > 65536) return ONELA_EINVAL;
   if (c->max_steps < 1 || c->max_steps > onela::kMaxSteps) return ONELA_EINVAL;
   if (c->io_dtype != ONELA_F32 && c->io_dtype != ONELA_BF16) return ONELA_EINVAL;
-  Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads, c->d_k, c->d_v,
-          c->max_beams,    c->max_steps,    c->io_dtype == ONELA_BF16};
+  if (c->record_kind != ONELA_RECORD_INPUTS && c->record_kind != ONELA_RECORD_DELTA)
+    return ONELA_EINVAL;
+  Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads,
+          c->d_k,          c->d_v,          c->max_beams,
+          c->max_steps,    c->io_dtype == ONELA_BF16, c->record_kind == ONELA_RECORD_DELTA};
   if (!onela::decode_supported(t)) return ONELA_EINVAL;
   // the kernels form 32-bit byte offsets: every region must stay below 2 GiB
   const double big = double(t.R) * t.tmax * (t.HV > t.HK ? t.HV : t.HK) * t.wmax *
@@ -66,7 +69,8 @@ Layout layout_of(const Shape& s) {
   l.k = round256(size_t(s.io_bytes()) * R * T * s.HK * W * s.dk);
   l.v = round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
   l.ab = round256(sizeof(float2) * R * T * s.HV * W);
-  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab;
+  l.d = s.delta ? l.v : 0;  // delta rows take the size of input v rows (fp16 / fp32)
+  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab + l.d;
   return l;
 }
 
@@ -130,6 +134,8 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   c->arena.v = p;
   p += l.v;
   c->arena.ab = reinterpret_cast<float2*>(p);
+  p += l.ab;
+  c->arena.d = s.delta ? p : nullptr;
 
   c->status_live = false;
   *out = c;
@@ -184,8 +190,11 @@ onela_status_t onela_decode_step(onela_ctx_t c, int32_t step, const void* q, flo
   if (!c) return ONELA_EINVAL;
   if (step < 0 || step != c->resolved || step != c->appended) return ONELA_ESTEP;
   if (!q || !o || !aligned16(q) || !aligned16(o)) return ONELA_EINVAL;
-  hipError_t e = onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
-                                      c->stream);
+  hipError_t e = c->shape.delta
+                     ? onela::launch_replay_decode(c->shape, step, c->widths[step], q, o,
+                                                   c->arena, c->stream)
+                     : onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
+                                            c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
   if (step == 0) c->status_live = true;
   return ONELA_OK;
@@ -207,9 +216,11 @@ onela_status_t onela_decode_step_fused(onela_ctx_t c, int32_t step, int32_t widt
   if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta) || !aligned16(q) ||
       !aligned16(o))
     return ONELA_EINVAL;
-  hipError_t e = onela::launch_fused_step(s, step, width, step > 0 ? c->widths[step - 1] : 0,
-                                          parents, k, v, alpha, beta, q, o, gather_out,
-                                          c->arena, c->stream);
+  const int prev = step > 0 ? c->widths[step - 1] : 0;
+  hipError_t e = s.delta ? onela::launch_replay_fused(s, step, width, prev, parents, k, v, alpha,
+                                                      beta, q, o, gather_out, c->arena, c->stream)
+                         : onela::launch_fused_step(s, step, width, prev, parents, k, v, alpha,
+                                                    beta, q, o, gather_out, c->arena, c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
   c->widths[step] = width;
   c->resolved = step;

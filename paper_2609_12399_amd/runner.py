@@ -67,9 +67,9 @@ def to_device(wl: Workload, device="cuda:0", with_prompt: bool = True) -> Device
 
 
 def config_for(spec: WorkloadSpec, max_beams: int | None = None,
-               max_steps: int | None = None) -> ab.onela_config_t:
+               max_steps: int | None = None, records: str = "inputs") -> ab.onela_config_t:
     return ab.make_config(spec.R, spec.HK, spec.HV, spec.dk, spec.dv,
-                          max_beams or spec.W, max_steps or spec.T, spec.io_dtype)
+                          max_beams or spec.W, max_steps or spec.T, spec.io_dtype, records)
 
 
 def prefill_state(spec: WorkloadSpec, prompt, device="cuda:0", stream=None):
@@ -86,10 +86,11 @@ class Decoder:
     """One decode context (workspace + onela_ctx_t) bound to a stream."""
 
     def __init__(self, spec: WorkloadSpec, s0, device="cuda:0", stream=None,
-                 max_beams: int | None = None, max_steps: int | None = None):
+                 max_beams: int | None = None, max_steps: int | None = None,
+                 records: str = "inputs"):
         torch = _torch()
         self.spec = spec
-        self.cfg = config_for(spec, max_beams, max_steps)
+        self.cfg = config_for(spec, max_beams, max_steps, records)
         self.ws_bytes = ab.onela_workspace_bytes(self.cfg)
         if self.ws_bytes == 0:
             raise ab.OnelaError(ab.ONELA_EINVAL, "onela_workspace_bytes")
