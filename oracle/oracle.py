@@ -163,3 +163,28 @@ def decode(S0, q, k, v, alpha, beta, parents, *, nthreads: int | None = None,
         out.append(o[off:off + n].reshape(int(widths[t]), HV, dv).copy())
         off += n
     return out
+
+
+def select_beams(scores, width: int):
+    """Global top-W beam selection of one request (Sec. 2.1: every live beam
+    is expanded over the codebook and the global top-W candidates are kept).
+
+    scores [W_prev][V] -> (parents [width], tokens [width], kept scores
+    [width]), in rank order.  Order: higher score first; equal scores by lower
+    flat index p * V + v; -0.0 ranks below +0.0 (IEEE total order) and NaN
+    below every number.  Implemented as a plain sort of (score, index) pairs.
+    """
+    s = np.asarray(scores, dtype=np.float32)
+    P, V = s.shape
+    flat = s.reshape(-1)
+    if not 1 <= width <= flat.size:
+        raise ValueError("width must be in [1, W_prev * V]")
+    isnan = np.isnan(flat)
+    sign = np.signbit(flat)
+    idx = np.arange(flat.size)
+    vals = np.where(isnan, 0.0, flat.astype(np.float64))
+    # lexsort: last key is primary.  Primary: not-NaN first; then value
+    # descending; then +0 before -0; then index ascending.
+    order = np.lexsort((idx, sign, -vals, isnan))
+    top = order[:width]
+    return (top // V).astype(np.int32), (top % V).astype(np.int32), flat[top]

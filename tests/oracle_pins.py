@@ -444,6 +444,53 @@ def pin_backward_fold_matches(lib, seed=19):
     return worst
 
 
+
+
+def _select_bruteforce(s, width):
+    """Python's sorted() over explicit tuples: (NaN last, value desc, +0 before
+    -0, index asc)."""
+    flat = [float(x) for x in np.asarray(s, dtype=np.float32).reshape(-1)]
+    V = s.shape[1]
+
+    def key(i):
+        x = flat[i]
+        if math.isnan(x):
+            return (1, 0.0, 0, i)
+        return (0, -x, 1 if math.copysign(1.0, x) < 0 else 0, i)
+
+    top = sorted(range(len(flat)), key=key)[:width]
+    return [i // V for i in top], [i % V for i in top]
+
+
+def pin_select_beams(lib=None, seed=20, select=None):
+    """Top-W selection against brute force on small inputs with many ties
+    (integer-valued scores), signed zeros, infinities and NaN; W = N keeps
+    everything in order; all-equal scores keep the lowest indices."""
+    select = select or orc.select_beams
+    rng = np.random.default_rng(seed)
+    for trial in range(60):
+        P, V = int(rng.integers(1, 7)), int(rng.integers(1, 9))
+        s = rng.integers(-3, 4, size=(P, V)).astype(np.float32)
+        if trial % 3 == 0:
+            s[rng.random((P, V)) < 0.2] = -0.0
+        if trial % 4 == 0:
+            s[rng.random((P, V)) < 0.1] = np.inf
+            s[rng.random((P, V)) < 0.1] = -np.inf
+            s[rng.random((P, V)) < 0.1] = np.nan
+        width = int(rng.integers(1, P * V + 1))
+        par, tok, sc = select(s, width)
+        bp, bt = _select_bruteforce(s, width)
+        assert list(par) == bp and list(tok) == bt, trial
+        assert np.array_equal(sc, s[par, tok], equal_nan=True)
+    s = np.zeros((4, 5), dtype=np.float32)
+    par, tok, _ = select(s, 7)
+    assert list(par * 5 + tok) == list(range(7))
+    s = rng.standard_normal((3, 4)).astype(np.float32)
+    par, tok, sc = select(s, 12)
+    assert np.all(np.diff(sc) <= 0) and sorted(par * 4 + tok) == list(range(12))
+    return 0.0
+
+
 ALL_PINS = [
     pin_exact_rational_bruteforce,
     pin_identity_gates_give_context_readout,
@@ -455,4 +502,5 @@ ALL_PINS = [
     pin_prefill_closed_form,
     pin_ancestry_pointer_chasing,
     pin_backward_fold_matches,
+    pin_select_beams,
 ]

@@ -69,3 +69,31 @@ def test_mutant_is_caught(tmp_path, name, orig, mut):
     with np.errstate(all="ignore"):
         failed = _pins_fail(lib)
     assert failed, f"mutant {name} passed every pin"
+
+
+# Mistakes planted in the beam-selection oracle (a numpy function): each is a
+# textual edit of its source, executed in a scratch namespace.
+SELECT_MUTANTS = [
+    ("ties_by_highest_index", "np.lexsort((idx, sign, -vals, isnan))",
+     "np.lexsort((-idx, sign, -vals, isnan))"),
+    ("signed_zero_ignored", "np.lexsort((idx, sign, -vals, isnan))",
+     "np.lexsort((idx, -vals, isnan))"),
+    ("nan_ranked_first", "np.lexsort((idx, sign, -vals, isnan))",
+     "np.lexsort((idx, sign, -vals, ~isnan))"),
+    ("ascending_scores", "np.lexsort((idx, sign, -vals, isnan))",
+     "np.lexsort((idx, sign, vals, isnan))"),
+    ("parent_token_swapped", "return (top // V).astype(np.int32), (top % V)",
+     "return (top % V).astype(np.int32), (top // V)"),
+]
+
+
+@pytest.mark.parametrize("name,orig,mut", SELECT_MUTANTS, ids=[m[0] for m in SELECT_MUTANTS])
+def test_select_mutant_is_caught(name, orig, mut):
+    import inspect
+    import textwrap
+    src = textwrap.dedent(inspect.getsource(orc.select_beams))
+    assert src.count(orig) == 1, f"mutation anchor not unique/present: {name}"
+    ns = {"np": np}
+    exec(compile(src.replace(orig, mut), f"<mutant {name}>", "exec"), ns)
+    with pytest.raises(AssertionError):
+        pins.pin_select_beams(select=ns["select_beams"])
