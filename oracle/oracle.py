@@ -165,22 +165,29 @@ def decode(S0, q, k, v, alpha, beta, parents, *, nthreads: int | None = None,
     return out
 
 
-def select_beams(scores, width: int):
+def select_beams(scores, width: int, beam_scores=None):
     """Global top-W beam selection of one request (Sec. 2.1: every live beam
     is expanded over the codebook and the global top-W candidates are kept).
 
-    scores [W_prev][V] -> (parents [width], tokens [width], kept scores
-    [width]), in rank order.  Order: higher score first; equal scores by lower
-    flat index p * V + v; -0.0 ranks below +0.0 (IEEE total order) and NaN
-    below every number.  Implemented as a plain sort of (score, index) pairs.
+    scores [W_prev][V] (fp32); beam_scores optional [W_prev] (fp32).  The
+    candidate score of (p, v) is scores[p][v], or beam_scores[p] +
+    scores[p][v] rounded once to fp32 when beam_scores is given.  Returns
+    (parents [width], tokens [width], candidate scores [width]) in rank order.
+    Order: higher score first; equal scores by lower flat index p * V + v;
+    -0.0 ranks below +0.0; NaN (of either sign) below every number, NaNs among
+    themselves by flat index.  Implemented as a plain sort of (score, index)
+    pairs.
     """
     s = np.asarray(scores, dtype=np.float32)
     P, V = s.shape
+    if beam_scores is not None:
+        b = np.asarray(beam_scores, dtype=np.float32).reshape(P, 1)
+        s = (b + s).astype(np.float32)
     flat = s.reshape(-1)
     if not 1 <= width <= flat.size:
         raise ValueError("width must be in [1, W_prev * V]")
     isnan = np.isnan(flat)
-    sign = np.signbit(flat)
+    sign = np.signbit(flat) & ~isnan
     idx = np.arange(flat.size)
     vals = np.where(isnan, 0.0, flat.astype(np.float64))
     # lexsort: last key is primary.  Primary: not-NaN first; then value

@@ -446,11 +446,18 @@ def pin_backward_fold_matches(lib, seed=19):
 
 
 
-def _select_bruteforce(s, width):
+def _select_bruteforce(s, width, beam=None):
     """Python's sorted() over explicit tuples: (NaN last, value desc, +0 before
-    -0, index asc)."""
-    flat = [float(x) for x in np.asarray(s, dtype=np.float32).reshape(-1)]
-    V = s.shape[1]
+    -0, index asc).  With beam scores, each candidate is one fp32 addition of
+    two fp32 scalars."""
+    s = np.asarray(s, dtype=np.float32)
+    P, V = s.shape
+    flat = []
+    for p in range(P):
+        for v in range(V):
+            x = s[p, v] if beam is None else np.float32(beam[p]) + s[p, v]
+            assert isinstance(x, np.float32)
+            flat.append(float(x))
 
     def key(i):
         x = flat[i]
@@ -464,11 +471,12 @@ def _select_bruteforce(s, width):
 
 def pin_select_beams(lib=None, seed=20, select=None):
     """Top-W selection against brute force on small inputs with many ties
-    (integer-valued scores), signed zeros, infinities and NaN; W = N keeps
-    everything in order; all-equal scores keep the lowest indices."""
+    (integer-valued scores), signed zeros, infinities and NaN of both signs,
+    with and without beam scores; W = N keeps everything in order; all-equal
+    scores keep the lowest indices."""
     select = select or orc.select_beams
     rng = np.random.default_rng(seed)
-    for trial in range(60):
+    for trial in range(80):
         P, V = int(rng.integers(1, 7)), int(rng.integers(1, 9))
         s = rng.integers(-3, 4, size=(P, V)).astype(np.float32)
         if trial % 3 == 0:
@@ -477,17 +485,32 @@ def pin_select_beams(lib=None, seed=20, select=None):
             s[rng.random((P, V)) < 0.1] = np.inf
             s[rng.random((P, V)) < 0.1] = -np.inf
             s[rng.random((P, V)) < 0.1] = np.nan
+            s[rng.random((P, V)) < 0.1] = -np.nan
+        beam = None
+        if trial % 2 == 1:
+            beam = rng.integers(-2, 3, size=P).astype(np.float32)
+            beam[rng.random(P) < 0.3] = -0.0
+            if trial % 5 == 1:
+                beam += np.float32(0.375)
         width = int(rng.integers(1, P * V + 1))
-        par, tok, sc = select(s, width)
-        bp, bt = _select_bruteforce(s, width)
+        par, tok, sc = select(s, width, beam_scores=beam)
+        bp, bt = _select_bruteforce(s, width, beam)
         assert list(par) == bp and list(tok) == bt, trial
-        assert np.array_equal(sc, s[par, tok], equal_nan=True)
+        ref = s[par, tok] if beam is None else beam[par] + s[par, tok]
+        assert np.array_equal(sc, ref, equal_nan=True)
     s = np.zeros((4, 5), dtype=np.float32)
     par, tok, _ = select(s, 7)
     assert list(par * 5 + tok) == list(range(7))
     s = rng.standard_normal((3, 4)).astype(np.float32)
     par, tok, sc = select(s, 12)
     assert np.all(np.diff(sc) <= 0) and sorted(par * 4 + tok) == list(range(12))
+    # -0.0 + +0.0 is +0.0 under round-to-nearest: a zero beam score turns a
+    # -0.0 log-probability into +0.0, which then ranks with the +0.0 entries.
+    s = np.array([[-0.0, 0.0]], dtype=np.float32)
+    par, tok, sc = select(s, 2, beam_scores=np.zeros(1, dtype=np.float32))
+    assert list(tok) == [0, 1] and not np.signbit(sc).any()
+    par, tok, _ = select(s, 2)
+    assert list(tok) == [1, 0]
     return 0.0
 
 

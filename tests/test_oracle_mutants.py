@@ -82,6 +82,8 @@ SELECT_MUTANTS = [
      "np.lexsort((idx, sign, -vals, ~isnan))"),
     ("ascending_scores", "np.lexsort((idx, sign, -vals, isnan))",
      "np.lexsort((idx, sign, vals, isnan))"),
+    ("nan_sign_kept", "sign = np.signbit(flat) & ~isnan", "sign = np.signbit(flat)"),
+    ("beam_score_ignored", "s = (b + s).astype(np.float32)", "s = s"),
     ("parent_token_swapped", "return (top // V).astype(np.int32), (top % V)",
      "return (top % V).astype(np.int32), (top // V)"),
 ]
