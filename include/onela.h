@@ -220,6 +220,37 @@ onela_status_t onela_fullstate_step(const onela_config_t* cfg, int32_t step,
                                     size_t workspace_bytes, int32_t* status_word,
                                     void* stream);
 
+/* ---- Global beam selection (Sec. 2.1) ------------------------------------
+ * After a decode step every live beam p < W_prev of a request is expanded
+ * over the V entries of the SID codebook, and the global top-W candidates
+ * become the next step's beams: candidate (p, v) has flat index p * V + v and
+ * score beam_scores[p] + logp[p][v] (one fp32 addition; logp[p][v] alone when
+ * beam_scores is NULL).  Order: higher score first, equal scores by lower
+ * flat index, -0.0 below +0.0, every NaN below every number (NaNs among
+ * themselves by flat index).  The result is unique.
+ *   logp         device fp32 [R][W_prev][V]
+ *   beam_scores  device fp32 [R][W_prev], or NULL
+ *   parents_out  device int32 [R][W]: p of the b-th best candidate, i.e. the
+ *                pi(b) that onela_resolve_ancestry takes for the next step
+ *   tokens_out   device int32 [R][W]: its codebook entry v
+ *   scores_out   device fp32 [R][W]: its candidate score (bit-exact)
+ *   workspace    device, >= the size from onela_select_workspace_bytes,
+ *                256-byte aligned (may be NULL when that size is 0); owned
+ *                by the caller, used only during the enqueued work
+ *   stream       hipStream_t (NULL: the default stream)
+ * Limits: 1 <= R <= 65536, 1 <= W <= min(4096, W_prev * V),
+ * W_prev * V <= 2^29.  All pointers 4-byte aligned.  Enqueued asynchronously;
+ * the inputs must stay valid until the work has run.
+ * Errors: ONELA_EINVAL (limits, pointers), ONELA_ECAPACITY (workspace too
+ * small), ONELA_EHIP. */
+onela_status_t onela_select_workspace_bytes(int32_t num_requests, int32_t prev_width,
+                                            int32_t vocab, int32_t width, size_t* bytes);
+onela_status_t onela_select_beams(int32_t num_requests, int32_t prev_width, int32_t vocab,
+                                  int32_t width, const float* logp,
+                                  const float* beam_scores, int32_t* parents_out,
+                                  int32_t* tokens_out, float* scores_out, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
 /* ---- Capacity model (host only) -----------------------------------------
  * Persistent recurrent-state bytes after `steps` decode steps for one GDN
  * layer (Sec. 4.4): one S_ctx per request and value head (state_bytes per

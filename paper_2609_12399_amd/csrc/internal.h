@@ -76,4 +76,25 @@ hipError_t launch_fullstate(const Shape& s, int step, int width, int prev_width,
 // True when the decode kernel has an instance for this shape.
 bool decode_supported(const Shape& s);
 
+// ---- global top-W beam selection ------------------------------------------
+constexpr int kSelectThreads = 512;            // one workgroup
+constexpr int kSelectChunk = 16384;            // candidates per workgroup
+constexpr int kSelectMaxWidth = 4096;          // W kept per request
+constexpr int kSelectMaxStages = 16;           // reduction stages before the final one
+constexpr unsigned kSelectMaxCandidates = 1u << 29;  // W_prev * V per request
+
+// Launch plan: stage s reads n[s] candidates per request in chunks[s] chunks
+// and writes out[s] (key, index) pairs per request into workspace buffer
+// s % 2; the final launch reads the last n_final (<= kSelectChunk).
+struct SelectPlan {
+  int stages;
+  unsigned n[kSelectMaxStages], chunks[kSelectMaxStages], out[kSelectMaxStages];
+  unsigned n_final;
+  size_t buf_bytes[2], total;
+};
+bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan);
+hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int vocab, int width,
+                         const float* logp, const float* beam, int* parents, int* tokens,
+                         float* scores, void* workspace, hipStream_t st);
+
 }  // namespace onela

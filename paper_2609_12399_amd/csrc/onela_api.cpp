@@ -311,4 +311,43 @@ uint64_t onela_fullstate_capacity_bytes(int32_t R, int32_t HV, int32_t dk, int32
   return uint64_t(R) * beams * HV * uint64_t(dv) * dk * state_bytes;
 }
 
+onela_status_t onela_select_workspace_bytes(int32_t num_requests, int32_t prev_width,
+                                            int32_t vocab, int32_t width, size_t* bytes) {
+  if (!bytes) return ONELA_EINVAL;
+  *bytes = 0;
+  onela::SelectPlan plan;
+  if (num_requests < 1 || num_requests > 65536 || prev_width < 1 || vocab < 1 || width < 1)
+    return ONELA_EINVAL;
+  const uint64_t n = uint64_t(prev_width) * uint64_t(vocab);
+  if (n > onela::kSelectMaxCandidates ||
+      !onela::select_plan(num_requests, unsigned(n), unsigned(width), &plan))
+    return ONELA_EINVAL;
+  *bytes = plan.total;
+  return ONELA_OK;
+}
+
+onela_status_t onela_select_beams(int32_t num_requests, int32_t prev_width, int32_t vocab,
+                                  int32_t width, const float* logp, const float* beam_scores,
+                                  int32_t* parents_out, int32_t* tokens_out, float* scores_out,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  size_t need = 0;
+  const onela_status_t st =
+      onela_select_workspace_bytes(num_requests, prev_width, vocab, width, &need);
+  if (st != ONELA_OK) return st;
+  if (!logp || !parents_out || !tokens_out || !scores_out || !aligned4(logp) ||
+      !aligned4(parents_out) || !aligned4(tokens_out) || !aligned4(scores_out))
+    return ONELA_EINVAL;
+  if (beam_scores && !aligned4(beam_scores)) return ONELA_EINVAL;
+  if (need > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0))
+    return ONELA_EINVAL;
+  if (workspace_bytes < need) return ONELA_ECAPACITY;
+  onela::SelectPlan plan;
+  onela::select_plan(num_requests, unsigned(prev_width) * unsigned(vocab), unsigned(width),
+                     &plan);
+  const hipError_t e = onela::launch_select(plan, num_requests, prev_width, vocab, width, logp,
+                                            beam_scores, parents_out, tokens_out, scores_out,
+                                            workspace, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ONELA_OK : ONELA_EHIP;
+}
+
 }  // extern "C"

@@ -30,7 +30,8 @@ EXPORTED = ["onela_status_str", "onela_check_config", "onela_workspace_bytes", "
             "onela_reset", "onela_resolve_ancestry", "onela_append_records",
             "onela_decode_step", "onela_decode_step_fused", "onela_get_device_status", "onela_destroy",
             "onela_prefill_state", "onela_fullstate_workspace_bytes", "onela_fullstate_step",
-            "onela_capacity_bytes", "onela_fullstate_capacity_bytes"]
+            "onela_capacity_bytes", "onela_fullstate_capacity_bytes",
+            "onela_select_workspace_bytes", "onela_select_beams"]
 
 
 class OnelaError(RuntimeError):
@@ -90,6 +91,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                   ctypes.c_size_t, _P, _P], _I32),
         "onela_capacity_bytes": ([_I32] * 8, ctypes.c_uint64),
         "onela_fullstate_capacity_bytes": ([_I32] * 6, ctypes.c_uint64),
+        "onela_select_workspace_bytes": ([_I32] * 4 + [ctypes.POINTER(ctypes.c_size_t)], _I32),
+        "onela_select_beams": ([_I32] * 4 + [_P] * 6 + [ctypes.c_size_t, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -227,3 +230,23 @@ def onela_fullstate_capacity_bytes(num_requests, num_v_heads, d_k, d_v, beams,
                                    state_bytes) -> int:
     return load_library().onela_fullstate_capacity_bytes(num_requests, num_v_heads, d_k, d_v,
                                                          beams, state_bytes)
+
+
+def onela_select_workspace_bytes(num_requests: int, prev_width: int, vocab: int,
+                                 width: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().onela_select_workspace_bytes(num_requests, prev_width, vocab, width,
+                                                        ctypes.byref(out)),
+           "onela_select_workspace_bytes")
+    return out.value
+
+
+def onela_select_beams(num_requests: int, prev_width: int, vocab: int, width: int, logp,
+                       beam_scores, parents_out, tokens_out, scores_out, workspace=None,
+                       workspace_bytes: int = 0, stream=None):
+    _check(load_library().onela_select_beams(
+        num_requests, prev_width, vocab, width, _dev(logp, "logp"),
+        _dev(beam_scores, "beam_scores", optional=True), _dev(parents_out, "parents_out"),
+        _dev(tokens_out, "tokens_out"), _dev(scores_out, "scores_out"),
+        _dev(workspace, "workspace", optional=True), int(workspace_bytes), _stream(stream)),
+        "onela_select_beams")

@@ -167,3 +167,26 @@ class FullStateBaseline:
                                     self.ws_bytes, self.status_word, self.stream)
             prev = st.width
         return outs
+
+
+class BeamSelector:
+    """Global top-W beam selection (onela_select_beams) for fixed
+    (R, W_prev, V, W): owns the workspace and the three output tensors."""
+
+    def __init__(self, R: int, prev_width: int, vocab: int, width: int, device="cuda:0",
+                 stream=None):
+        torch = _torch()
+        self.R, self.prev_width, self.vocab, self.width = R, prev_width, vocab, width
+        self.ws_bytes = ab.onela_select_workspace_bytes(R, prev_width, vocab, width)
+        self.workspace = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+                          if self.ws_bytes else None)
+        self.parents = torch.empty((R, width), dtype=torch.int32, device=device)
+        self.tokens = torch.empty((R, width), dtype=torch.int32, device=device)
+        self.scores = torch.empty((R, width), dtype=torch.float32, device=device)
+        self.stream = stream
+
+    def __call__(self, logp, beam_scores=None):
+        ab.onela_select_beams(self.R, self.prev_width, self.vocab, self.width, logp,
+                              beam_scores, self.parents, self.tokens, self.scores,
+                              self.workspace, self.ws_bytes, self.stream)
+        return self.parents, self.tokens, self.scores

@@ -209,3 +209,46 @@ def with_widths(spec: WorkloadSpec | str, widths, **kw) -> WorkloadSpec:
     d["widths"] = tuple(int(w) for w in widths)
     d.update(kw)
     return WorkloadSpec(**d)
+
+
+# ---- beam-selection inputs ---------------------------------------------------
+# The scores a model hands to global beam selection (Sec. 2.1): per live beam,
+# log-probabilities over the SID codebook, plus the beam's running score.  The
+# paper fixes neither the codebook size nor the model, so these stand in for
+# them: logits ~ N(0, sigma^2) with sigma = 2, turned into log-probabilities
+# by a numerically stable log-softmax over the codebook (fp64, then rounded
+# once to fp32), and beam scores ~ -|N(0, 4)| sorted descending (the previous
+# selection keeps beams in rank order).  Other kinds stress the ordering:
+# "ties" draws integers in [-3, 3] (most candidates tie), "special" is
+# log-softmax with 2% of the entries replaced by each of -0.0, +0.0, +inf,
+# -inf, +NaN and -NaN.
+
+SELECT_CODEBOOK = 8192
+
+
+def make_select_inputs(R: int, prev_width: int, vocab: int, seed: int,
+                       kind: str = "logsoftmax", with_beam: bool = True):
+    """(logp fp32 [R][W_prev][V], beam fp32 [R][W_prev] or None)."""
+    rng = np.random.default_rng(seed)
+    shape = (R, prev_width, vocab)
+    if kind == "ties":
+        logp = rng.integers(-3, 4, size=shape).astype(np.float32)
+    else:
+        x = rng.standard_normal(shape) * 2.0
+        m = x.max(axis=-1, keepdims=True)
+        logp = (x - m - np.log(np.exp(x - m).sum(axis=-1, keepdims=True))).astype(np.float32)
+        if kind == "special":
+            u = rng.random(shape)
+            specials = [-0.0, 0.0, np.inf, -np.inf, np.nan, -np.nan]
+            for j, val in enumerate(specials):
+                logp[(u >= 0.02 * j) & (u < 0.02 * (j + 1))] = np.float32(val)
+        elif kind != "logsoftmax":
+            raise ValueError(kind)
+    beam = None
+    if with_beam:
+        if kind == "ties":
+            beam = rng.integers(-2, 3, size=(R, prev_width)).astype(np.float32)
+        else:
+            b = -np.abs(rng.standard_normal((R, prev_width)) * 2.0)
+            beam = (-np.sort(-b, axis=-1)).astype(np.float32)
+    return logp, beam

@@ -141,3 +141,46 @@ def test_binding_rejects_host_tensors():
         ab._dev(torch.zeros(4), "x")
     assert ab._dev(None, "x", optional=True) is None
     assert ab._dev(1234, "x") == 1234
+
+
+def _select_plan_bytes(R, P, V, W, chunk=16384):
+    """Workspace model of the beam selection: a reduction tree of per-chunk
+    top-W stages, (key, index) pairs of 8 bytes ping-ponged between two
+    256-byte-aligned buffers, until at most one chunk is left."""
+    n, s, buf = P * V, 0, [0, 0]
+    while n > chunk:
+        chunks = -(-n // chunk)
+        out = (chunks - 1) * W + min(W, n - (chunks - 1) * chunk)
+        buf[s % 2] = max(buf[s % 2], R * out * 8)
+        n, s = out, s + 1
+    return sum(-(-b // 256) * 256 for b in buf)
+
+
+@pytest.mark.parametrize("R,P,V,W", [(1, 3, 5, 7), (2, 8, 2048, 4096), (1, 512, 8192, 512),
+                                     (3, 37, 1001, 300), (1, 1024, 4096, 4096),
+                                     (4, 1024, 4096, 1024), (1, 1, 16385, 17),
+                                     (7, 65536, 8192, 4096)])
+def test_select_workspace_bytes(lib, R, P, V, W):
+    assert ab.onela_select_workspace_bytes(R, P, V, W) == _select_plan_bytes(R, P, V, W)
+
+
+def test_select_host_errors(lib):
+    out = ctypes.c_size_t(123)
+    ws = lib.onela_select_workspace_bytes
+    assert ws(1, 4, 4, 17, ctypes.byref(out)) == ab.ONELA_EINVAL and out.value == 0  # W > N
+    assert ws(1, 4096, 4096, 4097, ctypes.byref(out)) == ab.ONELA_EINVAL  # W > 4096
+    assert ws(0, 4, 4, 1, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert ws(65537, 4, 4, 1, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert ws(1, 1 << 15, 1 << 15, 1, ctypes.byref(out)) == ab.ONELA_EINVAL  # N > 2^29
+    assert ws(1, 4, 4, 0, ctypes.byref(out)) == ab.ONELA_EINVAL
+    assert ws(1, 4, 4, 1, None) == ab.ONELA_EINVAL
+    sb = lib.onela_select_beams
+    big = 1 << 30
+    assert sb(1, 512, 8192, 513 * 0, 256, None, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, None, None, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 258, None, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 256, 258, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 256, None, None, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, None, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, 128, big, None) == ab.ONELA_EINVAL
+    assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, 256, 1024, None) == ab.ONELA_ECAPACITY
