@@ -83,14 +83,18 @@ constexpr int kSelectMaxWidth = 4096;          // W kept per request
 constexpr int kSelectMaxStages = 16;           // reduction stages before the final one
 constexpr unsigned kSelectMaxCandidates = 1u << 29;  // W_prev * V per request
 
-// Launch plan: stage s reads n[s] candidates per request in chunks[s] chunks
-// and writes out[s] (key, index) pairs per request into workspace buffer
-// s % 2; the final launch reads the last n_final (<= kSelectChunk).
+// Launch plan.  Stage 0 reads the raw scores in nwg[0] chunks of
+// kSelectChunk per request; stage s >= 1 reads the nin[s] output slots of
+// stage s - 1, `group` slots per workgroup.  Every stage workgroup writes one
+// slot of `cap` (key, index) pairs plus a count into buffer s % 2 of the
+// workspace.  The final launch reads final_in slots (or, with no stage, the
+// final_in raw scores) per request.
 struct SelectPlan {
   int stages;
-  unsigned n[kSelectMaxStages], chunks[kSelectMaxStages], out[kSelectMaxStages];
-  unsigned n_final;
-  size_t buf_bytes[2], total;
+  unsigned nin[kSelectMaxStages], nwg[kSelectMaxStages];
+  unsigned final_in;
+  unsigned cap, group;
+  size_t pair_off[2], count_off[2], total;
 };
 bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan);
 hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int vocab, int width,

@@ -6,24 +6,30 @@
 // candidates are kept, best first.  The order is total: higher score first,
 // equal scores by lower flat index, -0.0 below +0.0, every NaN below every
 // number.  It is realised on an unsigned 32-bit key that is monotone in the
-// score (sign-magnitude flip; all NaNs map to 0) plus the flat index.
+// score (sign-magnitude flip; all NaNs map to 0), then on the flat index.
 //
 // The work is HBM-bound (N = W_prev * V fp32 scores per request, read once),
-// so it is organised as a reduction tree of exact selections rather than a
-// global sort:
-//   * stage kernel: one 512-thread workgroup per chunk of 16384 candidates
-//     keeps that chunk's top min(W, n) candidates, written as (key, index)
-//     pairs in index order.  Any candidate of the global top W is in the
-//     top W of its own chunk, so each stage shrinks the set by 16384 / W
-//     without losing one.
-//   * final kernel: one workgroup per request selects the top W of the last
-//     <= 16384 candidates, sorts them (bitonic, in LDS) and writes parents,
-//     tokens and scores.
-// Inside a workgroup, selection is a three-pass radix select on the key
-// (11 + 11 + 10 bits) with LDS histograms; the boundary key's ties are
-// resolved by an index-ordered scan (ballot + mbcnt per wave, one 256-entry
-// scan across (element slot, wave)), so the result is deterministic and needs
-// no global atomics.
+// so it is organised as a reduction tree of filters rather than a global
+// sort.  A 512-thread workgroup holds 16384 candidates (32 per lane):
+//   * stage kernel: keeps a superset of its candidates' top min(W, n) and
+//     writes it, in index order, to an output slot of `cap` (key, index)
+//     pairs plus a count.  A 2048-bin histogram of the maxima of groups of
+//     4 consecutive slots of a lane gives a key that at least need of the
+//     candidates reach; everything below it is dropped, so no member of the
+//     top need is lost and about need survive.  When the survivors do not
+//     fit the slot, the exact cut is taken instead (radix select over the
+//     workgroup).
+//   * final kernel: one workgroup per request filters the last <= 16384
+//     candidates the same way, sorts the survivors on the composite (key,
+//     complemented index) -- eight runs sorted in registers, one per wave,
+//     then each value ranked by binary searches in the other runs -- and
+//     writes the first W.
+// The stage input of stage s >= 1 is the slot array of stage s - 1; a
+// workgroup reads 16384 / cap consecutive slots.  Slots hold increasing index
+// ranges, so position order inside a workgroup is index order, which is what
+// the tie rule needs.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace onela {
@@ -31,31 +37,114 @@ namespace {
 
 constexpr int kThreads = kSelectThreads;
 constexpr int kWaves = kThreads / 64;
-constexpr int kNI = kSelectChunk / kThreads;  // candidates per thread
-static_assert(kNI * kWaves == 256, "the index-ordered scan covers 256 (slot, wave) entries");
+constexpr int kNI = kSelectChunk / kThreads;  // candidates per lane
+constexpr int kSortCap = 4096;                // survivors the final kernel sorts
+constexpr int kMaxSlotsPerGroup = 256;
+static_assert(kNI == 32, "validity masks are 32-bit");
 
 struct SelectParams {
-  const float* logp;     // [R][N] log-probabilities, N = W_prev * V
-  const float* beam;     // [R][W_prev] beam scores, or null
-  const uint2* cand_in;  // [R][n_in] (key, flat index) pairs in index order; null: read logp
-  uint2* cand_out;       // [R][out_stride] (stage kernel)
-  int* parents;          // [R][W] (final kernel)
+  const float* logp;        // [R][N] log-probabilities, N = W_prev * V
+  const float* beam;        // [R][W_prev] beam scores, or null
+  const uint2* cand_in;     // [R][nslots_in][cap] (key, flat index); null: read logp
+  const unsigned* cnt_in;   // [R][nslots_in]
+  uint2* cand_out;          // [R][nwg][cap]        (stage kernel)
+  unsigned* cnt_out;        // [R][nwg]
+  int* parents;             // [R][W]               (final kernel)
   int* tokens;
   float* scores;
-  unsigned N, V, W_prev;
-  unsigned n_in;        // input candidates per request
-  unsigned nchunks;     // chunks per request (stage kernel)
-  unsigned out_stride;  // output pairs per request (stage kernel)
-  unsigned W;
-  double inv_v;  // 1 / V
+  unsigned N, V, W_prev, W;
+  unsigned cap, lcap;       // slot capacity (a power of two) and its log2
+  unsigned group;           // input slots per workgroup (16384 / cap)
+  unsigned nslots_in;       // input slots per request (slot input)
+  unsigned nwg;             // workgroups per request
+  double inv_v;             // 1 / V
 };
 
 struct alignas(16) SelShared {
-  unsigned hist[2048];
+  unsigned hist[2048];  // exact cut: one 2048-bin histogram; bound: 8 x 256 bins
   unsigned tab[kNI * kWaves + 4];
-  unsigned wsum[kWaves];
+  unsigned red[2][kWaves];
+  unsigned scnt[kMaxSlotsPerGroup];
   unsigned digit, need, cnt;
 };
+
+// ---- wave-level helpers (DPP) ----------------------------------------------
+
+template <int CTRL, int ROWS = 0xF>
+__device__ inline unsigned dppu(unsigned x) {
+  return unsigned(__builtin_amdgcn_update_dpp(0, int(x), CTRL, ROWS, 0xF, false));
+}
+
+__device__ inline unsigned lane_id() { return threadIdx.x & 63; }
+
+__device__ inline unsigned mbcnt(unsigned long long m) {
+  return __builtin_amdgcn_mbcnt_hi(unsigned(m >> 32), __builtin_amdgcn_mbcnt_lo(unsigned(m), 0u));
+}
+
+// Inclusive prefix sum over the 64 lanes.
+__device__ inline unsigned wave_scan(unsigned x) {
+  x += dppu<0x111>(x);       // row_shr:1
+  x += dppu<0x112>(x);       // row_shr:2
+  x += dppu<0x114>(x);       // row_shr:4
+  x += dppu<0x118>(x);       // row_shr:8
+  x += dppu<0x142, 0xA>(x);  // row_bcast:15 into rows 1, 3
+  x += dppu<0x143, 0xC>(x);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+// (sum, min, max) over the 64 lanes, wave-uniform.
+struct Red3 {
+  unsigned sum, lo, hi;
+};
+__device__ inline Red3 wave_reduce(unsigned s, unsigned lo, unsigned hi) {
+#define ONELA_RED_STEP(C)            \
+  {                                  \
+    s += dppu<C>(s);                 \
+    lo = min(lo, dppu<C>(lo));       \
+    hi = max(hi, dppu<C>(hi));       \
+  }
+  ONELA_RED_STEP(0xB1)   // quad_perm [1,0,3,2]
+  ONELA_RED_STEP(0x4E)   // quad_perm [2,3,0,1]
+  ONELA_RED_STEP(0x141)  // row_half_mirror
+  ONELA_RED_STEP(0x140)  // row_mirror
+#undef ONELA_RED_STEP
+  Red3 r{0u, ~0u, 0u};
+#pragma unroll
+  for (int row = 0; row < 4; ++row) {
+    r.sum += unsigned(__builtin_amdgcn_readlane(int(s), 16 * row));
+    r.lo = min(r.lo, unsigned(__builtin_amdgcn_readlane(int(lo), 16 * row)));
+    r.hi = max(r.hi, unsigned(__builtin_amdgcn_readlane(int(hi), 16 * row)));
+  }
+  return r;
+}
+
+// (sum, min, max) over the workgroup.
+__device__ inline Red3 block_reduce(SelShared& sh, unsigned s, unsigned lo, unsigned hi) {
+  const Red3 w = wave_reduce(s, lo, hi);
+  const unsigned wv = threadIdx.x >> 6;
+  if (lane_id() == 0) {
+    sh.tab[wv] = w.sum;
+    sh.red[0][wv] = w.lo;
+    sh.red[1][wv] = w.hi;
+  }
+  __syncthreads();
+  Red3 r{0u, ~0u, 0u};
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    r.sum += sh.tab[i];
+    r.lo = min(r.lo, sh.red[0][i]);
+    r.hi = max(r.hi, sh.red[1][i]);
+  }
+  __syncthreads();
+  return r;
+}
+
+// x >> s for 0 <= s <= 32 (a shift by 32 gives 0).
+__device__ inline unsigned shr(unsigned x, int s) {
+  return unsigned(static_cast<unsigned long long>(x) >> s);
+}
+
+// ---- keys ------------------------------------------------------------------
 
 // Monotone key of an fp32 score: larger score -> larger key, -0 < +0, every
 // NaN -> 0 (below -inf, whose key is 0x007fffff).
@@ -74,251 +163,525 @@ __device__ inline unsigned row_of(unsigned idx, unsigned V, double inv_v) {
   return p;
 }
 
-template <bool BEAM>
-__device__ inline float candidate_score(const float* logp_r, const float* beam_r, unsigned idx,
-                                        unsigned V, double inv_v) {
-  const float x = logp_r[idx];
-  if constexpr (BEAM) return beam_r[row_of(idx, V, inv_v)] + x;
-  return x;
-}
+// ---- index-ordered compaction ----------------------------------------------
 
-__device__ inline unsigned lane_id() { return threadIdx.x & 63; }
+// Ranks of the flagged elements (bit i of f: slot i) in position order, slot i
+// of a lane sitting at position i * kThreads + threadIdx.x.  plan() takes the
+// ballots and scans the 256 (slot, wave) counts; apply() calls fn(i, rank).
+// The caller puts a barrier between apply() and the next use of sh.tab.
+struct Ordered {
+  unsigned pre[kNI / 4];  // wave-local ranks, 8 bits each
+  unsigned total;
+};
 
-__device__ inline unsigned mbcnt(unsigned long long m) {
-  return __builtin_amdgcn_mbcnt_hi(unsigned(m >> 32), __builtin_amdgcn_mbcnt_lo(unsigned(m), 0u));
-}
-
-// hist[bin] += 1 for every lane with act.  The two most frequent cases of
-// many lanes hitting one bin (narrow score distributions) are aggregated with
-// a ballot so that one lane adds the count; the rest use LDS atomics.  Must be
-// reached by all lanes of the wave.
-__device__ inline void hist_add(unsigned* hist, unsigned bin, bool act) {
-  unsigned long long pend = __ballot(act);
-#pragma unroll
-  for (int round = 0; round < 2; ++round) {
-    if (pend == 0) return;
-    const int leader = __builtin_ctzll(pend);
-    const unsigned b = __builtin_amdgcn_readlane(bin, leader);
-    const unsigned long long same = __ballot(act && bin == b);
-    if (lane_id() == unsigned(leader)) atomicAdd(&hist[b], unsigned(__popcll(same)));
-    if (bin == b) act = false;
-    pend &= ~same;
-  }
-  if (act) atomicAdd(&hist[bin], 1u);
-}
-
-// After a histogram pass: the bin where the running count from the top first
-// reaches `need`.  Publishes (digit, need - count above it, bin count).
-__device__ inline void find_bin(SelShared& sh, unsigned need) {
-  const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
-  const uint4 h = reinterpret_cast<const uint4*>(sh.hist)[t];  // bins 4t .. 4t+3
-  const unsigned s = h.x + h.y + h.z + h.w;
-  unsigned suf = s;  // sum over lanes >= lane of this wave
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const unsigned y = __shfl_down(suf, d);
-    if (lane + d < 64) suf += y;
-  }
-  if (lane == 0) sh.wsum[w] = suf;
-  __syncthreads();
-  unsigned above = suf - s;
-  for (unsigned w2 = w + 1; w2 < unsigned(kWaves); ++w2) above += sh.wsum[w2];
-  const unsigned hb[4] = {h.x, h.y, h.z, h.w};
-#pragma unroll
-  for (int b = 3; b >= 0; --b) {
-    if (above < need && need <= above + hb[b]) {
-      sh.digit = 4 * t + b;
-      sh.need = need - above;
-      sh.cnt = hb[b];
-    }
-    above += hb[b];
-  }
-  __syncthreads();
-}
-
-// Calls fn(i, offset) for every flagged element (bit i of f: element i),
-// where offset is its exclusive rank among the flagged elements of the
-// workgroup in index order; element i of a thread sits at chunk position
-// i * kThreads + threadIdx.x.  Wave-local ranks come from ballot + mbcnt and
-// are kept packed 4 per register; one wave scans the 256 (slot, wave) counts.
-template <typename F>
-__device__ inline void for_each_ordered(unsigned f, SelShared& sh, F&& fn) {
+__device__ inline Ordered ordered_plan(unsigned f, SelShared& sh) {
+  Ordered o;
   const unsigned lane = lane_id(), w = threadIdx.x >> 6;
-  unsigned pre[kNI / 4];
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
     const unsigned long long b = __ballot((f >> i) & 1u);
     const unsigned m = mbcnt(b);
-    pre[i / 4] = (i % 4 == 0) ? m : (pre[i / 4] | (m << (8 * (i % 4))));
+    o.pre[i / 4] = (i % 4 == 0) ? m : (o.pre[i / 4] | (m << (8 * (i % 4))));
     if (lane == 0) sh.tab[i * kWaves + w] = unsigned(__popcll(b));
   }
   __syncthreads();
   if (w == 0) {
     const uint4 v = reinterpret_cast<const uint4*>(sh.tab)[lane];
     const unsigned s = v.x + v.y + v.z + v.w;
-    unsigned inc = s;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const unsigned y = __shfl_up(inc, d);
-      if (lane >= unsigned(d)) inc += y;
-    }
+    const unsigned inc = wave_scan(s);
     const unsigned ex = inc - s;
     reinterpret_cast<uint4*>(sh.tab)[lane] =
         make_uint4(ex, ex + v.x, ex + v.x + v.y, ex + v.x + v.y + v.z);
+    if (lane == 63) sh.tab[kNI * kWaves] = inc;
   }
   __syncthreads();
+  o.total = sh.tab[kNI * kWaves];
+  return o;
+}
+
+template <typename F>
+__device__ inline void ordered_apply(unsigned f, const Ordered& o, SelShared& sh, F&& fn) {
+  const unsigned w = threadIdx.x >> 6;
 #pragma unroll
   for (int i = 0; i < kNI; ++i)
-    if ((f >> i) & 1u) fn(i, sh.tab[i * kWaves + w] + ((pre[i / 4] >> (8 * (i % 4))) & 0xffu));
+    if ((f >> i) & 1u) fn(i, sh.tab[i * kWaves + w] + ((o.pre[i / 4] >> (8 * (i % 4))) & 0xffu));
+}
+
+// ---- histograms ------------------------------------------------------------
+
+// hist[bin] += 1 for every lane with act.  The most frequent bin of the wave
+// instruction is aggregated with a ballot; the rest use LDS atomics.  Must be
+// reached by all lanes of the wave.
+__device__ inline void hist_add(unsigned* hist, unsigned bin, bool act) {
+  const unsigned long long pend = __ballot(act);
+  if (pend == 0) return;
+  const int leader = __builtin_ctzll(pend);
+  const unsigned b = unsigned(__builtin_amdgcn_readlane(int(bin), leader));
+  const unsigned long long same = __ballot(act && bin == b);
+  if (lane_id() == unsigned(leader)) atomicAdd(&hist[b], unsigned(__popcll(same)));
+  if (act && bin != b) atomicAdd(&hist[bin], 1u);
+}
+
+// Number of bits of x (0 for x = 0).
+__device__ inline int bit_width(unsigned x) { return x ? 32 - __clz(x) : 0; }
+
+// After a histogram pass: the bin where the running count from the top first
+// reaches `need`.  Publishes (digit, need - count above it, bin count).
+__device__ inline void find_bin(SelShared& sh, unsigned need) {
+  const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
+  // thread t holds bins 2047 - 4t .. 2044 - 4t: thread order is descending key
+  const uint4 h = reinterpret_cast<const uint4*>(sh.hist)[kThreads - 1 - t];
+  const unsigned hb[4] = {h.w, h.z, h.y, h.x};
+  const unsigned s = h.x + h.y + h.z + h.w;
+  const unsigned inc = wave_scan(s);
+  if (lane == 63) sh.red[0][w] = inc;
+  __syncthreads();
+  unsigned above = inc - s;
+  for (unsigned w2 = 0; w2 < w; ++w2) above += sh.red[0][w2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (above < need && need <= above + hb[j]) {
+      sh.digit = 2047u - 4u * t - unsigned(j);
+      sh.need = need - above;
+      sh.cnt = hb[j];
+    }
+    above += hb[j];
+  }
   __syncthreads();
 }
 
-// One radix pass over the keys whose bits above `shift + bits` equal the
-// prefix found so far.
-template <int SHIFT, int BITS, int PSHIFT>
-__device__ inline void radix_pass(SelShared& sh, const unsigned (&key)[kNI], int nv,
-                                  unsigned prefix, unsigned need) {
+// ---- bound ------------------------------------------------------------------
+
+// A key that at least `need` of the workgroup's valid keys reach, or 0 when
+// there are too few.  The histogram counts maxima of groups of G consecutive
+// slots of a lane (distinct candidates, so need maxima reaching a key means
+// need candidates do): G = 4 while the 4096 group maxima leave need well
+// inside, fewer otherwise; a group counts when its first slot is valid
+// (invalid slots hold key 0).  The 2048 bins split [lo, hi] linearly (key -
+// lo), so scores that straddle a power of two still spread out; the bound is
+// the floor of the bin where the count from the top reaches need.
+__device__ inline unsigned group_bound(SelShared& sh, const unsigned (&key)[kNI], unsigned vm,
+                                       unsigned need) {
+  const unsigned G = need <= 1024u ? 4u : (need <= 2048u ? 2u : 1u);
+  unsigned gvm = 0u, gm[kNI], lo = ~0u, hi = 0u;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) {
+    gm[i] = key[i];
+    if (G >= 2u && (i & 1) == 0) gm[i] = max(key[i], key[i + 1]);
+    if (G == 4u && (i & 3) == 0) gm[i] = max(max(key[i], key[i + 1]), max(key[i + 2], key[i + 3]));
+    if ((unsigned(i) & (G - 1u)) == 0u) gvm |= ((vm >> i) & 1u) << i;
+    if ((vm >> i) & 1u) {
+      lo = min(lo, key[i]);
+      hi = max(hi, key[i]);
+    }
+  }
+  const Red3 r = block_reduce(sh, unsigned(__popc(gvm)), lo, hi);
+  if (r.sum < need) return 0u;
+  if (r.lo == r.hi) return r.lo;
+  const int width = bit_width(r.hi - r.lo);
+  const int shift = width > 11 ? width - 11 : 0;  // bins (key - lo) >> shift, all < 2048
   reinterpret_cast<uint4*>(sh.hist)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kNI; ++i) {
-    bool act = i < nv;
-    if constexpr (PSHIFT < 32) act = act && (key[i] >> PSHIFT) == prefix;
-    hist_add(sh.hist, (key[i] >> SHIFT) & ((1u << BITS) - 1u), act);
-  }
+  for (int i = 0; i < kNI; ++i)  // groups start at slots i % G == 0 (G is uniform)
+    if ((unsigned(i) & (G - 1u)) == 0u) hist_add(sh.hist, (gm[i] - r.lo) >> shift, (gvm >> i) & 1u);
   __syncthreads();
   find_bin(sh, need);
+  return r.lo + (sh.digit << shift);
 }
 
-// Flags (bit i: element i) the top `need0` elements of the workgroup's chunk
-// (key order, ties by chunk position).
-__device__ inline unsigned select_top(SelShared& sh, const unsigned (&key)[kNI], int nv,
-                                      unsigned need0) {
-  radix_pass<21, 11, 32>(sh, key, nv, 0u, need0);
-  unsigned prefix = sh.digit, need = sh.need;
-  radix_pass<10, 11, 21>(sh, key, nv, prefix, need);
-  prefix = (prefix << 11) | sh.digit;
-  need = sh.need;
-  radix_pass<0, 10, 10>(sh, key, nv, prefix, need);
-  const unsigned tau = (prefix << 10) | sh.digit;
-  need = sh.need;
-  const unsigned ties = sh.cnt;
-  unsigned gt = 0u, eq = 0u;
+// ---- exact cut (fallback) --------------------------------------------------
+
+// Where the top `need` of a set of keys ends: every key > tau is in it, and
+// of the keys == tau the first `take` (position order).  take == 0: the cut
+// falls on a bin edge and exactly the keys >= tau are in it.
+struct Cut {
+  unsigned tau, take, ties;
+};
+
+// Exact cut for the top need (1 <= need <= valid count) of the workgroup's
+// keys.  Radix passes of up to 11 bits run over key - lo (lo: the smallest
+// valid key), from its top bit down, and stop early when the boundary bin is
+// taken whole.
+__device__ inline Cut find_cut(SelShared& sh, const unsigned (&key)[kNI], unsigned vm,
+                               unsigned need) {
+  unsigned lo = ~0u, hi = 0u;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i)
+    if ((vm >> i) & 1u) {
+      lo = min(lo, key[i]);
+      hi = max(hi, key[i]);
+    }
+  const Red3 r = block_reduce(sh, 0u, lo, hi);
+  if (r.lo == r.hi) return Cut{r.lo, need, ~0u};  // all equal: ties by position
+  int shift = bit_width(r.hi - r.lo);
+  unsigned prefix = 0u;  // of key - lo
+#pragma nounroll
+  for (;;) {
+    const int bits = shift < 11 ? shift : 11;
+    shift -= bits;
+    reinterpret_cast<uint4*>(sh.hist)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+    const unsigned mask = (1u << bits) - 1u;
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) {
+      const unsigned rel = key[i] - r.lo;
+      const bool act = ((vm >> i) & 1u) && shr(rel, shift + bits) == prefix;
+      hist_add(sh.hist, (rel >> shift) & mask, act);
+    }
+    __syncthreads();
+    find_bin(sh, need);
+    prefix = (prefix << bits) | sh.digit;
+    need = sh.need;
+    const unsigned cnt = sh.cnt;
+    if (cnt == need) return Cut{r.lo + (prefix << shift), 0u, 0u};
+    if (shift == 0) return Cut{r.lo + prefix, need, cnt};
+  }
+}
+
+// Selection mask of a cut (bit i: slot i); ties resolved in position order.
+__device__ inline unsigned cut_mask(SelShared& sh, const unsigned (&key)[kNI], unsigned vm,
+                                    const Cut& c) {
+  unsigned ge = 0u, eq = 0u;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
-    gt |= unsigned(i < nv && key[i] > tau) << i;
-    eq |= unsigned(i < nv && key[i] == tau) << i;
+    ge |= unsigned(c.take == 0u ? key[i] >= c.tau : key[i] > c.tau) << i;
+    eq |= unsigned(key[i] == c.tau) << i;
   }
-  if (ties > need) {  // keep the first `need` ties in index order
+  ge &= vm;
+  if (c.take == 0u) return ge;
+  eq &= vm;
+  if (c.ties > c.take) {
+    const Ordered o = ordered_plan(eq, sh);
     unsigned drop = 0u;
-    for_each_ordered(eq, sh, [&](int i, unsigned o) { drop |= unsigned(o >= need) << i; });
+    const unsigned take = c.take;
+    ordered_apply(eq, o, sh, [&](int i, unsigned rank) { drop |= unsigned(rank >= take) << i; });
+    __syncthreads();
     eq &= ~drop;
   }
-  return gt | eq;
+  return ge | eq;
 }
 
-// Keys of the candidates at chunk positions [base, base + n) of request r;
-// for pair input also their flat indices (raw input: index = position).
-template <bool RAW, bool BEAM>
-__device__ inline void load_chunk(const SelectParams& p, unsigned r, unsigned base, int nv,
-                                  unsigned (&key)[kNI], unsigned (&idx)[kNI]) {
+// ---- loads -----------------------------------------------------------------
+
+// Valid-slot mask of a lane for n elements at positions i * kThreads + tid.
+__device__ inline unsigned valid_mask(unsigned n) {
+  const unsigned t = threadIdx.x;
+  const unsigned nv = n > t ? (n - t + kThreads - 1) / kThreads : 0u;
+  return nv >= 32u ? ~0u : (1u << nv) - 1u;
+}
+
+// Raw scores at chunk positions [base, base + n) of request r.  Invalid slots
+// get key 0.  Every lane issues all of its loads before using any (invalid
+// slots read a clamped, in-bounds address), so the chunk streams in one
+// round trip.
+template <bool BEAM>
+__device__ inline unsigned load_raw(const SelectParams& p, unsigned r, unsigned base, unsigned n,
+                                    unsigned (&key)[kNI]) {
+  const unsigned vm = valid_mask(n);
   const float* logp_r = p.logp + size_t(r) * p.N;
   const float* beam_r = BEAM ? p.beam + size_t(r) * p.W_prev : nullptr;
-  const uint2* cand_r = RAW ? nullptr : p.cand_in + size_t(r) * p.n_in;
+  const unsigned pos0 = base + threadIdx.x;
+  float x[kNI], bs[kNI];
+  unsigned row = 0u, rem = 0u;  // row of the current position and its offset in the row
+  if constexpr (BEAM) {
+    const unsigned first = min(pos0, p.N - 1u);
+    row = row_of(first, p.V, p.inv_v);
+    rem = first - row * p.V;
+  }
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
-    const unsigned pos = base + unsigned(i) * kThreads + threadIdx.x;
-    key[i] = 0u;
-    if constexpr (!RAW) idx[i] = 0u;
-    if (i < nv) {
-      if constexpr (RAW) {
-        key[i] = order_key(candidate_score<BEAM>(logp_r, beam_r, pos, p.V, p.inv_v));
-      } else {
-        const uint2 c = cand_r[pos];
-        key[i] = c.x;
-        idx[i] = c.y;
+    const bool valid = (vm >> i) & 1u;
+    const unsigned pos = pos0 + unsigned(i) * kThreads;
+    if constexpr (BEAM) {
+      if (i > 0) {
+        rem += kThreads;
+        if (rem >= p.V) {
+          if (p.V >= unsigned(kThreads)) {  // at most one row boundary per step
+            rem -= p.V;
+            ++row;
+          } else {
+            row = row_of(valid ? pos : base, p.V, p.inv_v);
+            rem = (valid ? pos : base) - row * p.V;
+          }
+        }
       }
+      bs[i] = beam_r[valid ? row : 0u];
+    }
+    x[i] = logp_r[valid ? pos : base];
+  }
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) {
+    float v = x[i];
+    if constexpr (BEAM) v = bs[i] + v;
+    key[i] = ((vm >> i) & 1u) ? order_key(v) : 0u;
+  }
+  return vm;
+}
+
+// Candidates of the input slots [s0, s0 + group) of request r.  Invalid
+// slots get key 0.  Returns the validity mask; sh.scnt holds the counts.
+// Loads are unconditional (invalid slots re-read the region's first pair).
+__device__ inline unsigned load_slots(const SelectParams& p, SelShared& sh, unsigned r,
+                                      unsigned s0, unsigned (&key)[kNI], unsigned (&idx)[kNI]) {
+  if (threadIdx.x < p.group) {
+    const unsigned s = s0 + threadIdx.x;
+    sh.scnt[threadIdx.x] = s < p.nslots_in ? p.cnt_in[size_t(r) * p.nslots_in + s] : 0u;
+  }
+  __syncthreads();
+  const uint2* in = p.cand_in + (size_t(r) * p.nslots_in + s0) * p.cap;
+  unsigned vm = 0u;
+  uint2 c[kNI];
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) {
+    const unsigned pos = unsigned(i) * kThreads + threadIdx.x;
+    const unsigned s = pos >> p.lcap, j = pos & (p.cap - 1u);
+    const bool valid = s < p.group && j < sh.scnt[s];
+    vm |= unsigned(valid) << i;
+    c[i] = in[valid ? pos : 0u];
+  }
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) {
+    const bool valid = (vm >> i) & 1u;
+    key[i] = valid ? c[i].x : 0u;
+    idx[i] = valid ? c[i].y : 0u;
+  }
+  return vm;
+}
+
+// ---- sort ------------------------------------------------------------------
+
+// x of lane (lane ^ M) without LDS: DPP quad permutes for 1 and 2, row
+// shifts for 4, a row rotate for 8 and the gfx950 permlane swaps for 16 and
+// 32 (lane layouts checked on the device).
+template <int M>
+__device__ inline unsigned xor_lane(unsigned x) {
+  const unsigned lane = lane_id();
+  if constexpr (M == 1) return dppu<0xB1>(x);  // quad_perm [1,0,3,2]
+  if constexpr (M == 2) return dppu<0x4E>(x);  // quad_perm [2,3,0,1]
+  if constexpr (M == 4) {
+    const unsigned up = dppu<0x104>(x), down = dppu<0x114>(x);  // row_shl:4, row_shr:4
+    return (lane & 4u) ? down : up;
+  }
+  if constexpr (M == 8) return dppu<0x128>(x);  // row_ror:8
+  if constexpr (M == 16) {
+    const auto s = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return (lane & 16u) ? s[0] : s[1];
+  }
+  if constexpr (M == 32) {
+    const auto s = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return (lane & 32u) ? s[0] : s[1];
+  }
+}
+
+template <int M>
+__device__ inline unsigned long long xor_lane64(unsigned long long x) {
+  const unsigned lo = xor_lane<M>(unsigned(x)), hi = xor_lane<M>(unsigned(x >> 32));
+  return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
+// One compare-exchange stage (block size K, stride J) of a descending bitonic
+// sort of 64 E values held by one wave, lane l holding positions l E .. l E +
+// E - 1.
+template <int E, int K, int J>
+__device__ inline void bitonic_stage(unsigned long long (&v)[E]) {
+  const unsigned lane = lane_id();
+  if constexpr (J < E) {
+#pragma unroll
+    for (int q = 0; q < E; ++q) {
+      if ((q & J) == 0) {
+        const unsigned g = lane * E + unsigned(q);
+        const bool desc = (g & unsigned(K)) == 0;
+        const unsigned long long a = v[q], b = v[q + J];
+        const bool swap = desc ? a < b : a > b;
+        v[q] = swap ? b : a;
+        v[q + J] = swap ? a : b;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < E; ++q) {
+      const unsigned long long pv = xor_lane64<J / E>(v[q]);
+      const unsigned g = lane * E + unsigned(q);
+      const bool keep_max = ((g & unsigned(J)) == 0) == ((g & unsigned(K)) == 0);
+      v[q] = keep_max ? (v[q] > pv ? v[q] : pv) : (v[q] < pv ? v[q] : pv);
     }
   }
 }
 
-__device__ inline int valid_per_thread(unsigned n) {
-  const unsigned t = threadIdx.x;
-  return n > t ? int((n - t + kThreads - 1) / kThreads) : 0;
+template <int E, int K, int J>
+__device__ inline void bitonic_merge(unsigned long long (&v)[E]) {
+  if constexpr (J >= 1) {
+    bitonic_stage<E, K, J>(v);
+    bitonic_merge<E, K, J / 2>(v);
+  }
 }
 
-template <bool RAW, bool BEAM>
-__global__ __launch_bounds__(kThreads) void select_stage_kernel(SelectParams p) {
+template <int E, int K>
+__device__ inline void bitonic_levels(unsigned long long (&v)[E]) {
+  if constexpr (K <= 64 * E) {
+    bitonic_merge<E, K, K / 2>(v);
+    bitonic_levels<E, K * 2>(v);
+  }
+}
+
+// Number of values of a descending run that exceed x.
+template <int N>
+__device__ inline unsigned count_above(const unsigned long long* run, unsigned long long x) {
+  unsigned lo = 0, hi = N;
+#pragma unroll
+  for (int it = 0; (1 << it) <= N; ++it) {
+    if (lo < hi) {
+      const unsigned mid = (lo + hi) >> 1;
+      if (run[mid] > x) lo = mid + 1;
+      else hi = mid;
+    }
+  }
+  return lo;
+}
+
+// Sorted top W of the m (<= kSortCap) composites in buf, handed out as
+// fn(rank, value) for rank < W.  The m values are cut into 8 runs of ceil(m
+// / 8), one per wave; each wave sorts its run in registers (padding 0 sorts
+// last), the runs go back to buf, and every value's rank is its place in its
+// own run plus the number of values above it in each other run (binary
+// searches).  Values are distinct, so ranks are exact.
+template <int E, typename F>
+__device__ inline void rank_sorted_runs(unsigned long long* buf, unsigned m, unsigned W, F&& fn) {
+  const unsigned lane = lane_id(), w = threadIdx.x >> 6;
+  const unsigned len = (m + kWaves - 1) / kWaves;
+  unsigned long long v[E];
+#pragma unroll
+  for (int q = 0; q < E; ++q) {
+    const unsigned i = lane * E + unsigned(q);
+    const unsigned g = w * len + i;
+    v[q] = (i < len && g < m) ? buf[g] : 0ull;
+  }
+  bitonic_levels<E, 2>(v);
+  __syncthreads();
+  constexpr unsigned N = 64u * E;
+#pragma unroll
+  for (int q = 0; q < E; ++q) buf[w * N + lane * E + unsigned(q)] = v[q];
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < E; ++q) {
+    if (v[q] == 0ull) continue;  // padding
+    unsigned rank = lane * E + unsigned(q);
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2)
+      if (unsigned(w2) != w) rank += count_above<N>(buf + w2 * N, v[q]);
+    if (rank < W) fn(rank, v[q]);
+  }
+}
+
+// ---- kernels ---------------------------------------------------------------
+
+// Superset (or exact set) of the top min(W, n) of one workgroup's candidates
+// into slot (r, g): survivors of the bound when they fit, else the exact cut.
+template <typename IdxFn>
+__device__ inline void reduce_group(const SelectParams& p, SelShared& sh, unsigned r, unsigned g,
+                                    const unsigned (&key)[kNI], unsigned vm, unsigned n,
+                                    IdxFn&& idx_of) {
+  uint2* out = p.cand_out + (size_t(r) * p.nwg + g) * p.cap;
+  const unsigned need = min(p.W, n);
+  unsigned keep = vm;
+  if (n > p.cap) {
+    const unsigned b = group_bound(sh, key, vm, need);
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < b) << i);
+  }
+  Ordered o = ordered_plan(keep, sh);
+  if (o.total > p.cap) {
+    __syncthreads();
+    const Cut c = find_cut(sh, key, vm, need);
+    keep = cut_mask(sh, key, vm, c);
+    o = ordered_plan(keep, sh);
+  }
+  ordered_apply(keep, o, sh,
+                [&](int i, unsigned rank) { out[rank] = make_uint2(key[i], idx_of(i)); });
+  if (threadIdx.x == 0) p.cnt_out[size_t(r) * p.nwg + g] = o.total;
+}
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_raw_stage_kernel(SelectParams p) {
   __shared__ SelShared sh;
-  const unsigned r = blockIdx.x / p.nchunks, c = blockIdx.x - r * p.nchunks;
-  const unsigned base = c * unsigned(kSelectChunk);
-  const unsigned n = min(p.n_in - base, unsigned(kSelectChunk));
-  const int nv = valid_per_thread(n);
-  unsigned key[kNI], idx[kNI];
-  load_chunk<RAW, BEAM>(p, r, base, nv, key, idx);
-  const unsigned sel = select_top(sh, key, nv, min(p.W, n));
-  uint2* out = p.cand_out + size_t(r) * p.out_stride + size_t(c) * p.W;
-  for_each_ordered(sel, sh, [&](int i, unsigned o) {
-    const unsigned fi = RAW ? base + unsigned(i) * kThreads + threadIdx.x : idx[i];
-    out[o] = make_uint2(key[i], fi);
-  });
+  const unsigned r = blockIdx.x / p.nwg, g = blockIdx.x - r * p.nwg;
+  const unsigned base = g * unsigned(kSelectChunk);
+  const unsigned n = min(p.N - base, unsigned(kSelectChunk));
+  unsigned key[kNI];
+  const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
+  reduce_group(p, sh, r, g, key, vm, n,
+               [&](int i) { return base + unsigned(i) * kThreads + threadIdx.x; });
 }
 
+__global__ __launch_bounds__(kThreads) void select_slot_stage_kernel(SelectParams p) {
+  __shared__ SelShared sh;
+  const unsigned r = blockIdx.x / p.nwg, g = blockIdx.x - r * p.nwg;
+  unsigned key[kNI], idx[kNI];
+  const unsigned vm = load_slots(p, sh, r, g * p.group, key, idx);
+  const Red3 t = block_reduce(sh, unsigned(__popc(vm)), 0u, 0u);
+  reduce_group(p, sh, r, g, key, vm, t.sum, [&](int i) { return idx[i]; });
+}
+
+// Top W of request r's last candidates, sorted, into parents/tokens/scores.
 template <bool RAW, bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) {
   __shared__ SelShared sh;
-  __shared__ unsigned long long srt[kSelectMaxWidth];
+  __shared__ unsigned long long srt[kSortCap];
   const unsigned r = blockIdx.x;
-  const int nv = valid_per_thread(p.n_in);
-  unsigned key[kNI], idx[kNI];
-  load_chunk<RAW, BEAM>(p, r, 0u, nv, key, idx);
-  const unsigned sel = select_top(sh, key, nv, p.W);
+  unsigned key[kNI], idx[kNI], vm, n;
+  if constexpr (RAW) {
+    n = p.N;
+    vm = load_raw<BEAM>(p, r, 0u, n, key);
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) idx[i] = unsigned(i) * kThreads + threadIdx.x;
+  } else {
+    vm = load_slots(p, sh, r, 0u, key, idx);
+    n = block_reduce(sh, unsigned(__popc(vm)), 0u, 0u).sum;
+  }
+  unsigned keep = vm;
+  if (n > unsigned(kSortCap)) {
+    const unsigned b = group_bound(sh, key, vm, p.W);
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < b) << i);
+  }
+  Ordered o = ordered_plan(keep, sh);
+  if (o.total > unsigned(kSortCap)) {
+    __syncthreads();
+    const Cut c = find_cut(sh, key, vm, p.W);
+    keep = cut_mask(sh, key, vm, c);
+    o = ordered_plan(keep, sh);
+  }
   // Composite sort key: score key high, complemented index low, so that the
   // descending order is (score desc, index asc).  Padding (0) sorts last.
-  for_each_ordered(sel, sh, [&](int i, unsigned o) {
-    const unsigned fi = RAW ? unsigned(i) * kThreads + threadIdx.x : idx[i];
-    srt[o] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~fi);
+  ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
+    srt[rank] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~idx[i]);
   });
-  unsigned n2 = 1;
-  while (n2 < p.W) n2 <<= 1;
-  for (unsigned j = p.W + threadIdx.x; j < n2; j += kThreads) srt[j] = 0ull;
   __syncthreads();
-  for (unsigned k = 2; k <= n2; k <<= 1) {
-    for (unsigned j = k >> 1; j > 0; j >>= 1) {
-      for (unsigned x = threadIdx.x; x < n2 / 2; x += kThreads) {
-        const unsigned a = 2 * x - (x & (j - 1)), b = a + j;
-        const unsigned long long va = srt[a], vb = srt[b];
-        const bool desc = (a & k) == 0;
-        if (desc ? va < vb : va > vb) {
-          srt[a] = vb;
-          srt[b] = va;
-        }
-      }
-      __syncthreads();
-    }
-  }
+  const unsigned m = o.total;
   const float* logp_r = p.logp + size_t(r) * p.N;
-  for (unsigned j = threadIdx.x; j < p.W; j += kThreads) {
-    const unsigned fi = ~unsigned(srt[j]);
-    const unsigned row = row_of(fi, p.V, p.inv_v);
-    const size_t o = size_t(r) * p.W + j;
-    p.parents[o] = int(row);
-    p.tokens[o] = int(fi - row * p.V);
-    if constexpr (BEAM) p.scores[o] = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
-    else p.scores[o] = logp_r[fi];
-  }
+  auto emit = [&](unsigned j, unsigned long long c) {
+    if (j < p.W) {
+      const unsigned fi = ~unsigned(c);
+      const unsigned row = row_of(fi, p.V, p.inv_v);
+      const size_t o2 = size_t(r) * p.W + j;
+      p.parents[o2] = int(row);
+      p.tokens[o2] = int(fi - row * p.V);
+      if constexpr (BEAM) p.scores[o2] = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
+      else p.scores[o2] = logp_r[fi];
+    }
+  };
+  const unsigned len = (m + kWaves - 1) / kWaves;  // run length per wave
+  if (len <= 64u) rank_sorted_runs<1>(srt, m, p.W, emit);
+  else if (len <= 128u) rank_sorted_runs<2>(srt, m, p.W, emit);
+  else if (len <= 256u) rank_sorted_runs<4>(srt, m, p.W, emit);
+  else rank_sorted_runs<8>(srt, m, p.W, emit);
 }
 
-template <bool RAW>
-void launch_stage(const SelectParams& p, unsigned blocks, bool beam, hipStream_t st) {
-  if (beam) select_stage_kernel<RAW, true><<<blocks, kThreads, 0, st>>>(p);
-  else select_stage_kernel<RAW, false><<<blocks, kThreads, 0, st>>>(p);
-}
-
-template <bool RAW>
-void launch_final(const SelectParams& p, unsigned blocks, bool beam, hipStream_t st) {
-  if (beam) select_final_kernel<RAW, true><<<blocks, kThreads, 0, st>>>(p);
-  else select_final_kernel<RAW, false><<<blocks, kThreads, 0, st>>>(p);
+unsigned pow2_ceil(unsigned x) {
+  unsigned y = 1;
+  while (y < x) y <<= 1;
+  return y;
 }
 
 }  // namespace
@@ -328,28 +691,46 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
   if (R < 1 || N < 1 || W < 1 || W > N || W > unsigned(kSelectMaxWidth) ||
       N > kSelectMaxCandidates)
     return false;
-  size_t buf[2] = {0, 0};
-  unsigned n = N;
+  // Slot capacity: room for about twice the kept count, at least 64, at most
+  // a quarter of a workgroup's candidates (never below W).
+  unsigned cap = pow2_ceil(2 * W);
+  if (cap < 64) cap = 64;
+  if (cap > unsigned(kSelectChunk) / 4) cap = std::max(unsigned(kSelectChunk) / 4, pow2_ceil(W));
+  plan->cap = cap;
+  plan->group = unsigned(kSelectChunk) / cap;
+  size_t pairs[2] = {0, 0}, counts[2] = {0, 0};
   int s = 0;
-  while (n > unsigned(kSelectChunk)) {
-    if (s == kSelectMaxStages) return false;
-    const unsigned chunks = (n + kSelectChunk - 1) / kSelectChunk;
-    const unsigned last = n - (chunks - 1) * unsigned(kSelectChunk);
-    const unsigned out = (chunks - 1) * W + (last < W ? last : W);
-    plan->n[s] = n;
-    plan->chunks[s] = chunks;
-    plan->out[s] = out;
-    const size_t bytes = size_t(R) * out * sizeof(uint2);
-    if (bytes > buf[s & 1]) buf[s & 1] = bytes;
-    n = out;
-    ++s;
+  if (N > unsigned(kSelectChunk)) {
+    unsigned slots = (N + kSelectChunk - 1) / kSelectChunk;  // stage 0: raw chunks
+    plan->nwg[0] = slots;
+    plan->nin[0] = N;
+    pairs[0] = size_t(R) * slots * cap * sizeof(uint2);
+    counts[0] = size_t(R) * slots * sizeof(unsigned);
+    s = 1;
+    while (slots > plan->group) {
+      if (s == kSelectMaxStages) return false;
+      const unsigned nwg = (slots + plan->group - 1) / plan->group;
+      plan->nin[s] = slots;
+      plan->nwg[s] = nwg;
+      pairs[s & 1] = std::max(pairs[s & 1], size_t(R) * nwg * cap * sizeof(uint2));
+      counts[s & 1] = std::max(counts[s & 1], size_t(R) * nwg * sizeof(unsigned));
+      slots = nwg;
+      ++s;
+    }
+    plan->final_in = slots;
+  } else {
+    plan->final_in = N;
   }
   plan->stages = s;
-  plan->n_final = n;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-  plan->buf_bytes[0] = up(buf[0]);
-  plan->buf_bytes[1] = up(buf[1]);
-  plan->total = plan->buf_bytes[0] + plan->buf_bytes[1];
+  size_t off = 0;
+  for (int b = 0; b < 2; ++b) {
+    plan->pair_off[b] = off;
+    off += up(pairs[b]);
+    plan->count_off[b] = off;
+    off += up(counts[b]);
+  }
+  plan->total = off;
   return true;
 }
 
@@ -366,29 +747,46 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
   p.W_prev = unsigned(prev_width);
   p.N = p.V * p.W_prev;
   p.W = unsigned(width);
+  p.cap = plan.cap;
+  p.lcap = unsigned(__builtin_ctz(plan.cap));
+  p.group = plan.group;
   p.inv_v = 1.0 / double(vocab);
-  uint2* bufs[2] = {static_cast<uint2*>(workspace),
-                    reinterpret_cast<uint2*>(static_cast<char*>(workspace) + plan.buf_bytes[0])};
+  char* ws = static_cast<char*>(workspace);
   const bool has_beam = beam != nullptr;
   for (int s = 0; s < plan.stages; ++s) {
-    p.cand_in = s == 0 ? nullptr : bufs[(s - 1) & 1];
-    p.cand_out = bufs[s & 1];
-    p.n_in = plan.n[s];
-    p.nchunks = plan.chunks[s];
-    p.out_stride = plan.out[s];
-    const unsigned blocks = unsigned(R) * plan.chunks[s];
-    if (s == 0) launch_stage<true>(p, blocks, has_beam, st);
-    else launch_stage<false>(p, blocks, false, st);
+    const int in = (s - 1) & 1, out = s & 1;
+    p.cand_in = s == 0 ? nullptr : reinterpret_cast<const uint2*>(ws + plan.pair_off[in]);
+    p.cnt_in = s == 0 ? nullptr : reinterpret_cast<const unsigned*>(ws + plan.count_off[in]);
+    p.cand_out = reinterpret_cast<uint2*>(ws + plan.pair_off[out]);
+    p.cnt_out = reinterpret_cast<unsigned*>(ws + plan.count_off[out]);
+    p.nslots_in = s == 0 ? 0u : plan.nin[s];
+    p.nwg = plan.nwg[s];
+    const unsigned blocks = unsigned(R) * plan.nwg[s];
+    if (s == 0) {
+      if (has_beam) select_raw_stage_kernel<true><<<blocks, kThreads, 0, st>>>(p);
+      else select_raw_stage_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    } else {
+      select_slot_stage_kernel<<<blocks, kThreads, 0, st>>>(p);
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  p.cand_in = plan.stages == 0 ? nullptr : bufs[(plan.stages - 1) & 1];
+  const int last = (plan.stages - 1) & 1;
+  p.cand_in =
+      plan.stages == 0 ? nullptr : reinterpret_cast<const uint2*>(ws + plan.pair_off[last]);
+  p.cnt_in =
+      plan.stages == 0 ? nullptr : reinterpret_cast<const unsigned*>(ws + plan.count_off[last]);
   p.cand_out = nullptr;
-  p.n_in = plan.n_final;
-  p.nchunks = 1;
-  p.out_stride = 0;
-  if (plan.stages == 0) launch_final<true>(p, unsigned(R), has_beam, st);
-  else launch_final<false>(p, unsigned(R), has_beam, st);
+  p.cnt_out = nullptr;
+  p.nslots_in = plan.stages == 0 ? 0u : plan.final_in;
+  p.nwg = 1;
+  if (plan.stages == 0) {
+    if (has_beam) select_final_kernel<true, true><<<R, kThreads, 0, st>>>(p);
+    else select_final_kernel<true, false><<<R, kThreads, 0, st>>>(p);
+  } else {
+    if (has_beam) select_final_kernel<false, true><<<R, kThreads, 0, st>>>(p);
+    else select_final_kernel<false, false><<<R, kThreads, 0, st>>>(p);
+  }
   return hipGetLastError();
 }
 

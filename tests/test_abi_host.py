@@ -144,16 +144,28 @@ def test_binding_rejects_host_tensors():
 
 
 def _select_plan_bytes(R, P, V, W, chunk=16384):
-    """Workspace model of the beam selection: a reduction tree of per-chunk
-    top-W stages, (key, index) pairs of 8 bytes ping-ponged between two
-    256-byte-aligned buffers, until at most one chunk is left."""
-    n, s, buf = P * V, 0, [0, 0]
-    while n > chunk:
-        chunks = -(-n // chunk)
-        out = (chunks - 1) * W + min(W, n - (chunks - 1) * chunk)
-        buf[s % 2] = max(buf[s % 2], R * out * 8)
-        n, s = out, s + 1
-    return sum(-(-b // 256) * 256 for b in buf)
+    """Workspace model of the beam selection: a reduction tree whose
+    workgroups each take `chunk` candidates and write one slot of `cap`
+    (key, index) pairs (8 bytes each) plus a 4-byte count; stage outputs
+    alternate between two buffers, every region 256-byte aligned."""
+    p2 = lambda x: 1 << (x - 1).bit_length()
+    cap = max(64, p2(2 * W))
+    if cap > chunk // 4:
+        cap = max(chunk // 4, p2(W))
+    group = chunk // cap
+    pairs, counts = [0, 0], [0, 0]
+    n = P * V
+    if n > chunk:
+        slots = -(-n // chunk)
+        pairs[0], counts[0] = R * slots * cap * 8, R * slots * 4
+        s = 1
+        while slots > group:
+            slots = -(-slots // group)
+            pairs[s % 2] = max(pairs[s % 2], R * slots * cap * 8)
+            counts[s % 2] = max(counts[s % 2], R * slots * 4)
+            s += 1
+    up = lambda x: -(-x // 256) * 256
+    return sum(up(x) for x in pairs + counts)
 
 
 @pytest.mark.parametrize("R,P,V,W", [(1, 3, 5, 7), (2, 8, 2048, 4096), (1, 512, 8192, 512),
