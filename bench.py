@@ -216,6 +216,9 @@ def main():
     ap.add_argument("--records", choices=("inputs", "delta"), default="inputs",
                     help="record kind of the headline path (the other is timed as an A/B)")
     ap.add_argument("--skip-ab", action="store_true")
+    ap.add_argument("--skip-select", action="store_true")
+    ap.add_argument("--select-vocab", type=int, default=None,
+                    help="codebook size of the beam-selection measurement")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -313,6 +316,8 @@ def main():
     kind = args.records
     log(f"[bench] fused path ({kind} records): warmup {args.warmup}, {K} timed steps")
     ms_per_step = timed_steps(True, K, args.warmup, kind)
+    # outputs of the headline path, before any other leg reuses the buffers
+    head_outs = [o[0].cpu().numpy() for o in batches[0]["outs"]]
     beam_tokens_per_step = spec.R * sum(spec.widths)
     value = beam_tokens_per_step / (ms_per_step / 1e3)
     log(f"[bench] fused: {ms_per_step * 1e3:.1f} us/step")
@@ -460,6 +465,59 @@ def main():
         log(f"[bench] fullstate baseline {fs_ms:.3f} ms/step")
         del base
 
+    # ---- global top-W beam selection (supplementary: not part of `value`):
+    # the next step's parents from W_prev x V candidate scores per request
+    if not args.skip_select:
+        wp = spec.widths[-1]
+        vocab = args.select_vocab or Wm.SELECT_CODEBOOK
+        logp_np, beam_np = Wm.make_select_inputs(spec.R, wp, vocab, seed=spec.seed + 1)
+        logp_d = torch.from_numpy(logp_np).to(dev)
+        beam_d = torch.from_numpy(beam_np).to(dev)
+        ss = torch.cuda.Stream()
+        sel = runner.BeamSelector(spec.R, wp, vocab, wp, dev, stream=ss)
+        sel(logp_d, beam_d)
+        torch.cuda.synchronize()
+        reps_g = 20
+        gsel = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gsel, stream=ss):
+            for _ in range(reps_g):
+                sel(logp_d, beam_d)
+        torch.cuda.synchronize()
+        gsel.replay()
+        torch.cuda.synchronize()
+        se0, se1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(ss):
+            se0.record()
+            for _ in range(5):
+                gsel.replay()
+            se1.record()
+        torch.cuda.synchronize()
+        sel_us = se0.elapsed_time(se1) * 1e3 / (5 * reps_g)
+        sel_bytes = spec.R * wp * (vocab + 1) * 4 + spec.R * wp * 12
+        # reference: torch.topk over precomputed candidate scores (no fused
+        # beam-score add, no defined order among ties)
+        flat = (beam_d[:, :, None] + logp_d).reshape(spec.R, -1)
+        torch.topk(flat, wp, dim=1)
+        torch.cuda.synchronize()
+        te0, te1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        te0.record()
+        for _ in range(20):
+            torch.topk(flat, wp, dim=1)
+        te1.record()
+        torch.cuda.synchronize()
+        topk_us = te0.elapsed_time(te1) * 1e3 / 20
+        result["beam_selection"] = {
+            "workload": f"R{spec.R}_wprev{wp}_v{vocab}_w{wp}",
+            "us_per_call": sel_us, "alg_bytes": sel_bytes,
+            "achieved_GBs": sel_bytes / (sel_us * 1e-6) / 1e9,
+            "frac_of_hbm_peak": sel_bytes / (sel_us * 1e-6) / 8.0e12,
+            "torch_topk_us": topk_us,
+            "note": "onela_select_beams (fused beam-score add, total order); torch.topk is "
+                    "timed on precomputed scores as a reference only"}
+        log(f"[bench] beam selection {sel_us:.1f} us/call ({wp}x{vocab} -> {wp}), "
+            f"torch.topk {topk_us:.1f} us")
+        del sel, gsel, logp_d, beam_d, flat
+
     # ---- practical HBM ceiling: a plain device copy (torch copy_, 16-byte
     # vector blit) of the same size as the dominant kernel's traffic, and of
     # a size far beyond the caches, buffers rotated so data comes from HBM
@@ -494,8 +552,7 @@ def main():
 
     if not args.skip_cpu:
         log("[bench] cpu baseline (oracle)")
-        gpu_outs = [o[0].cpu().numpy() for o in batches[0]["outs"]]
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu_outs)
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, head_outs)
 
     print(json.dumps(result), flush=True)
 

@@ -37,6 +37,9 @@ def short_name(name: str) -> str:
               "clear_status_kernel"):
         if k in name:
             return k
+    m = re.search(r"(select_\w+_kernel)(<[^>]*>)?", name)
+    if m:
+        return m.group(1) + (m.group(2) or "")
     name = re.sub(r"\(.*", "", name).replace("void ", "")
     return name[:60]
 
