@@ -40,11 +40,11 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_12399_amd", "csrc", "kernel_decode.h
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_fused_h16_d128_w512_traffic.md")
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, variant: str):
     """HBM bytes per fused launch per step t from the committed PMC summary
     (FETCH_SIZE and WRITE_SIZE runs, copy-calibrated), or None when the
-    summary is missing, is for another workload, or was taken on a different
-    kernel source than the one built now."""
+    summary is missing, is for another workload or record variant, or was
+    taken on a different kernel source than the one built now."""
     import hashlib
     if not os.path.exists(TRAFFIC_PROFILE):
         return None
@@ -52,7 +52,8 @@ def measured_traffic(workload: str):
     for line in open(TRAFFIC_PROFILE):
         if line.startswith("bench-traffic: "):
             rec = json.loads(line[len("bench-traffic: "):])
-            if rec.get("kernel_source_sha256") == want and rec.get("workload") == workload:
+            if (rec.get("kernel_source_sha256") == want and rec.get("workload") == workload
+                    and rec.get("variant", "inputs") == variant):
                 return rec["bytes_per_t"]
     return None
 
@@ -103,15 +104,17 @@ def unique_parents(wl, t):
     return sum(len(np.unique(wl.steps[t].parents[r])) for r in range(wl.spec.R)) if t else 0
 
 
-def fused_alg_bytes(wl, t):
+def fused_alg_bytes(wl, t, borrow=False):
     """Algorithmic HBM bytes of one fused step launch at step t: the decode's
     bytes with the step-t records read from the caller instead of the arena,
-    plus writing them into the arena, the parents, the parents' rows of
-    h_{t-1} and the new h_t."""
+    plus writing them into the arena (not with borrowed record slabs, which
+    the later steps read in place), the parents, the parents' rows of h_{t-1}
+    and the new h_t."""
     s = wl.spec
     W = s.widths[t]
     b = decode_alg_bytes(wl, t) - s.R * W * t * 4   # h_t is written, not read
-    b += slab_bytes(wl, t)                          # arena write of the step-t records
+    if not borrow:
+        b += slab_bytes(wl, t)                      # arena write of the step-t records
     if t == 0:
         b += s.R * s.HV * s.dv * s.dk * 4           # S_ctx split (bf16 hi + lo) write
     if t > 0:
@@ -143,19 +146,27 @@ def fused_alg_bytes_delta(wl, t):
     return b
 
 
-def kernel_alg_bytes(wl, t, records):
-    return fused_alg_bytes(wl, t) if records == "inputs" else fused_alg_bytes_delta(wl, t)
+# Record variants: (record kind, record storage) of the library's config.
+VARIANTS = {"borrow": ("inputs", "borrow"), "inputs": ("inputs", "copy"),
+            "delta": ("delta", "copy")}
 
 
-def step_alg_bytes(wl, fused=True):
+def kernel_alg_bytes(wl, t, variant):
+    if variant == "delta":
+        return fused_alg_bytes_delta(wl, t)
+    return fused_alg_bytes(wl, t, borrow=variant == "borrow")
+
+
+def step_alg_bytes(wl, fused=True, variant="borrow"):
     """Algorithmic bytes of one whole step (T decode steps; init moves none)."""
     s = wl.spec
     total = 0
     for t, W in enumerate(s.widths):
         if fused:
-            total += fused_alg_bytes(wl, t)
+            total += kernel_alg_bytes(wl, t, variant)
         else:
-            total += 2 * slab_bytes(wl, t) + decode_alg_bytes(wl, t)
+            append = 0 if variant == "borrow" else 2 * slab_bytes(wl, t)
+            total += append + decode_alg_bytes(wl, t)
             if t > 0:
                 total += s.R * W * 4 + unique_parents(wl, t) * (t - 1) * 4 + s.R * W * t * 4
     return total
@@ -213,8 +224,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--skip-fullstate", action="store_true")
-    ap.add_argument("--records", choices=("inputs", "delta"), default="inputs",
-                    help="record kind of the headline path (the other is timed as an A/B)")
+    ap.add_argument("--variant", choices=tuple(VARIANTS), default="borrow",
+                    help="record variant of the headline path: borrowed zero-copy input "
+                         "records, input records copied into the arena, or the paper's "
+                         "delta records (the others are timed as an A/B)")
     ap.add_argument("--skip-ab", action="store_true")
     ap.add_argument("--skip-select", action="store_true")
     ap.add_argument("--select-vocab", type=int, default=None,
@@ -249,7 +262,7 @@ def main():
     s0 = runner.prefill_state(spec, dw0.prompt, dev, stream)
     torch.cuda.synchronize()
     NB = args.batches
-    cfgs = {kind: runner.config_for(spec, records=kind) for kind in ("inputs", "delta")}
+    cfgs = {v: runner.config_for(spec, records=rk, storage=st) for v, (rk, st) in VARIANTS.items()}
     ws_bytes = max(ab.onela_workspace_bytes(c) for c in cfgs.values())
     batches = []
     for i in range(NB):
@@ -313,8 +326,8 @@ def main():
         return e0.elapsed_time(e1) / K
 
     K = args.steps
-    kind = args.records
-    log(f"[bench] fused path ({kind} records): warmup {args.warmup}, {K} timed steps")
+    kind = args.variant
+    log(f"[bench] fused path ({kind}): warmup {args.warmup}, {K} timed steps")
     ms_per_step = timed_steps(True, K, args.warmup, kind)
     # outputs of the headline path, before any other leg reuses the buffers
     head_outs = [o[0].cpu().numpy() for o in batches[0]["outs"]]
@@ -403,44 +416,51 @@ def main():
                    "parents": f"{spec.parents}{spec.zipf_s if spec.parents == 'zipf' else ''}",
                    "step": "onela_init + per t onela_decode_step_fused (resolve + append "
                            "+ decode in one launch)",
-                   "records": kind,
+                   "records": {"borrow": "step inputs (k, v, alpha, beta), borrowed "
+                                         "in place (zero-copy slabs)",
+                               "inputs": "step inputs (k, v, alpha, beta) copied into the "
+                                         "workspace arena",
+                               "delta": "(alpha, delta fp16, k) transition records"}[kind],
                    "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
                                   "fp32 accum",
                    "graph": not args.no_graph, "batches": NB},
         "decode_step_us": {"per_t": [round(float(x), 3) for x in dec_us],
                            "mean": round(float(dec_us.mean()), 3)},
         "beam_tokens_per_step": beam_tokens_per_step,
-        "step_alg_bytes": step_alg_bytes(wl, fused=True),
+        "step_alg_bytes": step_alg_bytes(wl, fused=True, variant=kind),
         "separate_calls": {"ms_per_step": ms_sep,
                            "beam_tokens_per_s": beam_tokens_per_step / (ms_sep / 1e3),
                            "step": "onela_init + per t (resolve_ancestry, append_records, "
                                    "decode_step)",
-                           "step_alg_bytes": step_alg_bytes(wl, fused=False)},
+                           "step_alg_bytes": step_alg_bytes(wl, fused=False, variant=kind)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": ("decode_kernel<FUSED>" if kind == "inputs"
-                                else "replay_kernel<FUSED>"),
+                     "kernel": ("replay_kernel<FUSED>" if kind == "delta"
+                                else "decode_kernel<FUSED>"),
                      "alg_bytes_per_t": bytes_t,
                      "us_per_t": [round(float(x), 3) for x in dec_us],
                      "timing": f"HIP events around {NB} back-to-back launches per t"},
     }
 
-    # ---- A/B: the other record kind (inputs: k, v, alpha, beta with the
-    # backward query fold; delta: the paper's (alpha, delta, k) with forward
-    # replay), same workload and protocol
+    # ---- A/B: the other record variants (borrowed or copied input records
+    # with the backward query fold; the paper's (alpha, delta, k) records with
+    # forward replay), same workload and protocol
     if not args.skip_ab:
-        other = "delta" if kind == "inputs" else "inputs"
-        ms_o = timed_steps(True, K, args.warmup, other)
-        us_o = fused_kernel_us(other)
-        bytes_o = [kernel_alg_bytes(wl, t, other) for t in range(T)]
-        result["record_kind_ab"] = {
-            "records": other, "ms_per_step": ms_o,
-            "beam_tokens_per_s": beam_tokens_per_step / (ms_o / 1e3),
-            "fused_kernel_us_per_t": [round(float(x), 3) for x in us_o],
-            "alg_bytes_per_t": bytes_o,
-            "achieved_GBs": sum(bytes_o) / (us_o.sum() * 1e-6) / 1e9}
-        log(f"[bench] A/B {other} records: {ms_o * 1e3:.1f} us/step, kernel us per t "
-            f"{np.round(us_o, 2).tolist()}")
+        result["record_variant_ab"] = {}
+        for other in VARIANTS:
+            if other == kind:
+                continue
+            ms_o = timed_steps(True, K, args.warmup, other)
+            us_o = fused_kernel_us(other)
+            bytes_o = [kernel_alg_bytes(wl, t, other) for t in range(T)]
+            result["record_variant_ab"][other] = {
+                "ms_per_step": ms_o,
+                "beam_tokens_per_s": beam_tokens_per_step / (ms_o / 1e3),
+                "fused_kernel_us_per_t": [round(float(x), 3) for x in us_o],
+                "alg_bytes_per_t": bytes_o,
+                "achieved_GBs": sum(bytes_o) / (us_o.sum() * 1e-6) / 1e9}
+            log(f"[bench] A/B {other}: {ms_o * 1e3:.1f} us/step, kernel us per t "
+                f"{np.round(us_o, 2).tolist()}")
 
     # ---- per-beam FullState GPU baseline
     if not args.skip_fullstate:
@@ -542,7 +562,7 @@ def main():
         del src, dst
     result["copy_ceiling"] = ceil
     result["roofline"]["frac_of_copy_ceiling_same_size"] = achieved / ceil["same_size"]["GB/s"]
-    traffic = measured_traffic(name) if kind == "inputs" else None
+    traffic = measured_traffic(name, kind)
     if traffic is not None:
         result["roofline"]["traffic"] = float(np.mean(traffic))
         result["roofline"]["traffic_per_t"] = traffic

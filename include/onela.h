@@ -67,6 +67,19 @@ typedef enum { ONELA_F32 = 0, ONELA_BF16 = 1 } onela_dtype_t;
  *   in fp16 for bf16 io (fp32 for fp32 io). */
 typedef enum { ONELA_RECORD_INPUTS = 0, ONELA_RECORD_DELTA = 1 } onela_record_kind_t;
 
+/* Where ONELA_RECORD_INPUTS records live (Sec. 3.3: a step's records are
+ * written once, into the current step's physical slots, and never moved).
+ * ONELA_RECORDS_COPY: the library copies each step's (k, v, alpha, beta) into
+ *   its workspace arena; the caller may reuse its buffers once the step's
+ *   launch has run.
+ * ONELA_RECORDS_BORROW: the caller's step-t buffers ARE the slab of step t
+ *   (zero copy): appending only registers their addresses.  The caller keeps
+ *   k, v, alpha and beta of every step of the current beam search allocated
+ *   and unmodified until onela_reset or onela_destroy.  The workspace then has
+ *   no record arena.  Not available with ONELA_RECORD_DELTA (delta records are
+ *   computed by the library and must be stored). */
+typedef enum { ONELA_RECORDS_COPY = 0, ONELA_RECORDS_BORROW = 1 } onela_record_storage_t;
+
 /* Shape of one decode context.  Supported (d_k, d_v): (32, 32), (64, 64),
  * (128, 128) with io_dtype ONELA_BF16 or ONELA_F32, and (128, 256), (128, 512),
  * (256, 256), (256, 512) with ONELA_BF16; num_v_heads a multiple of num_qk_heads;
@@ -82,6 +95,7 @@ typedef struct {
   int32_t max_steps;    /* T_max: decode steps 0 .. T_max - 1 */
   int32_t io_dtype;     /* onela_dtype_t of q, k, v */
   int32_t record_kind;  /* onela_record_kind_t */
+  int32_t record_storage; /* onela_record_storage_t */
 } onela_config_t;
 
 /* Human-readable name of a status code (static string). */
@@ -94,10 +108,11 @@ onela_status_t onela_check_config(const onela_config_t* cfg);
 /* Bytes of device workspace onela_init needs for cfg (0 if cfg is invalid).
  * Layout (each part 256-byte aligned): status word, double-buffered ancestry
  * index [2][R][W_max][T_max] int32, S_ctx split into bf16 high/low halves
- * (written by the step-0 launch, read by later steps), and the record arena:
- * k [R][T_max][H_K][W_max][d_k], v [R][T_max][H_V][W_max][d_v] in the io
- * dtype, (alpha, beta) [R][T_max][H_V][W_max] fp32 pairs and, for
- * ONELA_RECORD_DELTA, delta [R][T_max][H_V][W_max][d_v] (fp16 / fp32). */
+ * (written by the step-0 launch, read by later steps), and, unless records
+ * are borrowed, the record arena: k [R][T_max][H_K][W_max][d_k],
+ * v [R][T_max][H_V][W_max][d_v] in the io dtype, (alpha, beta)
+ * [R][T_max][H_V][W_max] fp32 pairs and, for ONELA_RECORD_DELTA,
+ * delta [R][T_max][H_V][W_max][d_v] (fp16 / fp32). */
 size_t onela_workspace_bytes(const onela_config_t* cfg);
 
 /* Creates a decode context and binds the shared post-prefill state
@@ -141,7 +156,9 @@ onela_status_t onela_resolve_ancestry(onela_ctx_t ctx, int32_t step,
 
 /* Appends the records of step `step` into the arena (Sec. 3.3: records are
  * written once to the physical slots of the current step and never
- * relocated).  Slot b of step t holds beam b's (k, v, alpha, beta).
+ * relocated).  Slot b of step t holds beam b's (k, v, alpha, beta).  With
+ * ONELA_RECORDS_BORROW nothing is enqueued: the four buffers become step t's
+ * slab and must stay valid for the rest of the beam search.
  *   k     device [R][W_t][H_K][d_k] io dtype
  *   v     device [R][W_t][H_V][d_v] io dtype
  *   alpha device fp32 [R][W_t][H_V]   (decay, Eq. 1)

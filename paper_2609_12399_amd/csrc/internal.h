@@ -23,6 +23,7 @@ struct Shape {
   int wmax, tmax;
   bool bf16;  // q/k/v stored as bf16 bits (else fp32)
   bool delta;  // records are (alpha, delta, k) transition records (else step inputs)
+  bool borrow;  // step-input records stay in the caller's buffers (no arena copy)
   int io_bytes() const { return bf16 ? 2 : 4; }
 };
 
@@ -36,6 +37,13 @@ struct Arena {
   void* v;           // [R][tmax][HV][wmax][dv] io dtype
   float2* ab;        // [R][tmax][HV][wmax] (alpha, beta)
   void* d;           // delta records [R][tmax][HV][wmax][dv], fp16 (bf16 io) / fp32; or null
+  // borrowed records (Shape::borrow): the caller's buffers of step j,
+  // k [R][w[j]][HK][dk], v [R][w[j]][HV][dv], alpha / beta [R][w[j]][HV]
+  const void* bk[kMaxSteps];
+  const void* bv[kMaxSteps];
+  const float* balpha[kMaxSteps];
+  const float* bbeta[kMaxSteps];
+  int bw[kMaxSteps];
 };
 
 // Bytes of each region, in workspace order, each rounded up to 256.

@@ -80,6 +80,13 @@ struct DecodeParams {
   uint4* s_frag;    // S_ctx split into bf16 hi/lo, A-fragment order (written at step 0)
   void* ak;
   void* av;
+  // borrowed records: per-step caller buffers (see Arena); borrow != 0 selects them
+  int borrow;
+  const void* bk[kMaxSteps];
+  const void* bv[kMaxSteps];
+  const float* balpha[kMaxSteps];
+  const float* bbeta[kMaxSteps];
+  int bw[kMaxSteps];
   float2* ab;
   const int* anc_rd;  // h_t (DECODE) or h_{t-1} (FUSED)
   int* anc_wr;        // FUSED: h_t
@@ -161,13 +168,36 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   // uniform bases (per workgroup)
   const int* anc_r = p.anc_rd + long(r) * wmax * tmax;
   const unsigned kslot = DK * IOB, vslot = DV * IOB;
-  auto k_slab = [&](int j) {  // arena k rows of (r, j, hk)
+  // Record rows of step j: slot s of (r, j, head) at slab(j) + s * stride.
+  // Arena: head-major slabs, stride one row.  Borrowed: the caller's step-j
+  // buffers, beam-major, stride one beam.
+  const bool borrow = p.borrow != 0;
+  const unsigned kstride = borrow ? unsigned(p.HK) * kslot : kslot;
+  const unsigned vstride = borrow ? unsigned(p.HV) * vslot : vslot;
+  auto k_slab = [&](int j) -> char* {
+    if (borrow)
+      return const_cast<char*>(static_cast<const char*>(p.bk[j])) +
+             (long(r) * p.bw[j] * p.HK + hk) * long(kslot);
     return static_cast<char*>(p.ak) + ((long(r) * tmax + j) * p.HK + hk) * wmax * long(kslot);
   };
-  auto v_slab = [&](int j) {
+  auto v_slab = [&](int j) -> char* {
+    if (borrow)
+      return const_cast<char*>(static_cast<const char*>(p.bv[j])) +
+             (long(r) * p.bw[j] * p.HV + hv) * long(vslot);
     return static_cast<char*>(p.av) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
   };
   auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
+  // slot bound of step j's records (borrowed buffers hold exactly w[j] beams)
+  auto slot_ok = [&](int j, int sl) {
+    return unsigned(sl) < unsigned(borrow ? p.bw[j] : wmax);
+  };
+  auto load_ab = [&](int j, int slot) -> float2 {
+    if (borrow) {
+      const long i = (long(r) * p.bw[j] + slot) * p.HV + hv;
+      return make_float2(p.balpha[j][i], p.bbeta[j][i]);
+    }
+    return ab_slab(j)[slot];
+  };
 
   // ---- round 1: indices (parents in FUSED mode, h_t otherwise), then every
   // load that needs no index: the query and the beam's own step-t record
@@ -215,11 +245,11 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       const char* ks = k_slab(NA);
 #pragma unroll
       for (int c = 0; c < C8; ++c)
-        kr[NA][c].load(ks, fbc * kslot + li * EPL * IOB + c * K8::kBytes);
-      abr[NA] = ab_slab(NA)[fbc];
+        kr[NA][c].load(ks, fbc * kstride + li * EPL * IOB + c * K8::kBytes);
+      abr[NA] = load_ab(NA, fbc);
       const char* vs = v_slab(NA);
 #pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb) vr[nb][NA].load(vs, sbc[nb] * vslot + row0 * IOB);
+      for (int nb = 0; nb < NBLK; ++nb) vr[nb][NA].load(vs, sbc[nb] * vstride + row0 * IOB);
     }
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -233,8 +263,8 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   auto load_fold_record = [&](int j, int slot) {
     const char* ks = k_slab(j);
 #pragma unroll
-    for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
-    abr[j] = ab_slab(j)[slot];
+    for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kstride + li * EPL * IOB + c * K8::kBytes);
+    abr[j] = load_ab(j, slot);
   };
   if constexpr (FUSED && NA > 0) {
     fpok = unsigned(fpar) < unsigned(p.W_prev);
@@ -248,7 +278,7 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
       ps[nb] = spok[nb] ? spar[nb] : 0;
       ssrc[nb][NA - 1] = ps[nb];
-      vr[nb][NA - 1].load(v_slab(NA - 1), ps[nb] * vslot + row0 * IOB);
+      vr[nb][NA - 1].load(v_slab(NA - 1), ps[nb] * vstride + row0 * IOB);
     }
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
@@ -259,28 +289,28 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) {
-      fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
+      fok[j] = fpok && slot_ok(j, fsrc[j]);
       load_fold_record(j, fok[j] ? fsrc[j] : 0);
     }
 #pragma unroll
     for (int nb = 0; nb < NBLK; ++nb)
 #pragma unroll
       for (int j = 0; j < NA - 1; ++j) {
-        const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
-        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+        const bool ok = spok[nb] && slot_ok(j, ssrc[nb][j]);
+        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vstride + row0 * IOB);
       }
   } else {
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
-      fok[j] = unsigned(fsrc[j]) < unsigned(wmax);
+      fok[j] = slot_ok(j, fsrc[j]);
       load_fold_record(j, fok[j] ? fsrc[j] : 0);
     }
 #pragma unroll
     for (int nb = 0; nb < NBLK; ++nb)
 #pragma unroll
       for (int j = 0; j < NA; ++j) {
-        const bool ok = unsigned(ssrc[nb][j]) < unsigned(wmax);
-        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
+        const bool ok = slot_ok(j, ssrc[nb][j]);
+        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vstride + row0 * IOB);
       }
   }
 
@@ -370,17 +400,20 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
         }
         if (!fpok) atomicOr(p.status, kStatusParent);
       }
-      if (hv % p.G == 0) {
+      if (!borrow && hv % p.G == 0) {
         char* ks = k_slab(NA);
 #pragma unroll
         for (int c = 0; c < C8; ++c)
           kr[NA][c].store(ks, fbeam * kslot + li * EPL * IOB + c * K8::kBytes);
       }
-      if (li == 0) ab_slab(NA)[fbeam] = abr[NA];
+      if (!borrow && li == 0) ab_slab(NA)[fbeam] = abr[NA];
     }
+    if (!borrow) {
 #pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-      if (b0 + nb * 16 + (lane & 15) < W) vr[nb][NA].store(v_slab(NA), sbc[nb] * vslot + row0 * IOB);
+      for (int nb = 0; nb < NBLK; ++nb)
+        if (b0 + nb * 16 + (lane & 15) < W)
+          vr[nb][NA].store(v_slab(NA), sbc[nb] * vslot + row0 * IOB);
+    }
   }
   __syncthreads();
 
@@ -517,6 +550,14 @@ DecodeParams base_params(const Shape& s, int width, const void* q, float* o, con
   prm.ak = a.k;
   prm.av = a.v;
   prm.ab = a.ab;
+  prm.borrow = s.borrow ? 1 : 0;
+  for (int j = 0; j < kMaxSteps; ++j) {
+    prm.bk[j] = a.bk[j];
+    prm.bv[j] = a.bv[j];
+    prm.balpha[j] = a.balpha[j];
+    prm.bbeta[j] = a.bbeta[j];
+    prm.bw[j] = a.bw[j];
+  }
   prm.status = a.status;
   prm.R = s.R;
   prm.HK = s.HK;

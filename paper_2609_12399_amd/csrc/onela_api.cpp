@@ -40,9 +40,14 @@ onela_status_t shape_of(const onela_config_t* c, Shape* s) {
   if (c->io_dtype != ONELA_F32 && c->io_dtype != ONELA_BF16) return ONELA_EINVAL;
   if (c->record_kind != ONELA_RECORD_INPUTS && c->record_kind != ONELA_RECORD_DELTA)
     return ONELA_EINVAL;
+  if (c->record_storage != ONELA_RECORDS_COPY && c->record_storage != ONELA_RECORDS_BORROW)
+    return ONELA_EINVAL;
+  if (c->record_storage == ONELA_RECORDS_BORROW && c->record_kind == ONELA_RECORD_DELTA)
+    return ONELA_EINVAL;
   Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads,
           c->d_k,          c->d_v,          c->max_beams,
-          c->max_steps,    c->io_dtype == ONELA_BF16, c->record_kind == ONELA_RECORD_DELTA};
+          c->max_steps,    c->io_dtype == ONELA_BF16, c->record_kind == ONELA_RECORD_DELTA,
+          c->record_storage == ONELA_RECORDS_BORROW};
   if (!onela::decode_supported(t)) return ONELA_EINVAL;
   // the kernels form 32-bit byte offsets: every region must stay below 2 GiB
   const double big = double(t.R) * t.tmax * (t.HV > t.HK ? t.HV : t.HK) * t.wmax *
@@ -56,6 +61,16 @@ onela_status_t shape_of(const onela_config_t* c, Shape* s) {
 
 bool launch_ok(hipError_t e) { return e == hipSuccess; }
 
+// Registers the caller's buffers as step t's record slab (borrowed records).
+void borrow_step(onela_ctx_s* c, int t, const void* k, const void* v, const float* alpha,
+                 const float* beta) {
+  c->arena.bk[t] = k;
+  c->arena.bv[t] = v;
+  c->arena.balpha[t] = alpha;
+  c->arena.bbeta[t] = beta;
+  c->arena.bw[t] = c->widths[t];
+}
+
 }  // namespace
 
 namespace onela {
@@ -66,9 +81,10 @@ Layout layout_of(const Shape& s) {
   l.status = 256;
   l.anc = round256(sizeof(int) * R * W * T);
   l.s_frag = round256(sizeof(uint16_t) * 2 * R * s.HV * size_t(s.dv) * s.dk);
-  l.k = round256(size_t(s.io_bytes()) * R * T * s.HK * W * s.dk);
-  l.v = round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
-  l.ab = round256(sizeof(float2) * R * T * s.HV * W);
+  const size_t arena = s.borrow ? 0 : 1;  // borrowed records need no arena
+  l.k = arena * round256(size_t(s.io_bytes()) * R * T * s.HK * W * s.dk);
+  l.v = arena * round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
+  l.ab = arena * round256(sizeof(float2) * R * T * s.HV * W);
   l.d = s.delta ? l.v : 0;  // delta rows take the size of input v rows (fp16 / fp32)
   l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab + l.d;
   return l;
@@ -129,11 +145,11 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   c->arena.s0 = s0;
   c->arena.s_frag = reinterpret_cast<uint16_t*>(p);
   p += l.s_frag;
-  c->arena.k = p;
+  c->arena.k = s.borrow ? nullptr : p;
   p += l.k;
-  c->arena.v = p;
+  c->arena.v = s.borrow ? nullptr : p;
   p += l.v;
-  c->arena.ab = reinterpret_cast<float2*>(p);
+  c->arena.ab = s.borrow ? nullptr : reinterpret_cast<float2*>(p);
   p += l.ab;
   c->arena.d = s.delta ? p : nullptr;
 
@@ -179,9 +195,13 @@ onela_status_t onela_append_records(onela_ctx_t c, int32_t step, const void* k,
   if (!k || !v || !alpha || !beta) return ONELA_EINVAL;
   if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta))
     return ONELA_EINVAL;
-  hipError_t e = onela::launch_append(c->shape, step, c->widths[step], k, v, alpha,
-                                      beta, c->arena, c->stream);
-  if (!launch_ok(e)) return ONELA_EHIP;
+  if (c->shape.borrow) {
+    borrow_step(c, step, k, v, alpha, beta);
+  } else {
+    hipError_t e = onela::launch_append(c->shape, step, c->widths[step], k, v, alpha,
+                                        beta, c->arena, c->stream);
+    if (!launch_ok(e)) return ONELA_EHIP;
+  }
   c->appended = step;
   return ONELA_OK;
 }
@@ -223,6 +243,7 @@ onela_status_t onela_decode_step_fused(onela_ctx_t c, int32_t step, int32_t widt
                                                     beta, q, o, gather_out, c->arena, c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
   c->widths[step] = width;
+  if (s.borrow) borrow_step(c, step, k, v, alpha, beta);
   c->resolved = step;
   c->appended = step;
   if (step == 0) c->status_live = true;

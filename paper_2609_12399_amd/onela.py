@@ -21,6 +21,7 @@ ONELA_OK, ONELA_EINVAL, ONELA_ESTEP, ONELA_EPARENT = 0, 1, 2, 3
 ONELA_ECAPACITY, ONELA_EHIP, ONELA_ENOMEM = 4, 5, 6
 ONELA_F32, ONELA_BF16 = 0, 1
 ONELA_RECORD_INPUTS, ONELA_RECORD_DELTA = 0, 1
+ONELA_RECORDS_COPY, ONELA_RECORDS_BORROW = 0, 1
 
 STATUS_NAMES = {0: "ONELA_OK", 1: "ONELA_EINVAL", 2: "ONELA_ESTEP", 3: "ONELA_EPARENT",
                 4: "ONELA_ECAPACITY", 5: "ONELA_EHIP", 6: "ONELA_ENOMEM"}
@@ -45,17 +46,20 @@ class onela_config_t(ctypes.Structure):
                 ("num_v_heads", ctypes.c_int32), ("d_k", ctypes.c_int32),
                 ("d_v", ctypes.c_int32), ("max_beams", ctypes.c_int32),
                 ("max_steps", ctypes.c_int32), ("io_dtype", ctypes.c_int32),
-                ("record_kind", ctypes.c_int32)]
+                ("record_kind", ctypes.c_int32), ("record_storage", ctypes.c_int32)]
 
 
 def make_config(num_requests, num_qk_heads, num_v_heads, d_k, d_v, max_beams, max_steps,
-                io_dtype, record_kind=ONELA_RECORD_INPUTS) -> onela_config_t:
+                io_dtype, record_kind=ONELA_RECORD_INPUTS,
+                record_storage=ONELA_RECORDS_COPY) -> onela_config_t:
     if isinstance(io_dtype, str):
         io_dtype = {"bf16": ONELA_BF16, "f32": ONELA_F32}[io_dtype]
     if isinstance(record_kind, str):
         record_kind = {"inputs": ONELA_RECORD_INPUTS, "delta": ONELA_RECORD_DELTA}[record_kind]
+    if isinstance(record_storage, str):
+        record_storage = {"copy": ONELA_RECORDS_COPY, "borrow": ONELA_RECORDS_BORROW}[record_storage]
     return onela_config_t(num_requests, num_qk_heads, num_v_heads, d_k, d_v, max_beams,
-                          max_steps, io_dtype, record_kind)
+                          max_steps, io_dtype, record_kind, record_storage)
 
 
 _lib = None

@@ -67,9 +67,11 @@ def to_device(wl: Workload, device="cuda:0", with_prompt: bool = True) -> Device
 
 
 def config_for(spec: WorkloadSpec, max_beams: int | None = None,
-               max_steps: int | None = None, records: str = "inputs") -> ab.onela_config_t:
+               max_steps: int | None = None, records: str = "inputs",
+               storage: str = "copy") -> ab.onela_config_t:
     return ab.make_config(spec.R, spec.HK, spec.HV, spec.dk, spec.dv,
-                          max_beams or spec.W, max_steps or spec.T, spec.io_dtype, records)
+                          max_beams or spec.W, max_steps or spec.T, spec.io_dtype, records,
+                          storage)
 
 
 def prefill_state(spec: WorkloadSpec, prompt, device="cuda:0", stream=None):
@@ -87,10 +89,13 @@ class Decoder:
 
     def __init__(self, spec: WorkloadSpec, s0, device="cuda:0", stream=None,
                  max_beams: int | None = None, max_steps: int | None = None,
-                 records: str = "inputs"):
+                 records: str = "inputs", storage: str = "copy"):
+        """storage="borrow": the steps' k/v/alpha/beta tensors are the record
+        slabs and must outlive the beam search (run() keeps them referenced)."""
         torch = _torch()
         self.spec = spec
-        self.cfg = config_for(spec, max_beams, max_steps, records)
+        self.cfg = config_for(spec, max_beams, max_steps, records, storage)
+        self._borrowed = []
         self.ws_bytes = ab.onela_workspace_bytes(self.cfg)
         if self.ws_bytes == 0:
             raise ab.OnelaError(ab.ONELA_EINVAL, "onela_workspace_bytes")
@@ -100,6 +105,8 @@ class Decoder:
         self.ctx = ab.onela_init(self.cfg, s0, self.workspace, self.ws_bytes, stream)
 
     def step(self, t: int, st: DeviceStep, o, gather_out=None, fused: bool = False):
+        if self.cfg.record_storage == ab.ONELA_RECORDS_BORROW:
+            self._borrowed.append(st)
         if fused:
             ab.onela_decode_step_fused(self.ctx, t, st.width, st.parents, st.k, st.v, st.alpha,
                                        st.beta, st.q, o, gather_out)
@@ -125,6 +132,7 @@ class Decoder:
 
     def reset(self):
         ab.onela_reset(self.ctx)
+        self._borrowed = []
 
     def status(self) -> int:
         return ab.onela_get_device_status(self.ctx)

@@ -53,6 +53,11 @@ def test_config_validation(lib):
         assert ab.onela_check_config(cfg(d_k=dk, d_v=dv)) == ab.ONELA_EINVAL, (dk, dv)
     assert ab.onela_check_config(cfg(record_kind=ab.ONELA_RECORD_DELTA)) == ab.ONELA_OK
     assert ab.onela_check_config(cfg(record_kind=2)) == ab.ONELA_EINVAL
+    assert ab.onela_check_config(cfg(record_storage=ab.ONELA_RECORDS_BORROW)) == ab.ONELA_OK
+    assert ab.onela_check_config(cfg(record_storage=2)) == ab.ONELA_EINVAL
+    # delta records are computed by the library: they cannot be borrowed
+    assert ab.onela_check_config(cfg(record_kind=ab.ONELA_RECORD_DELTA,
+                                     record_storage=ab.ONELA_RECORDS_BORROW)) == ab.ONELA_EINVAL
     bad = [dict(num_v_heads=24, num_qk_heads=16), dict(d_k=96, d_v=96), dict(d_k=128, d_v=64),
            dict(max_beams=0), dict(max_beams=65537), dict(max_steps=0), dict(max_steps=9),
            dict(io_dtype=7), dict(num_requests=0), dict(num_qk_heads=0)]
@@ -72,6 +77,9 @@ def test_workspace_bytes_layout(lib):
     # transition records add a delta arena the size of the v arena (fp16 rows)
     nd = ab.onela_workspace_bytes(cfg(record_kind=ab.ONELA_RECORD_DELTA))
     assert nd == n + T * H * W * d * 2
+    # borrowed records: no arena at all
+    nb = ab.onela_workspace_bytes(cfg(record_storage=ab.ONELA_RECORDS_BORROW))
+    assert nb == 256 + 2 * (W * T * 4) + 2 * 2 * H * d * d
 
 
 def test_host_errors_before_any_hip_call(lib):

@@ -20,9 +20,10 @@ torch = pytest.importorskip("torch")
 DEV = "cuda:0"
 
 
-def run_gpu(wl, s0, with_gather=True, fused=False, records="inputs"):
+def run_gpu(wl, s0, with_gather=True, fused=False, records="inputs", storage="copy"):
     dw = runner.to_device(wl, DEV, with_prompt=False)
-    dec = runner.Decoder(wl.spec, torch.from_numpy(s0).to(DEV), DEV, records=records)
+    dec = runner.Decoder(wl.spec, torch.from_numpy(s0).to(DEV), DEV, records=records,
+                         storage=storage)
     gathers = None
     if with_gather:
         gathers = [torch.full((wl.spec.R, st.width, max(t, 1)), -7, dtype=torch.int32,
@@ -348,6 +349,69 @@ def test_delta_records_bad_parent_and_mixed_forms(fused):
     dw = runner.to_device(wl, DEV, with_prompt=False)
     dec = runner.Decoder(spec, torch.from_numpy(s0).to(DEV), DEV, records="delta")
     outs = dec.run(dw, fused=[fused, not fused, fused])
+    assert dec.status() == ab.ONELA_EPARENT
+    o = [x.cpu().numpy() for x in outs]
+    keep1 = np.arange(16) != bad_beam
+    keep2 = wl.steps[2].parents[0] != bad_beam
+    assert rel_err(o[1][0][keep1], ref[1][0][keep1]) <= REL_TOL
+    assert rel_err(o[2][0][keep2], ref[2][0][keep2]) <= REL_TOL
+    dec.close()
+
+
+# Borrowed record slabs (zero-copy append): the caller's per-step buffers are
+# read in place.  Same arithmetic as the arena copy, so the outputs must be
+# bitwise identical to it, and within the bar of the oracle.
+@pytest.mark.parametrize("name", list(W.SPECS))
+def test_borrowed_records_match_oracle(name):
+    log(f"[borrow] {name}")
+    wl, s0, ref = cached_case(name)
+    anc = oracle_ancestry(wl)
+    for fused in (False, True, [True, False] * 4):
+        pat = fused if isinstance(fused, bool) else fused[:wl.spec.T]
+        o, g = run_gpu(wl, s0, fused=pat, storage="borrow")
+        oc, _ = run_gpu(wl, s0, fused=pat, storage="copy")
+        for t in range(wl.spec.T):
+            assert np.array_equal(g[t], anc[t])
+            assert np.array_equal(o[t], oc[t]), f"step {t}: borrow != copy"
+        errs = [rel_err(o[t], ref[t]) for t in range(wl.spec.T)]
+        log(f"[borrow] {name} fused={pat} max rel err {max(errs):.2e}")
+        assert max(errs) <= REL_TOL
+
+
+@pytest.mark.parametrize("widths", [(16, 40, 7, 33), (48, 3, 64)])
+def test_borrowed_records_ragged_widths(widths):
+    """Each borrowed slab holds exactly W_t beams (no W_max padding)."""
+    spec = W.with_widths("h16_d128_w128", widths)
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    for fused in (False, True):
+        o, _ = run_gpu(wl, s0, fused=fused, storage="borrow")
+        assert max(rel_err(o[t], ref[t]) for t in range(spec.T)) <= REL_TOL
+
+
+@pytest.mark.parametrize("spec", WIDE, ids=[s.name for s in WIDE])
+def test_borrowed_records_wide_geometries(spec):
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    o, _ = run_gpu(wl, s0, fused=True, storage="borrow")
+    assert max(rel_err(o[t], ref[t]) for t in range(spec.T)) <= REL_TOL
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_borrowed_records_bad_parent_contained(fused):
+    spec = _small(widths=(16, 16, 16), seed=21)
+    wl = W.make_workload(spec)
+    bad_beam = 5
+    wl.steps[1].parents[0, bad_beam] = 16
+    good_wl = W.make_workload(spec)
+    good_wl.steps[1].parents[0, bad_beam] = 0
+    s0 = oracle_s0(good_wl)
+    ref, _ = oracle_outputs(good_wl, s0)
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    dec = runner.Decoder(spec, torch.from_numpy(s0).to(DEV), DEV, storage="borrow")
+    outs = dec.run(dw, fused=fused)
     assert dec.status() == ab.ONELA_EPARENT
     o = [x.cpu().numpy() for x in outs]
     keep1 = np.arange(16) != bad_beam
