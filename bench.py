@@ -423,7 +423,7 @@ def main():
                                "delta": "(alpha, delta fp16, k) transition records"}[kind],
                    "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
                                   "fp32 accum",
-                   "graph": not args.no_graph, "batches": NB},
+                   "variant": kind, "graph": not args.no_graph, "batches": NB},
         "decode_step_us": {"per_t": [round(float(x), 3) for x in dec_us],
                            "mean": round(float(dec_us.mean()), 3)},
         "beam_tokens_per_step": beam_tokens_per_step,
