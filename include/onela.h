@@ -217,6 +217,25 @@ onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len
                                    const float* alpha, const float* beta,
                                    float* s0_out, void* stream);
 
+/* ---- Chunked prefill of S_ctx (Sec. 3.1; Eq. 1 over the prompt) ----------
+ * Same result as onela_prefill_state (Eq. 1 from S = 0 over the prompt, fp32
+ * state), computed in chunks of 64 tokens: per chunk, the correction terms
+ * delta_t of Eq. 2 solve a unit lower-triangular 64 x 64 system whose
+ * matrices depend only on the chunk's own tokens (formed for all chunks in
+ * parallel); a second launch then carries the state across the chunks in
+ * order, on fp32 MFMA.  Inputs and output as for onela_prefill_state.
+ * Workspace: onela_prefill_workspace_bytes(cfg, prompt_len) bytes (0 for an
+ * empty prompt, or for an invalid cfg), 256-byte aligned, owned by the caller
+ * and used only by the enqueued work: per (request, value head, chunk) the
+ * fp32 matrices W [64][d_k], Kt^T [d_k][64], U^T [d_v][64] and one decay.
+ * Errors: ONELA_EINVAL, ONELA_ECAPACITY (workspace too small), ONELA_EHIP. */
+size_t onela_prefill_workspace_bytes(const onela_config_t* cfg, int32_t prompt_len);
+onela_status_t onela_prefill_state_chunked(const onela_config_t* cfg, int32_t prompt_len,
+                                           const void* k, const void* v,
+                                           const float* alpha, const float* beta,
+                                           float* s0_out, void* workspace,
+                                           size_t workspace_bytes, void* stream);
+
 /* ---- Baseline: per-beam materialised states ("FullState", Sec. 2.3) ----
  * Every live beam keeps a full fp32 d_v x d_k state per value head.  One
  * call performs step t for all beams: copy the parent's state (S_ctx at

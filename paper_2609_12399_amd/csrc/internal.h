@@ -84,6 +84,13 @@ hipError_t launch_fullstate(const Shape& s, int step, int width, int prev_width,
 // True when the decode kernel has an instance for this shape.
 bool decode_supported(const Shape& s);
 
+// ---- chunked prefill --------------------------------------------------------
+constexpr int kPrefillChunk = 64;  // tokens per chunk
+size_t prefill_chunked_workspace_bytes(const Shape& s, int prompt_len);
+hipError_t launch_prefill_chunked(const Shape& s, int prompt_len, const void* k, const void* v,
+                                  const float* alpha, const float* beta, float* s0_out,
+                                  void* workspace, hipStream_t st);
+
 // ---- global top-W beam selection ------------------------------------------
 constexpr int kSelectThreads = 512;            // one workgroup
 constexpr int kSelectChunk = 16384;            // candidates per workgroup

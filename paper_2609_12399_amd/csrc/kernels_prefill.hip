@@ -1,0 +1,341 @@
+// Chunked prefill of the shared post-prefill state S_ctx (Sec. 3.1) on gfx950:
+// Eq. 1 (Sec. 2.2) over a prompt, from S = 0, in chunks of C = 64 tokens.
+//
+// Inside a chunk that starts from state S_0, write Eq. 1 with the paper's
+// correction term (Eq. 2), delta_t = beta_t (v_t - alpha_t S_{t-1} k_t), as
+// S_t = alpha_t S_{t-1} + delta_t k_t^T.  Unrolling it with
+// Gamma(t, i) = alpha_{i+1} ... alpha_t and gamma_t = Gamma(t, -1):
+//   S_t     = gamma_t S_0 + sum_{i<=t} Gamma(t, i) delta_i k_i^T
+//   delta_t = beta_t v_t - beta_t gamma_t S_0 k_t
+//             - sum_{i<t} beta_t Gamma(t, i) (k_t . k_i) delta_i.
+// With M the strictly lower C x C matrix M(t, i) = beta_t Gamma(t, i) (k_t.k_i)
+// and T = (I + M)^{-1} (unit lower triangular), the deltas of the chunk are
+//   D = U - W S_0^T,   U = T diag(beta) V,   W = T diag(beta gamma) K,
+// and the state after the chunk is
+//   S_C = g S_0 + D^T Kt,   Kt = diag(sigma) K,  sigma_t = Gamma(C - 1, t),
+// g = gamma_{C-1}.  U, W and Kt depend only on the chunk's own tokens.
+//
+//   phase 1 (prefill_chunk_kernel): one workgroup per (request, value head,
+//     chunk) forms Gamma, M, T (column-parallel forward substitution), W, U
+//     and Kt in LDS with fp32 FMAs and stores W [C][d_k], Kt^T [d_k][C],
+//     U^T [d_v][C] and g to the workspace.  No division: products of alpha
+//     are formed directly, so alpha = 0 is exact.
+//   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
+//     state rows) walks the chunks in order: X^T = W S^T, D^T = U^T - X^T,
+//     S^T <- g S^T + Kt^T D^T, on v_mfma_f32_16x16x4f32.  Wave w owns the
+//     state columns 16 w .. 16 w + 15 (a 16 x 16 fp32 accumulator tile that
+//     never leaves registers); the contraction orders are chosen so that the
+//     tile is directly the B operand of the next chunk's X and X's output is
+//     directly the B operand of the update.  The partial X of the waves are
+//     summed through LDS.
+// A ragged last chunk is padded with alpha = 1, beta = 0, k = v = 0, which
+// leaves the state unchanged.
+#include <type_traits>
+
+#include "internal.h"
+
+namespace onela {
+namespace {
+
+constexpr int kC = kPrefillChunk;  // tokens per chunk
+constexpr int kP1Threads = 256;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct PrefillParams {
+  const void* k;      // [R][P][HK][DK] io dtype
+  const void* v;      // [R][P][HV][DV] io dtype
+  const float* alpha; // [R][P][HV]
+  const float* beta;
+  float* s_out;       // [R][HV][DV][DK]
+  float* wb;          // [R*HV][nch][C][DK]
+  float* ktb;         // [R*HV][nch][DK][C]
+  float* utb;         // [R*HV][nch][DV][C]
+  float* gb;          // [R*HV][nch]
+  int HK, HV, P, nch;
+};
+
+template <bool BF16>
+__device__ inline float load_io(const void* base, long i) {
+  if constexpr (BF16)
+    return __uint_as_float(unsigned(static_cast<const uint16_t*>(base)[i]) << 16);
+  else
+    return static_cast<const float*>(base)[i];
+}
+
+// ---- phase 1 ----------------------------------------------------------------
+
+template <int DK>
+struct P1Shared {
+  float K[kC][DK + 1];    // the chunk's keys, fp32 (padding rows zero)
+  float T[kC][kC + 1];    // (I + M)^{-1}, then reused
+  float M[kC][kC + 1];
+  float X[kC][128 + 1];   // a 128-column block of beta V or beta gamma K
+  float al[kC], be[kC], gam[kC], sig[kC];
+};
+
+// out[t][c0 + j] = sum_s T[t][s] X[s][j] for j < ncols (<= 128), written by
+// fn(t, j, value).  Each thread computes an 8 x 4 block (rows t0 .. t0 + 7,
+// columns 4 j0 .. 4 j0 + 3): 12 LDS reads per 32 FMAs.
+template <typename Sh, typename F>
+__device__ inline void tri_times_block(const Sh& sh, int ncols, F&& fn) {
+  const int tid = threadIdx.x;
+  const int jb = tid & 31, tb = tid >> 5;  // 32 column groups x 8 row groups
+  if (4 * jb >= ncols) return;
+  float acc[8][4] = {};
+  for (int s = 0; s < kC; ++s) {
+    float x[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[q] = sh.X[s][4 * jb + q];
+#pragma unroll
+    for (int a = 0; a < 8; ++a) {
+      const float tv = sh.T[8 * tb + a][s];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[a][q] = fmaf(tv, x[q], acc[a][q]);
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fn(8 * tb + a, 4 * jb + q, acc[a][q]);
+}
+
+template <int DK, int DV, bool BF16>
+__global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams p) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  P1Shared<DK>& sh = *reinterpret_cast<P1Shared<DK>*>(smem);
+  const int tid = threadIdx.x;
+  const int c = blockIdx.x % p.nch, unit = blockIdx.x / p.nch;
+  const int r = unit / p.HV, hv = unit - r * p.HV, hk = hv / (p.HV / p.HK);
+  const int t0 = c * kC;
+  const int n = min(kC, p.P - t0);
+  const long tok0 = long(r) * p.P + t0;
+
+  for (int i = tid; i < kC * DK; i += kP1Threads) {
+    const int t = i / DK, kk = i - t * DK;
+    sh.K[t][kk] = t < n ? load_io<BF16>(p.k, ((tok0 + t) * p.HK + hk) * DK + kk) : 0.f;
+  }
+  if (tid < kC) {
+    const bool in = tid < n;
+    sh.al[tid] = in ? p.alpha[(tok0 + tid) * p.HV + hv] : 1.f;
+    sh.be[tid] = in ? p.beta[(tok0 + tid) * p.HV + hv] : 0.f;
+  }
+  __syncthreads();
+  if (tid == 0) {  // gamma_t = alpha_0 ... alpha_t
+    float g = 1.f;
+    for (int t = 0; t < kC; ++t) {
+      g *= sh.al[t];
+      sh.gam[t] = g;
+    }
+  } else if (tid == 64) {  // sigma_t = alpha_{t+1} ... alpha_{C-1}
+    float s = 1.f;
+    for (int t = kC - 1; t >= 0; --t) {
+      sh.sig[t] = s;
+      s *= sh.al[t];
+    }
+  }
+  // M(t, i) = beta_t Gamma(t, i) (k_t . k_i) for i < t: a 4 x 4 block of
+  // (t, i) per thread, Gamma by direct products.
+  {
+    const int ib = tid & 15, tb = tid >> 4;
+    float acc[4][4] = {};
+    for (int kk = 0; kk < DK; ++kk) {
+      float kt[4], ki[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        kt[a] = sh.K[4 * tb + a][kk];
+        ki[a] = sh.K[4 * ib + a][kk];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = fmaf(kt[a], ki[b], acc[a][b]);
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int t = 4 * tb + a, i = 4 * ib + b;
+        float m = 0.f;
+        if (i < t) {
+          float gm = 1.f;
+          for (int j = i + 1; j <= t; ++j) gm *= sh.al[j];
+          m = sh.be[t] * gm * acc[a][b];
+        }
+        sh.M[t][i] = m;
+      }
+  }
+  __syncthreads();
+  // T = (I + M)^{-1}: column j by the 4 lanes 4j .. 4j + 3 (one wave holds
+  // 16 columns); T(t, j) = -sum_{j <= i < t} M(t, i) T(i, j) for t > j.
+  {
+    const int j = tid >> 2, sub = tid & 3;
+    for (int t = sub; t < kC; t += 4) sh.T[t][j] = t == j ? 1.f : 0.f;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    for (int t = 1; t < kC; ++t) {
+      float s = 0.f;
+      if (t > j)
+        for (int i = j + sub; i < t; i += 4) s = fmaf(sh.M[t][i], sh.T[i][j], s);
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      if (t > j && sub == 0) sh.T[t][j] = -s;
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    }
+  }
+  __syncthreads();
+
+  const long cu = long(unit) * p.nch + c;
+  // W = T diag(beta gamma) K  -> wb [C][DK];  Kt^T = (diag(sigma) K)^T -> ktb [DK][C]
+  float* wdst = p.wb + cu * kC * DK;
+  float* ktdst = p.ktb + cu * DK * kC;
+  for (int i = tid; i < kC * DK; i += kP1Threads) {
+    const int kk = i / kC, t = i - kk * kC;
+    ktdst[i] = sh.sig[t] * sh.K[t][kk];
+  }
+  for (int cb = 0; cb < DK; cb += 128) {
+    const int nc = DK - cb < 128 ? DK - cb : 128;
+    for (int i = tid; i < kC * nc; i += kP1Threads) {
+      const int t = i / nc, jj = i - t * nc;
+      sh.X[t][jj] = sh.be[t] * sh.gam[t] * sh.K[t][cb + jj];
+    }
+    __syncthreads();
+    tri_times_block(sh, nc, [&](int t, int jj, float x) { wdst[t * DK + cb + jj] = x; });
+    __syncthreads();
+  }
+  // U = T diag(beta) V -> utb [DV][C]
+  float* udst = p.utb + cu * DV * kC;
+  for (int cb = 0; cb < DV; cb += 128) {
+    const int nc = DV - cb < 128 ? DV - cb : 128;
+    for (int i = tid; i < kC * nc; i += kP1Threads) {
+      const int t = i / nc, jj = i - t * nc;
+      sh.X[t][jj] = t < n ? sh.be[t] * load_io<BF16>(p.v, ((tok0 + t) * p.HV + hv) * DV + cb + jj)
+                          : 0.f;
+    }
+    __syncthreads();
+    tri_times_block(sh, nc, [&](int t, int jj, float x) { udst[(cb + jj) * kC + t] = x; });
+    __syncthreads();
+  }
+  if (tid == 0) p.gb[cu] = sh.gam[kC - 1];
+}
+
+// ---- phase 2 ----------------------------------------------------------------
+
+template <int DK, int DV>
+__global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
+  constexpr int NW = DK / 16;  // waves: state columns 16 w .. 16 w + 15
+  __shared__ f32x4 xp[NW][4][64];  // partial X^T tiles of every wave
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rb = blockIdx.x % (DV / 16), unit = blockIdx.x / (DV / 16);
+  const int row0 = 16 * rb;
+  const int lr = lane & 15, lq = lane >> 4;
+  // st[i] = S^T(k = 16 w + 4 lq + i, n = lr) = S(row0 + lr, 16 w + 4 lq + i)
+  f32x4 st = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < p.nch; ++c) {
+    const long cu = long(unit) * p.nch + c;
+    const float* wc = p.wb + cu * kC * DK;
+    const float* kt = p.ktb + cu * DK * kC;
+    const float* ut = p.utb + cu * DV * kC;
+    const float g = p.gb[cu];
+    f32x4 wa[4], ka[4], ua[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      // A of X: W(t = 16 mt + lr, k = 16 w + 4 lq + i), i = 0..3
+      wa[mt] = *reinterpret_cast<const f32x4*>(wc + (16 * mt + lr) * DK + 16 * w + 4 * lq);
+      // A of the update: Kt^T(k = 16 w + lr, t = 16 mt + 4 lq + j), j = 0..3
+      ka[mt] = *reinterpret_cast<const f32x4*>(kt + (16 * w + lr) * kC + 16 * mt + 4 * lq);
+      // U^T(row0 + lr, t = 16 mt + 4 lq + j)
+      ua[mt] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
+    }
+    // partial X^T(t, n) over this wave's 16 state columns
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[mt][i], st[i], acc, 0, 0, 0);
+      xp[w][mt][lane] = acc;
+    }
+    __syncthreads();
+    // D^T(t = 16 mt + 4 lq + j, n = lr) = U^T - sum over waves of X^T
+    f32x4 dt[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      f32x4 x = xp[0][mt][lane];
+#pragma unroll
+      for (int v = 1; v < NW; ++v) x += xp[v][mt][lane];
+      dt[mt] = ua[mt] - x;
+    }
+    __syncthreads();
+    // S^T <- g S^T + Kt^T D^T
+    st *= g;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        st = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[mt][j], dt[mt][j], st, 0, 0, 0);
+  }
+  float* dst = p.s_out + (long(unit) * DV + row0 + lr) * DK + 16 * w + 4 * lq;
+  *reinterpret_cast<f32x4*>(dst) = st;
+}
+
+template <int DK, int DV, bool BF16>
+hipError_t launch_t(const Shape& s, const PrefillParams& prm, hipStream_t st) {
+  const unsigned units = unsigned(s.R * s.HV);
+  const size_t lds = sizeof(P1Shared<DK>);
+  auto k1 = prefill_chunk_kernel<DK, DV, BF16>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k1),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  if (prm.nch > 0) {  // an empty prompt leaves S = 0 (phase 2 stores zeros)
+    k1<<<units * unsigned(prm.nch), kP1Threads, lds, st>>>(prm);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  prefill_scan_kernel<DK, DV><<<units * unsigned(DV / 16), 4 * DK, 0, st>>>(prm);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t prefill_chunked_workspace_bytes(const Shape& s, int prompt_len) {
+  const size_t nch = size_t(prompt_len + kC - 1) / kC;
+  const size_t per = size_t(kC) * (2 * s.dk + s.dv) * sizeof(float);
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t units = size_t(s.R) * s.HV;
+  return up(units * nch * per) + up(units * nch * sizeof(float));
+}
+
+hipError_t launch_prefill_chunked(const Shape& s, int prompt_len, const void* k, const void* v,
+                                  const float* alpha, const float* beta, float* s0_out,
+                                  void* workspace, hipStream_t st) {
+  PrefillParams prm{};
+  prm.k = k;
+  prm.v = v;
+  prm.alpha = alpha;
+  prm.beta = beta;
+  prm.s_out = s0_out;
+  prm.HK = s.HK;
+  prm.HV = s.HV;
+  prm.P = prompt_len;
+  prm.nch = (prompt_len + kC - 1) / kC;
+  const size_t units = size_t(s.R) * s.HV, nch = size_t(prm.nch);
+  float* base = static_cast<float*>(workspace);
+  prm.wb = base;
+  prm.ktb = prm.wb + units * nch * kC * s.dk;
+  prm.utb = prm.ktb + units * nch * kC * s.dk;
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  prm.gb = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                    up(units * nch * size_t(kC) * (2 * s.dk + s.dv) * 4));
+#define ONELA_PF_SHAPE(DK, DV)                                                            \
+  if (s.dk == DK && s.dv == DV)                                                         \
+    return s.bf16 ? launch_t<DK, DV, true>(s, prm, st) : launch_t<DK, DV, false>(s, prm, st);
+  ONELA_PF_SHAPE(32, 32)
+  ONELA_PF_SHAPE(64, 64)
+  ONELA_PF_SHAPE(128, 128)
+  ONELA_PF_SHAPE(128, 256)
+  ONELA_PF_SHAPE(128, 512)
+  ONELA_PF_SHAPE(256, 256)
+  ONELA_PF_SHAPE(256, 512)
+#undef ONELA_PF_SHAPE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace onela

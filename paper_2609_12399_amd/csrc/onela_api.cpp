@@ -281,6 +281,33 @@ onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len
   return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
 }
 
+size_t onela_prefill_workspace_bytes(const onela_config_t* cfg, int32_t prompt_len) {
+  Shape s;
+  if (shape_of(cfg, &s) != ONELA_OK || prompt_len < 0) return 0;
+  return onela::prefill_chunked_workspace_bytes(s, prompt_len);
+}
+
+onela_status_t onela_prefill_state_chunked(const onela_config_t* cfg, int32_t prompt_len,
+                                           const void* k, const void* v, const float* alpha,
+                                           const float* beta, float* s0_out, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  Shape s;
+  const onela_status_t rc = shape_of(cfg, &s);
+  if (rc != ONELA_OK) return rc;
+  if (prompt_len < 0 || !s0_out || !aligned16(s0_out)) return ONELA_EINVAL;
+  if (prompt_len > 0 && (!k || !v || !alpha || !beta || !aligned16(k) || !aligned16(v) ||
+                         !aligned4(alpha) || !aligned4(beta)))
+    return ONELA_EINVAL;
+  const size_t need = onela::prefill_chunked_workspace_bytes(s, prompt_len);
+  if (need > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0))
+    return ONELA_EINVAL;
+  if (workspace_bytes < need) return ONELA_ECAPACITY;
+  const hipError_t e =
+      onela::launch_prefill_chunked(s, prompt_len, k, v, alpha, beta, s0_out, workspace,
+                                    static_cast<hipStream_t>(stream));
+  return launch_ok(e) ? ONELA_OK : ONELA_EHIP;
+}
+
 size_t onela_fullstate_workspace_bytes(const onela_config_t* cfg) {
   Shape s;
   if (shape_of(cfg, &s) != ONELA_OK) return 0;

@@ -32,7 +32,8 @@ EXPORTED = ["onela_status_str", "onela_check_config", "onela_workspace_bytes", "
             "onela_decode_step", "onela_decode_step_fused", "onela_get_device_status", "onela_destroy",
             "onela_prefill_state", "onela_fullstate_workspace_bytes", "onela_fullstate_step",
             "onela_capacity_bytes", "onela_fullstate_capacity_bytes",
-            "onela_select_workspace_bytes", "onela_select_beams"]
+            "onela_select_workspace_bytes", "onela_select_beams",
+            "onela_prefill_workspace_bytes", "onela_prefill_state_chunked"]
 
 
 class OnelaError(RuntimeError):
@@ -97,6 +98,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "onela_fullstate_capacity_bytes": ([_I32] * 6, ctypes.c_uint64),
         "onela_select_workspace_bytes": ([_I32] * 4 + [ctypes.POINTER(ctypes.c_size_t)], _I32),
         "onela_select_beams": ([_I32] * 4 + [_P] * 6 + [ctypes.c_size_t, _P], _I32),
+        "onela_prefill_workspace_bytes": ([cfgp, _I32], ctypes.c_size_t),
+        "onela_prefill_state_chunked": ([cfgp, _I32] + [_P] * 6 + [ctypes.c_size_t, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -254,3 +257,17 @@ def onela_select_beams(num_requests: int, prev_width: int, vocab: int, width: in
         _dev(tokens_out, "tokens_out"), _dev(scores_out, "scores_out"),
         _dev(workspace, "workspace", optional=True), int(workspace_bytes), _stream(stream)),
         "onela_select_beams")
+
+
+def onela_prefill_workspace_bytes(cfg: onela_config_t, prompt_len: int) -> int:
+    return load_library().onela_prefill_workspace_bytes(ctypes.byref(cfg), prompt_len)
+
+
+def onela_prefill_state_chunked(cfg: onela_config_t, prompt_len: int, k, v, alpha, beta,
+                                s0_out, workspace=None, workspace_bytes: int = 0, stream=None):
+    opt = prompt_len == 0
+    _check(load_library().onela_prefill_state_chunked(
+        ctypes.byref(cfg), prompt_len, _dev(k, "k", opt), _dev(v, "v", opt),
+        _dev(alpha, "alpha", opt), _dev(beta, "beta", opt), _dev(s0_out, "s0_out"),
+        _dev(workspace, "workspace", optional=True), int(workspace_bytes), _stream(stream)),
+        "onela_prefill_state_chunked")

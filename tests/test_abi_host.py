@@ -204,3 +204,31 @@ def test_select_host_errors(lib):
     assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, None, big, None) == ab.ONELA_EINVAL
     assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, 128, big, None) == ab.ONELA_EINVAL
     assert sb(1, 512, 8192, 512, 256, None, 256, 256, 256, 256, 1024, None) == ab.ONELA_ECAPACITY
+
+
+@pytest.mark.parametrize("P,dk,dv", [(4096, 128, 128), (1, 128, 128), (65, 256, 512), (200, 32, 32)])
+def test_prefill_workspace_bytes(lib, P, dk, dv):
+    """Per (request, value head, 64-token chunk): fp32 W [64][d_k], Kt^T
+    [d_k][64], U^T [d_v][64], then one fp32 decay per chunk; two 256-byte
+    aligned regions."""
+    c = cfg(d_k=dk, d_v=dv, num_requests=2, num_v_heads=32)
+    nch = -(-P // 64)
+    up = lambda x: -(-x // 256) * 256
+    units = 2 * 32
+    assert ab.onela_prefill_workspace_bytes(c, P) == up(units * nch * 64 * (2 * dk + dv) * 4) + \
+        up(units * nch * 4)
+    assert ab.onela_prefill_workspace_bytes(c, 0) == 0
+    assert ab.onela_prefill_workspace_bytes(cfg(d_k=96, d_v=96), P) == 0
+    assert ab.onela_prefill_workspace_bytes(c, -1) == 0
+
+
+def test_prefill_chunked_host_errors(lib):
+    c = cfg()
+    f = lib.onela_prefill_state_chunked
+    big = 1 << 40
+    assert f(ctypes.byref(c), -1, 256, 256, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert f(ctypes.byref(c), 64, None, 256, 256, 256, 256, 256, big, None) == ab.ONELA_EINVAL
+    assert f(ctypes.byref(c), 64, 256, 256, 256, 256, 260, 256, big, None) == ab.ONELA_EINVAL
+    assert f(ctypes.byref(c), 64, 256, 256, 256, 256, 256, None, big, None) == ab.ONELA_EINVAL
+    assert f(ctypes.byref(c), 64, 256, 256, 256, 256, 256, 384, big, None) == ab.ONELA_EINVAL
+    assert f(ctypes.byref(c), 64, 256, 256, 256, 256, 256, 256, 16, None) == ab.ONELA_ECAPACITY
