@@ -230,6 +230,7 @@ def main():
                          "delta records (the others are timed as an A/B)")
     ap.add_argument("--skip-ab", action="store_true")
     ap.add_argument("--skip-select", action="store_true")
+    ap.add_argument("--skip-prefill", action="store_true")
     ap.add_argument("--select-vocab", type=int, default=None,
                     help="codebook size of the beam-selection measurement")
     args = ap.parse_args()
@@ -484,6 +485,38 @@ def main():
             "speedup_fused_kernels": fs_ms / (dec_us.sum() / 1e3)}
         log(f"[bench] fullstate baseline {fs_ms:.3f} ms/step")
         del base
+
+    # ---- S_ctx prefill of the workload's prompt (supplementary: setup work
+    # before the decode loop): the sequential kernel and the chunked one
+    if not args.skip_prefill and dw0.prompt is not None:
+        cfg_p = runner.config_for(spec)
+        pf_bytes = ab.onela_prefill_workspace_bytes(cfg_p, spec.P)
+        pf_ws = torch.empty(max(pf_bytes, 1), dtype=torch.uint8, device=dev)
+        s_tmp = torch.empty_like(s0)
+
+        def time_ms(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a0.record()
+            for _ in range(reps):
+                fn()
+            a1.record()
+            torch.cuda.synchronize()
+            return a0.elapsed_time(a1) / reps
+
+        seq_ms = time_ms(lambda: ab.onela_prefill_state(cfg_p, spec.P, *dw0.prompt, s_tmp), 3)
+        chk_ms = time_ms(lambda: ab.onela_prefill_state_chunked(cfg_p, spec.P, *dw0.prompt, s_tmp,
+                                                                pf_ws, pf_bytes), 10)
+        result["prefill"] = {
+            "prompt_tokens": spec.P, "requests": spec.R,
+            "sequential_ms": seq_ms, "chunked_ms": chk_ms,
+            "chunked_tokens_per_s": spec.R * spec.P / (chk_ms / 1e3),
+            "chunked_workspace_bytes": pf_bytes,
+            "note": "onela_prefill_state (token by token) vs onela_prefill_state_chunked "
+                    "(64-token chunks); setup work, not part of `value`"}
+        log(f"[bench] prefill {spec.P} tokens: sequential {seq_ms:.2f} ms, chunked {chk_ms:.3f} ms")
+        del pf_ws, s_tmp
 
     # ---- global top-W beam selection (supplementary: not part of `value`):
     # the next step's parents from W_prev x V candidate scores per request

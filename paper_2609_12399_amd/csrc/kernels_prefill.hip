@@ -54,12 +54,54 @@ struct PrefillParams {
   int HK, HV, P, nch;
 };
 
+// 8 consecutive io elements (16 B of bf16 or 32 B of fp32) at element i.
 template <bool BF16>
-__device__ inline float load_io(const void* base, long i) {
-  if constexpr (BF16)
-    return __uint_as_float(unsigned(static_cast<const uint16_t*>(base)[i]) << 16);
-  else
-    return static_cast<const float*>(base)[i];
+struct Io8 {
+  uint4 u[BF16 ? 1 : 2];
+  __device__ void load(const void* base, long i) {
+    if constexpr (BF16) {
+      u[0] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + i);
+    } else {
+      const uint4* q = reinterpret_cast<const uint4*>(static_cast<const float*>(base) + i);
+      u[0] = q[0];
+      u[1] = q[1];
+    }
+  }
+  __device__ float get(int e) const {
+    if constexpr (BF16) {
+      const unsigned w = (&u[0].x)[e >> 1];
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float((&u[e >> 2].x)[e & 3]);
+    }
+  }
+};
+
+// Fills dst[t][c] (t < kC, c < NCOL, row stride LD) from rows of an io
+// array (row t at element row0(t) + c0, zero for t >= n), scaled by
+// scale(t).  Every thread issues all of its loads before its first store.
+template <int NCOL, int LD, bool BF16, typename RowFn, typename ScaleFn>
+__device__ inline void fill_rows(float* dst, const void* src, int n, int c0, RowFn&& row0,
+                                 ScaleFn&& scale) {
+  constexpr int NV = kC * NCOL / 8;  // 8-element vectors
+  constexpr int PER = (NV + kP1Threads - 1) / kP1Threads;
+  Io8<BF16> buf[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int vi = threadIdx.x + q * kP1Threads;
+    const int t = vi / (NCOL / 8), c = (vi - t * (NCOL / 8)) * 8;
+    if (vi < NV && t < n) buf[q].load(src, row0(t) + c0 + c);
+  }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int vi = threadIdx.x + q * kP1Threads;
+    const int t = vi / (NCOL / 8), c = (vi - t * (NCOL / 8)) * 8;
+    if (vi < NV) {
+      const float sc = t < n ? scale(t) : 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dst[t * LD + c + e] = t < n ? sc * buf[q].get(e) : 0.f;
+    }
+  }
 }
 
 // ---- phase 1 ----------------------------------------------------------------
@@ -110,10 +152,9 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   const int n = min(kC, p.P - t0);
   const long tok0 = long(r) * p.P + t0;
 
-  for (int i = tid; i < kC * DK; i += kP1Threads) {
-    const int t = i / DK, kk = i - t * DK;
-    sh.K[t][kk] = t < n ? load_io<BF16>(p.k, ((tok0 + t) * p.HK + hk) * DK + kk) : 0.f;
-  }
+  fill_rows<DK, DK + 1, BF16>(&sh.K[0][0], p.k, n, 0,
+                               [&](int t) { return ((tok0 + t) * p.HK + hk) * DK; },
+                               [](int) { return 1.f; });
   if (tid < kC) {
     const bool in = tid < n;
     sh.al[tid] = in ? p.alpha[(tok0 + tid) * p.HV + hv] : 1.f;
@@ -133,8 +174,20 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
       s *= sh.al[t];
     }
   }
+  __syncthreads();
+  // Gamma(t, i) = alpha_{i+1} ... alpha_t for i < t, column i by thread i
+  // (held in T until T is formed)
+  if (tid < kC) {
+    const int i = tid;
+    float gm = 1.f;
+    for (int t = i + 1; t < kC; ++t) {
+      gm *= sh.al[t];
+      sh.T[t][i] = gm;
+    }
+  }
+  __syncthreads();
   // M(t, i) = beta_t Gamma(t, i) (k_t . k_i) for i < t: a 4 x 4 block of
-  // (t, i) per thread, Gamma by direct products.
+  // (t, i) per thread.
   {
     const int ib = tid & 15, tb = tid >> 4;
     float acc[4][4] = {};
@@ -155,13 +208,7 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int t = 4 * tb + a, i = 4 * ib + b;
-        float m = 0.f;
-        if (i < t) {
-          float gm = 1.f;
-          for (int j = i + 1; j <= t; ++j) gm *= sh.al[j];
-          m = sh.be[t] * gm * acc[a][b];
-        }
-        sh.M[t][i] = m;
+        sh.M[t][i] = i < t ? sh.be[t] * sh.T[t][i] * acc[a][b] : 0.f;
       }
   }
   __syncthreads();
@@ -203,13 +250,12 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   }
   // U = T diag(beta) V -> utb [DV][C]
   float* udst = p.utb + cu * DV * kC;
-  for (int cb = 0; cb < DV; cb += 128) {
-    const int nc = DV - cb < 128 ? DV - cb : 128;
-    for (int i = tid; i < kC * nc; i += kP1Threads) {
-      const int t = i / nc, jj = i - t * nc;
-      sh.X[t][jj] = t < n ? sh.be[t] * load_io<BF16>(p.v, ((tok0 + t) * p.HV + hv) * DV + cb + jj)
-                          : 0.f;
-    }
+  constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
+  for (int cb = 0; cb < DV; cb += VC) {
+    const int nc = VC;
+    fill_rows<VC, 129, BF16>(&sh.X[0][0], p.v, n, cb,
+                             [&](int t) { return ((tok0 + t) * p.HV + hv) * DV; },
+                             [&](int t) { return sh.be[t]; });
     __syncthreads();
     tri_times_block(sh, nc, [&](int t, int jj, float x) { udst[(cb + jj) * kC + t] = x; });
     __syncthreads();
@@ -219,58 +265,93 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
 
 // ---- phase 2 ----------------------------------------------------------------
 
+// Operands of one chunk for one lane (see prefill_scan_kernel).
+struct ScanOps {
+  f32x4 w[4], k[4], u[4];
+  float g;
+};
+
 template <int DK, int DV>
 __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   constexpr int NW = DK / 16;  // waves: state columns 16 w .. 16 w + 15
   __shared__ f32x4 xp[NW][4][64];  // partial X^T tiles of every wave
+  __shared__ f32x4 xs[4][64];      // their sums
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rb = blockIdx.x % (DV / 16), unit = blockIdx.x / (DV / 16);
   const int row0 = 16 * rb;
   const int lr = lane & 15, lq = lane >> 4;
   // st[i] = S^T(k = 16 w + 4 lq + i, n = lr) = S(row0 + lr, 16 w + 4 lq + i)
   f32x4 st = {0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < p.nch; ++c) {
-    const long cu = long(unit) * p.nch + c;
+  // Loads are unconditional (past the end they re-read the last chunk) so
+  // the compiler can count them and wait only for the set about to be used.
+  auto load = [&](int c, ScanOps& o) {
+    const long cu = long(unit) * p.nch + (c < p.nch ? c : p.nch - 1);
     const float* wc = p.wb + cu * kC * DK;
     const float* kt = p.ktb + cu * DK * kC;
     const float* ut = p.utb + cu * DV * kC;
-    const float g = p.gb[cu];
-    f32x4 wa[4], ka[4], ua[4];
+    o.g = p.gb[cu];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       // A of X: W(t = 16 mt + lr, k = 16 w + 4 lq + i), i = 0..3
-      wa[mt] = *reinterpret_cast<const f32x4*>(wc + (16 * mt + lr) * DK + 16 * w + 4 * lq);
+      o.w[mt] = *reinterpret_cast<const f32x4*>(wc + (16 * mt + lr) * DK + 16 * w + 4 * lq);
       // A of the update: Kt^T(k = 16 w + lr, t = 16 mt + 4 lq + j), j = 0..3
-      ka[mt] = *reinterpret_cast<const f32x4*>(kt + (16 * w + lr) * kC + 16 * mt + 4 * lq);
+      o.k[mt] = *reinterpret_cast<const f32x4*>(kt + (16 * w + lr) * kC + 16 * mt + 4 * lq);
       // U^T(row0 + lr, t = 16 mt + 4 lq + j)
-      ua[mt] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
+      o.u[mt] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
     }
+  };
+  auto step = [&](int c, const ScanOps& o) {
+    if (c >= p.nch) return;
     // partial X^T(t, n) over this wave's 16 state columns
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[mt][i], st[i], acc, 0, 0, 0);
+      for (int i = 0; i < 4; ++i)
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(o.w[mt][i], st[i], acc, 0, 0, 0);
       xp[w][mt][lane] = acc;
     }
     __syncthreads();
-    // D^T(t = 16 mt + 4 lq + j, n = lr) = U^T - sum over waves of X^T
-    f32x4 dt[4];
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = w; mt < 4; mt += NW) {  // wave w sums tiles w, w + NW, .. over the waves
       f32x4 x = xp[0][mt][lane];
 #pragma unroll
       for (int v = 1; v < NW; ++v) x += xp[v][mt][lane];
-      dt[mt] = ua[mt] - x;
+      xs[mt][lane] = x;
     }
     __syncthreads();
+    // D^T(t = 16 mt + 4 lq + j, n = lr) = U^T - X^T
+    f32x4 dt[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) dt[mt] = o.u[mt] - xs[mt][lane];
     // S^T <- g S^T + Kt^T D^T
-    st *= g;
+    st *= o.g;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        st = __builtin_amdgcn_mfma_f32_16x16x4f32(ka[mt][j], dt[mt][j], st, 0, 0, 0);
+        st = __builtin_amdgcn_mfma_f32_16x16x4f32(o.k[mt][j], dt[mt][j], st, 0, 0, 0);
+  };
+  // Three operand sets in flight: chunk c + 2 is requested before chunk c is
+  // processed.  (xp and xs are rewritten only after the next chunk's first
+  // barrier, which every wave reaches after reading them.)
+  // The scheduling barriers keep every load group in program order, so the
+  // wait before a step covers only its own (oldest) group.
+  ScanOps a, b, c3;
+  load(0, a);
+  load(1, b);
+  for (int c = 0; c < p.nch; c += 3) {
+    __builtin_amdgcn_sched_barrier(0);
+    load(c + 2, c3);
+    __builtin_amdgcn_sched_barrier(0);
+    step(c, a);
+    __builtin_amdgcn_sched_barrier(0);
+    load(c + 3, a);
+    __builtin_amdgcn_sched_barrier(0);
+    step(c + 1, b);
+    __builtin_amdgcn_sched_barrier(0);
+    load(c + 4, b);
+    __builtin_amdgcn_sched_barrier(0);
+    step(c + 2, c3);
   }
   float* dst = p.s_out + (long(unit) * DV + row0 + lr) * DK + 16 * w + 4 * lq;
   *reinterpret_cast<f32x4*>(dst) = st;
