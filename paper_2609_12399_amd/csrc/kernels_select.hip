@@ -451,127 +451,88 @@ __device__ inline unsigned load_slots(const SelectParams& p, SelShared& sh, unsi
 
 // ---- sort ------------------------------------------------------------------
 
-// x of lane (lane ^ M) without LDS: DPP quad permutes for 1 and 2, row
-// shifts for 4, a row rotate for 8 and the gfx950 permlane swaps for 16 and
-// 32 (lane layouts checked on the device).
-template <int M>
-__device__ inline unsigned xor_lane(unsigned x) {
-  const unsigned lane = lane_id();
-  if constexpr (M == 1) return dppu<0xB1>(x);  // quad_perm [1,0,3,2]
-  if constexpr (M == 2) return dppu<0x4E>(x);  // quad_perm [2,3,0,1]
-  if constexpr (M == 4) {
-    const unsigned up = dppu<0x104>(x), down = dppu<0x114>(x);  // row_shl:4, row_shr:4
-    return (lane & 4u) ? down : up;
-  }
-  if constexpr (M == 8) return dppu<0x128>(x);  // row_ror:8
-  if constexpr (M == 16) {
-    const auto s = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-    return (lane & 16u) ? s[0] : s[1];
-  }
-  if constexpr (M == 32) {
-    const auto s = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-    return (lane & 32u) ? s[0] : s[1];
-  }
-}
+// Stable LSD radix sort of the m (<= kSortCap) composites in a, descending
+// by their high 32 bits (the score key), in 8-bit passes over key - lo (lo:
+// the smallest key), as many as key - lo needs; the sorted values end in
+// the returned buffer (a or b).  The composites arrive in index order and
+// every pass is stable, so equal keys stay in index order: the result is the
+// (score desc, index asc) order.  Element p of a pass is handled by round p / kThreads, lane p % 64
+// of wave (p / 64) % 8; its rank among the equal digits before it is the
+// count of lower lanes of its wave with that digit (the digit's lane mask
+// from 8 ballots) plus the counts of the earlier (round, wave) pairs.
+struct RadixShared {
+  unsigned cnt[kSortCap / kThreads][kWaves][256];
+  unsigned tot[256];
+};
 
-template <int M>
-__device__ inline unsigned long long xor_lane64(unsigned long long x) {
-  const unsigned lo = xor_lane<M>(unsigned(x)), hi = xor_lane<M>(unsigned(x >> 32));
-  return (static_cast<unsigned long long>(hi) << 32) | lo;
-}
-
-// One compare-exchange stage (block size K, stride J) of a descending bitonic
-// sort of 64 E values held by one wave, lane l holding positions l E .. l E +
-// E - 1.
-template <int E, int K, int J>
-__device__ inline void bitonic_stage(unsigned long long (&v)[E]) {
-  const unsigned lane = lane_id();
-  if constexpr (J < E) {
+__device__ inline unsigned long long* radix_sort_desc(unsigned long long* a, unsigned long long* b,
+                                                      unsigned m, unsigned lo, unsigned hi,
+                                                      RadixShared& rs) {
+  constexpr int RMAX = kSortCap / kThreads;
+  const unsigned lane = lane_id(), w = threadIdx.x >> 6;
+  const unsigned rounds = (m + kThreads - 1) / kThreads;
+  const int passes = (bit_width(hi - lo) + 7) / 8;
+  unsigned* cflat = &rs.cnt[0][0][0];
+  unsigned long long* src = a;
+  unsigned long long* dst = b;
+  for (int pass = 0; pass < passes; ++pass) {
+    const int shift = 8 * pass;
+    for (unsigned i = threadIdx.x; i < rounds * kWaves * 256; i += kThreads) cflat[i] = 0u;
+    __syncthreads();
+    unsigned long long v[RMAX];
+    unsigned dg[RMAX], rk[RMAX];
 #pragma unroll
-    for (int q = 0; q < E; ++q) {
-      if ((q & J) == 0) {
-        const unsigned g = lane * E + unsigned(q);
-        const bool desc = (g & unsigned(K)) == 0;
-        const unsigned long long a = v[q], b = v[q + J];
-        const bool swap = desc ? a < b : a > b;
-        v[q] = swap ? b : a;
-        v[q + J] = swap ? a : b;
+    for (int j = 0; j < RMAX; ++j) {
+      if (unsigned(j) < rounds) {
+        const unsigned pos = unsigned(j) * kThreads + threadIdx.x;
+        const bool valid = pos < m;
+        v[j] = valid ? src[pos] : 0ull;
+        const unsigned d = 255u - (((unsigned(v[j] >> 32) - lo) >> shift) & 255u);
+        unsigned long long same = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+          const unsigned long long mb = __ballot((d >> bit) & 1u);
+          same &= ((d >> bit) & 1u) ? mb : ~mb;
+        }
+        rk[j] = mbcnt(same);
+        dg[j] = d;
+        if (valid && rk[j] == 0u) rs.cnt[j][w][d] = unsigned(__popcll(same));
       }
     }
-  } else {
-#pragma unroll
-    for (int q = 0; q < E; ++q) {
-      const unsigned long long pv = xor_lane64<J / E>(v[q]);
-      const unsigned g = lane * E + unsigned(q);
-      const bool keep_max = ((g & unsigned(J)) == 0) == ((g & unsigned(K)) == 0);
-      v[q] = keep_max ? (v[q] > pv ? v[q] : pv) : (v[q] < pv ? v[q] : pv);
+    __syncthreads();
+    if (threadIdx.x < 256) {  // per digit: exclusive prefix over (round, wave)
+      const unsigned d = threadIdx.x;
+      unsigned run = 0u;
+      for (unsigned j = 0; j < rounds; ++j)
+        for (int w2 = 0; w2 < kWaves; ++w2) {
+          const unsigned c = rs.cnt[j][w2][d];
+          rs.cnt[j][w2][d] = run;
+          run += c;
+        }
+      rs.tot[d] = run;
     }
-  }
-}
-
-template <int E, int K, int J>
-__device__ inline void bitonic_merge(unsigned long long (&v)[E]) {
-  if constexpr (J >= 1) {
-    bitonic_stage<E, K, J>(v);
-    bitonic_merge<E, K, J / 2>(v);
-  }
-}
-
-template <int E, int K>
-__device__ inline void bitonic_levels(unsigned long long (&v)[E]) {
-  if constexpr (K <= 64 * E) {
-    bitonic_merge<E, K, K / 2>(v);
-    bitonic_levels<E, K * 2>(v);
-  }
-}
-
-// Number of values of a descending run that exceed x.
-template <int N>
-__device__ inline unsigned count_above(const unsigned long long* run, unsigned long long x) {
-  unsigned lo = 0, hi = N;
-#pragma unroll
-  for (int it = 0; (1 << it) <= N; ++it) {
-    if (lo < hi) {
-      const unsigned mid = (lo + hi) >> 1;
-      if (run[mid] > x) lo = mid + 1;
-      else hi = mid;
+    __syncthreads();
+    if (w == 0) {  // exclusive prefix of the digit totals
+      const uint4 t4 = reinterpret_cast<const uint4*>(rs.tot)[lane];
+      const unsigned sum = t4.x + t4.y + t4.z + t4.w;
+      const unsigned ex = wave_scan(sum) - sum;
+      reinterpret_cast<uint4*>(rs.tot)[lane] =
+          make_uint4(ex, ex + t4.x, ex + t4.x + t4.y, ex + t4.x + t4.y + t4.z);
     }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < RMAX; ++j) {
+      if (unsigned(j) < rounds) {
+        const unsigned pos = unsigned(j) * kThreads + threadIdx.x;
+        if (pos < m) dst[rs.tot[dg[j]] + rs.cnt[j][w][dg[j]] + rk[j]] = v[j];
+      }
+    }
+    __syncthreads();
+    unsigned long long* tmp = src;
+    src = dst;
+    dst = tmp;
   }
-  return lo;
-}
-
-// Sorted top W of the m (<= kSortCap) composites in buf, handed out as
-// fn(rank, value) for rank < W.  The m values are cut into 8 runs of ceil(m
-// / 8), one per wave; each wave sorts its run in registers (padding 0 sorts
-// last), the runs go back to buf, and every value's rank is its place in its
-// own run plus the number of values above it in each other run (binary
-// searches).  Values are distinct, so ranks are exact.
-template <int E, typename F>
-__device__ inline void rank_sorted_runs(unsigned long long* buf, unsigned m, unsigned W, F&& fn) {
-  const unsigned lane = lane_id(), w = threadIdx.x >> 6;
-  const unsigned len = (m + kWaves - 1) / kWaves;
-  unsigned long long v[E];
-#pragma unroll
-  for (int q = 0; q < E; ++q) {
-    const unsigned i = lane * E + unsigned(q);
-    const unsigned g = w * len + i;
-    v[q] = (i < len && g < m) ? buf[g] : 0ull;
-  }
-  bitonic_levels<E, 2>(v);
-  __syncthreads();
-  constexpr unsigned N = 64u * E;
-#pragma unroll
-  for (int q = 0; q < E; ++q) buf[w * N + lane * E + unsigned(q)] = v[q];
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < E; ++q) {
-    if (v[q] == 0ull) continue;  // padding
-    unsigned rank = lane * E + unsigned(q);
-#pragma unroll
-    for (int w2 = 0; w2 < kWaves; ++w2)
-      if (unsigned(w2) != w) rank += count_above<N>(buf + w2 * N, v[q]);
-    if (rank < W) fn(rank, v[q]);
-  }
+  return src;
 }
 
 // ---- kernels ---------------------------------------------------------------
@@ -628,6 +589,8 @@ template <bool RAW, bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) {
   __shared__ SelShared sh;
   __shared__ unsigned long long srt[kSortCap];
+  __shared__ unsigned long long srt2[kSortCap];
+  __shared__ RadixShared rsh;
   const unsigned r = blockIdx.x;
   unsigned key[kNI], idx[kNI], vm, n;
   if constexpr (RAW) {
@@ -652,8 +615,15 @@ __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) 
     keep = cut_mask(sh, key, vm, c);
     o = ordered_plan(keep, sh);
   }
-  // Composite sort key: score key high, complemented index low, so that the
-  // descending order is (score desc, index asc).  Padding (0) sorts last.
+  // Composite: score key high, complemented index low (the index is
+  // recovered from it; the sort orders by the key and keeps index order).
+  unsigned klo = ~0u, khi = 0u;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i)
+    if ((keep >> i) & 1u) {
+      klo = min(klo, key[i]);
+      khi = max(khi, key[i]);
+    }
   ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
     srt[rank] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~idx[i]);
   });
@@ -671,11 +641,9 @@ __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) 
       else p.scores[o2] = logp_r[fi];
     }
   };
-  const unsigned len = (m + kWaves - 1) / kWaves;  // run length per wave
-  if (len <= 64u) rank_sorted_runs<1>(srt, m, p.W, emit);
-  else if (len <= 128u) rank_sorted_runs<2>(srt, m, p.W, emit);
-  else if (len <= 256u) rank_sorted_runs<4>(srt, m, p.W, emit);
-  else rank_sorted_runs<8>(srt, m, p.W, emit);
+  const Red3 kr = block_reduce(sh, 0u, klo, khi);
+  const unsigned long long* sorted = radix_sort_desc(srt, srt2, m, kr.lo, kr.hi, rsh);
+  for (unsigned j = threadIdx.x; j < p.W; j += kThreads) emit(j, sorted[j]);
 }
 
 unsigned pow2_ceil(unsigned x) {
