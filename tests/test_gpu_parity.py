@@ -419,3 +419,19 @@ def test_borrowed_records_bad_parent_contained(fused):
     assert rel_err(o[1][0][keep1], ref[1][0][keep1]) <= REL_TOL
     assert rel_err(o[2][0][keep2], ref[2][0][keep2]) <= REL_TOL
     dec.close()
+
+
+@pytest.mark.parametrize("storage", ["copy", "borrow"])
+def test_fused_wide_beams(storage):
+    """2100 beams (66 beam tiles, a ragged last one) over four fused steps,
+    with ancestry tables of 2100 x 3 entries."""
+    spec = W.WorkloadSpec("wide_beam", 1, 2, 2, 32, 32, 16, (8, 2100, 2100, 2100), "f32",
+                          "uniform", seed=17)
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    anc = oracle_ancestry(wl)
+    o, g = run_gpu(wl, s0, fused=True, storage=storage)
+    for t in range(spec.T):
+        assert np.array_equal(g[t], anc[t])
+        assert rel_err(o[t], ref[t]) <= REL_TOL
