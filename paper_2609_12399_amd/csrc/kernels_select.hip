@@ -20,10 +20,9 @@
 //     fit the slot, the exact cut is taken instead (radix select over the
 //     workgroup).
 //   * final kernel: one workgroup per request filters the last <= 16384
-//     candidates the same way, sorts the survivors on the composite (key,
-//     complemented index) -- eight runs sorted in registers, one per wave,
-//     then each value ranked by binary searches in the other runs -- and
-//     writes the first W.
+//     candidates the same way, sorts the survivors (a stable LSD radix sort
+//     on the score key; they arrive in index order, so ties stay in index
+//     order) and writes the first W.
 // The stage input of stage s >= 1 is the slot array of stage s - 1; a
 // workgroup reads 16384 / cap consecutive slots.  Slots hold increasing index
 // ranges, so position order inside a workgroup is index order, which is what
