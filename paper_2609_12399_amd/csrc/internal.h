@@ -97,8 +97,9 @@ constexpr int kSelectChunk = 16384;            // candidates per workgroup
 constexpr int kSelectMaxWidth = 4096;          // W kept per request
 constexpr int kSelectMaxStages = 16;           // reduction stages before the final one
 constexpr unsigned kSelectMaxCandidates = 1u << 29;  // W_prev * V per request
+constexpr int kSelectMaxGatherSlots = 2048;          // chunks per request, two-pass path
 
-// Launch plan.  Stage 0 reads the raw scores in nwg[0] chunks of
+// Launch plan (tree path).  Stage 0 reads the raw scores in nwg[0] chunks of
 // kSelectChunk per request; stage s >= 1 reads the nin[s] output slots of
 // stage s - 1, `group` slots per workgroup.  Every stage workgroup writes one
 // slot of `cap` (key, index) pairs plus a count into buffer s % 2 of the
@@ -110,6 +111,11 @@ struct SelectPlan {
   unsigned final_in;
   unsigned cap, group;
   size_t pair_off[2], count_off[2], total;
+  // Two-pass path (see kernels_select.hip): per request nseg wave maxima,
+  // then nchunks slots of `cap` pairs and their counts.
+  bool two_pass;
+  unsigned nchunks, nseg;
+  size_t seg_off, slot_off, cnt_off;
 };
 bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan);
 hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int vocab, int width,

@@ -45,9 +45,9 @@ struct SelectParams {
   const float* logp;        // [R][N] log-probabilities, N = W_prev * V
   const float* beam;        // [R][W_prev] beam scores, or null
   const uint2* cand_in;     // [R][nslots_in][cap] (key, flat index); null: read logp
-  const unsigned* cnt_in;   // [R][nslots_in]
+  const unsigned* cnt_in;   // [R][nslots_in] counts (two-pass: (count, largest key) pairs)
   uint2* cand_out;          // [R][nwg][cap]        (stage kernel)
-  unsigned* cnt_out;        // [R][nwg]
+  unsigned* cnt_out;        // [R][nwg] counts (two-pass: (count, largest key) pairs)
   int* parents;             // [R][W]               (final kernel)
   int* tokens;
   float* scores;
@@ -55,6 +55,8 @@ struct SelectParams {
   unsigned cap, lcap;       // slot capacity (a power of two) and its log2
   unsigned group;           // input slots per workgroup (16384 / cap)
   unsigned nslots_in;       // input slots per request (slot input)
+  unsigned* segmax;         // [R][nseg] largest key of each wave's candidates (two-pass)
+  unsigned nseg;
   unsigned nwg;             // workgroups per request
   double inv_v;             // 1 / V
 };
@@ -260,8 +262,9 @@ __device__ inline void find_bin(SelShared& sh, unsigned need) {
 // lo), so scores that straddle a power of two still spread out; the bound is
 // the floor of the bin where the count from the top reaches need.
 __device__ inline unsigned group_bound(SelShared& sh, const unsigned (&key)[kNI], unsigned vm,
-                                       unsigned need) {
-  const unsigned G = need <= 1024u ? 4u : (need <= 2048u ? 2u : 1u);
+                                       unsigned need, unsigned G = 0u) {
+  // G = 0: choose by need; G = 1 counts every key (e.g. keys that are maxima)
+  if (G == 0u) G = need <= 1024u ? 4u : (need <= 2048u ? 2u : 1u);
   unsigned gvm = 0u, gm[kNI], lo = ~0u, hi = 0u;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
@@ -459,10 +462,16 @@ __device__ inline unsigned load_slots(const SelectParams& p, SelShared& sh, unsi
 // of wave (p / 64) % 8; its rank among the equal digits before it is the
 // count of lower lanes of its wave with that digit (the digit's lane mask
 // from 8 ballots) plus the counts of the earlier (round, wave) pairs.
-struct RadixShared {
-  unsigned cnt[kSortCap / kThreads][kWaves][256];
+struct alignas(16) RadixShared {
+  union {
+    unsigned cnt[kSortCap / kThreads][kWaves][256];
+    unsigned flat[kSelectChunk];  // free for other use between sorts
+    uint4 flat4[kSelectChunk / 4];
+  };
   unsigned tot[256];
 };
+static_assert(sizeof(unsigned[kSortCap / kThreads][kWaves][256]) == kSelectChunk * sizeof(unsigned),
+              "the sort counters span one chunk of words");
 
 __device__ inline unsigned long long* radix_sort_desc(unsigned long long* a, unsigned long long* b,
                                                       unsigned m, unsigned lo, unsigned hi,
@@ -583,24 +592,45 @@ __global__ __launch_bounds__(kThreads) void select_slot_stage_kernel(SelectParam
   reduce_group(p, sh, r, g, key, vm, t.sum, [&](int i) { return idx[i]; });
 }
 
-// Top W of request r's last candidates, sorted, into parents/tokens/scores.
-template <bool RAW, bool BEAM>
-__global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) {
-  __shared__ SelShared sh;
-  __shared__ unsigned long long srt[kSortCap];
-  __shared__ unsigned long long srt2[kSortCap];
-  __shared__ RadixShared rsh;
-  const unsigned r = blockIdx.x;
-  unsigned key[kNI], idx[kNI], vm, n;
-  if constexpr (RAW) {
-    n = p.N;
-    vm = load_raw<BEAM>(p, r, 0u, n, key);
-#pragma unroll
-    for (int i = 0; i < kNI; ++i) idx[i] = unsigned(i) * kThreads + threadIdx.x;
-  } else {
-    vm = load_slots(p, sh, r, 0u, key, idx);
-    n = block_reduce(sh, unsigned(__popc(vm)), 0u, 0u).sum;
-  }
+// Shared memory of the last stage of a selection.
+struct FinalShared {
+  SelShared sh;
+  unsigned long long srt[kSortCap];
+  unsigned long long srt2[kSortCap];
+  RadixShared rsh;
+};
+
+// Sorts the m (key, ~index) pairs in fs.srt (in index order, written before
+// the call by any thread) best first and writes the first W to
+// parents / tokens / scores of request r.  klo / khi: this thread's share of
+// the key range.
+template <bool BEAM>
+__device__ inline void sort_emit(const SelectParams& p, FinalShared& fs, unsigned r, unsigned m,
+                                 unsigned klo, unsigned khi) {
+  const float* logp_r = p.logp + size_t(r) * p.N;
+  auto emit = [&](unsigned j, unsigned long long c) {
+    const unsigned fi = ~unsigned(c);
+    const unsigned row = row_of(fi, p.V, p.inv_v);
+    const size_t o2 = size_t(r) * p.W + j;
+    p.parents[o2] = int(row);
+    p.tokens[o2] = int(fi - row * p.V);
+    if constexpr (BEAM) p.scores[o2] = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
+    else p.scores[o2] = logp_r[fi];
+  };
+  __syncthreads();  // srt is written; the caller's reads of fs.sh are done
+  const Red3 kr = block_reduce(fs.sh, 0u, klo, khi);
+  const unsigned long long* sorted = radix_sort_desc(fs.srt, fs.srt2, m, kr.lo, kr.hi, fs.rsh);
+  for (unsigned j = threadIdx.x; j < p.W; j += kThreads) emit(j, sorted[j]);
+}
+
+// Top W of the n candidates held in registers (slot i of a lane at position
+// i * kThreads + tid, position order = flat-index order), sorted, written to
+// parents / tokens / scores of request r.
+template <bool BEAM>
+__device__ inline void finish_select(const SelectParams& p, FinalShared& fs, unsigned r,
+                                     const unsigned (&key)[kNI], const unsigned (&idx)[kNI],
+                                     unsigned vm, unsigned n) {
+  SelShared& sh = fs.sh;
   unsigned keep = vm;
   if (n > unsigned(kSortCap)) {
     const unsigned b = group_bound(sh, key, vm, p.W);
@@ -624,25 +654,299 @@ __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) 
       khi = max(khi, key[i]);
     }
   ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
-    srt[rank] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~idx[i]);
+    fs.srt[rank] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~idx[i]);
   });
-  __syncthreads();
-  const unsigned m = o.total;
-  const float* logp_r = p.logp + size_t(r) * p.N;
-  auto emit = [&](unsigned j, unsigned long long c) {
-    if (j < p.W) {
-      const unsigned fi = ~unsigned(c);
-      const unsigned row = row_of(fi, p.V, p.inv_v);
-      const size_t o2 = size_t(r) * p.W + j;
-      p.parents[o2] = int(row);
-      p.tokens[o2] = int(fi - row * p.V);
-      if constexpr (BEAM) p.scores[o2] = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
-      else p.scores[o2] = logp_r[fi];
+  sort_emit<BEAM>(p, fs, r, o.total, klo, khi);
+}
+
+// Top W of request r's last candidates, sorted, into parents/tokens/scores.
+template <bool RAW, bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) {
+  __shared__ FinalShared fs;
+  const unsigned r = blockIdx.x;
+  unsigned key[kNI], idx[kNI], vm, n;
+  if constexpr (RAW) {
+    n = p.N;
+    vm = load_raw<BEAM>(p, r, 0u, n, key);
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) idx[i] = unsigned(i) * kThreads + threadIdx.x;
+  } else {
+    vm = load_slots(p, fs.sh, r, 0u, key, idx);
+    n = block_reduce(fs.sh, unsigned(__popc(vm)), 0u, 0u).sum;
+  }
+  finish_select<BEAM>(p, fs, r, key, idx, vm, n);
+}
+
+// ---- two-pass path ----------------------------------------------------------
+// For W_prev * V >= 2 W * 2048 (and at most 16384 * 2048) candidates:
+//   segmax: every wave of a raw chunk writes the largest key of its 2048
+//     candidates;
+//   filter: every workgroup takes as bound a key that at least W of the
+//     request's wave maxima reach (one histogram pass over them) -- W maxima
+//     are W distinct candidates, so no member of the top W is below it --
+//     re-reads its chunk and keeps the candidates at or above the bound, in
+//     index order, in its chunk's slot of `cap` (>= W) pairs, with the count
+//     and the chunk's largest key; a chunk with more survivors than the slot
+//     holds keeps their exact top W;
+//   gather: one workgroup per request walks the slots in chunk order (index
+//     order), 16384 candidates at a time, keeping the exact top W of what it
+//     has seen in LDS between rounds, and finishes like the final kernel.
+//     Every later candidate has a higher index than the kept ones, so once W
+//     are kept it can only enter with a key above their smallest: slots whose
+//     largest key is not above it are skipped whole, and so are such
+//     candidates.
+// For smooth score distributions about W candidates survive the bound.
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_segmax_kernel(SelectParams p) {
+  const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
+  const unsigned base = c * unsigned(kSelectChunk);
+  const unsigned n = min(p.N - base, unsigned(kSelectChunk));
+  unsigned key[kNI];
+  load_raw<BEAM>(p, r, base, n, key);
+  unsigned mx = 0u;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) mx = max(mx, key[i]);  // invalid slots hold 0
+  const Red3 w = wave_reduce(0u, 0u, mx);
+  if (lane_id() == 0) p.segmax[size_t(r) * p.nseg + c * kWaves + (threadIdx.x >> 6)] = w.hi;
+}
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p) {
+  __shared__ SelShared sh;
+  const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
+  const unsigned base = c * unsigned(kSelectChunk);
+  const unsigned n = min(p.N - base, unsigned(kSelectChunk));
+  unsigned key[kNI];
+  const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
+  // wave maxima of the request; segment (chunk s / 8, wave s % 8) exists when
+  // its first candidate does
+  unsigned mk[kNI], mvm = 0u;
+  const unsigned* seg = p.segmax + size_t(r) * p.nseg;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) {
+    const unsigned s = unsigned(i) * kThreads + threadIdx.x;
+    const bool valid = s < p.nseg && (s / kWaves) * unsigned(kSelectChunk) + (s % kWaves) * 64u < p.N;
+    mk[i] = seg[valid ? s : 0u];
+    mvm |= unsigned(valid) << i;
+  }
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) mk[i] = ((mvm >> i) & 1u) ? mk[i] : 0u;
+  // at least W maxima reach the bound (floor of the histogram bin where
+  // their count from the top reaches W)
+  const unsigned bound = group_bound(sh, mk, mvm, p.W, 1u);
+  unsigned keep = vm;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < bound) << i);
+  Ordered o = ordered_plan(keep, sh);
+  if (o.total > p.cap) {  // rare: keep the chunk's exact top W of the survivors
+    __syncthreads();
+    keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
+    o = ordered_plan(keep, sh);
+  }
+  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
+  ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
+    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + threadIdx.x);
+  });
+  if (threadIdx.x == 0) {  // (count, largest key of the chunk: its waves' maxima)
+    unsigned top = 0u;
+    for (int w = 0; w < kWaves; ++w) top = max(top, seg[c * kWaves + unsigned(w)]);
+    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(o.total, top);
+  }
+}
+
+// Inclusive running maximum over the 64 lanes.
+__device__ inline unsigned wave_scan_max(unsigned x) {
+  x = max(x, dppu<0x111>(x));       // row_shr:1
+  x = max(x, dppu<0x112>(x));       // row_shr:2
+  x = max(x, dppu<0x114>(x));       // row_shr:4
+  x = max(x, dppu<0x118>(x));       // row_shr:8
+  x = max(x, dppu<0x142, 0xA>(x));  // row_bcast:15 into rows 1, 3
+  x = max(x, dppu<0x143, 0xC>(x));  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_gather_kernel(SelectParams p) {
+  __shared__ FinalShared fs;
+  __shared__ unsigned next[2];  // (slot, offset) where the next round starts
+  // Round position q -> 1 + (index of its pair in the request's slots) - q,
+  // in fs.rsh.flat (the radix sort's counters are idle until the last
+  // round).  Within a live slot that difference is constant, and it does not
+  // decrease from slot to slot (a slot holds at most cap pairs), so writing
+  // it at each slot's first position and taking a running maximum fills the
+  // map.
+  const unsigned r = blockIdx.x, ns = p.nslots_in;
+  const unsigned lane = lane_id(), w = threadIdx.x >> 6;
+  const uint2* slots = p.cand_in + size_t(r) * ns * p.cap;
+  unsigned c4[4], m4[4];  // count and largest key of slots 4t .. 4t + 3 (ns <= 4 * kThreads)
+  {
+    const uint2* cm = reinterpret_cast<const uint2*>(p.cnt_in) + size_t(r) * ns;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const unsigned sl = 4u * threadIdx.x + unsigned(q);
+      const uint2 e = cm[sl < ns ? sl : 0u];
+      c4[q] = sl < ns ? e.x : 0u;
+      m4[q] = e.y;
     }
-  };
-  const Red3 kr = block_reduce(sh, 0u, klo, khi);
-  const unsigned long long* sorted = radix_sort_desc(srt, srt2, m, kr.lo, kr.hi, rsh);
-  for (unsigned j = threadIdx.x; j < p.W; j += kThreads) emit(j, sorted[j]);
+  }
+  unsigned cur = 0u, off = 0u, carried = 0u, floor_key = 0u;
+  for (;;) {
+    // The thread id is re-read every round so that the compiler rebuilds the
+    // per-slot positions here instead of keeping 32 of them live across rounds.
+    unsigned t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    // live counts: slots before cur are consumed, cur up to off; with W kept,
+    // a slot whose largest key does not beat the smallest kept one is dead
+    unsigned v[4], sum = 0u;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const unsigned sl = 4u * t + unsigned(q);
+      unsigned c = sl < cur ? 0u : c4[q] - (sl == cur ? off : 0u);
+      if (carried > 0u && m4[q] <= floor_key) c = 0u;
+      v[q] = c;
+      sum += c;
+    }
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) fs.rsh.flat[unsigned(i) * kThreads + t] = 0u;
+    const unsigned inc = wave_scan(sum);
+    if (lane == 63) fs.sh.red[0][w] = inc;
+    __syncthreads();
+    unsigned run = inc - sum, total = 0u;
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2) {
+      const unsigned x = fs.sh.red[0][w2];
+      total += x;
+      run += unsigned(w2) < w ? x : 0u;
+    }
+    const unsigned room = unsigned(kSelectChunk) - carried;
+    const unsigned fresh = total < room ? total : room;
+    const bool last = fresh == total;
+    unsigned st[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const unsigned sl = 4u * t + unsigned(q);
+      st[q] = run;
+      // live slots start at distinct positions; sl * cap + skipped >= run
+      if (v[q] > 0u && run < fresh)
+        fs.rsh.flat[run] = 1u + (sl << p.lcap) + (sl == cur ? off : 0u) - run;
+      run += v[q];
+    }
+    __syncthreads();
+    {  // running maximum over the map: thread t holds entries 32t .. 32t + 31
+      uint4 a[8];
+      unsigned mx = 0u;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        a[k] = fs.rsh.flat4[8u * t + unsigned(k)];
+        mx = max(mx, max(max(a[k].x, a[k].y), max(a[k].z, a[k].w)));
+      }
+      const unsigned wi = wave_scan_max(mx);
+      if (lane == 63) fs.sh.red[1][w] = wi;
+      // exclusive across lanes: lane - 1's inclusive value
+      unsigned pre = unsigned(__shfl_up(int(wi), 1));
+      if (lane == 0) pre = 0u;
+      __syncthreads();
+#pragma unroll
+      for (int w2 = 0; w2 < kWaves; ++w2) pre = unsigned(w2) < w ? max(pre, fs.sh.red[1][w2]) : pre;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        a[k].x = pre = max(pre, a[k].x);
+        a[k].y = pre = max(pre, a[k].y);
+        a[k].z = pre = max(pre, a[k].z);
+        a[k].w = pre = max(pre, a[k].w);
+        fs.rsh.flat4[8u * t + unsigned(k)] = a[k];
+      }
+    }
+    __syncthreads();
+    if (carried == 0u && total <= unsigned(kSortCap)) {
+      // every survivor fits the sort: straight from the slots into it
+      unsigned long long pr[kSortCap / kThreads];
+      unsigned klo = ~0u, khi = 0u;
+#pragma unroll
+      for (int i = 0; i < kSortCap / kThreads; ++i) {
+        const unsigned q = unsigned(i) * kThreads + t;
+        const bool ok = q < total;
+        const unsigned d = fs.rsh.flat[ok ? q : 0u];
+        const unsigned at = ok ? q + d - 1u : 0u;
+        const uint2 e = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(slots) +
+                                                        at * unsigned(sizeof(uint2)));
+        pr[i] = (static_cast<unsigned long long>(e.x) << 32) | unsigned(~e.y);
+        klo = ok ? min(klo, e.x) : klo;
+        khi = ok ? max(khi, e.x) : khi;
+      }
+      __syncthreads();  // the map has been read (it shares storage with the sort)
+#pragma unroll
+      for (int i = 0; i < kSortCap / kThreads; ++i) {
+        const unsigned q = unsigned(i) * kThreads + t;
+        if (q < total) fs.srt[q] = pr[i];
+      }
+      sort_emit<BEAM>(p, fs, r, total, klo, khi);
+      return;
+    }
+    // candidates: the carry (positions < carried, from LDS) then `fresh` from
+    // the slots; every load is issued unconditionally from a clamped address
+    unsigned key[kNI], idx[kNI], fm = 0u;
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) {
+      const unsigned j = unsigned(i) * kThreads + t;
+      const unsigned q = j - carried;
+      const bool in_fresh = j >= carried && q < fresh;
+      const unsigned d = fs.rsh.flat[in_fresh ? q : 0u];
+      const unsigned at = in_fresh ? q + d - 1u : 0u;  // pair index, < 2048 * 4096
+      const uint2 e = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(slots) +
+                                                      at * unsigned(sizeof(uint2)));
+      key[i] = e.x;
+      idx[i] = e.y;
+      fm |= unsigned(in_fresh) << i;
+    }
+    unsigned vm = 0u;
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) {
+      const bool ok = ((fm >> i) & 1u) && !(carried > 0u && key[i] <= floor_key);
+      vm |= unsigned(ok) << i;
+      key[i] = ok ? key[i] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kSortCap / kThreads; ++i) {  // the carry: positions < carried <= W
+      const unsigned j = unsigned(i) * kThreads + t;
+      if (j < carried) {
+        const unsigned long long cv = fs.srt2[j];
+        key[i] = unsigned(cv >> 32);
+        idx[i] = ~unsigned(cv);
+        vm |= 1u << i;
+      }
+    }
+    __syncthreads();  // the carry and the map have been read
+    if (!last) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (v[q] > 0u && st[q] <= fresh && fresh < st[q] + v[q]) {
+          const unsigned sl = 4u * t + unsigned(q);
+          next[0] = sl;
+          next[1] = (sl == cur ? off : 0u) + (fresh - st[q]);
+        }
+    }
+    const unsigned live = block_reduce(fs.sh, unsigned(__popc(vm)), 0u, 0u).sum;
+    if (last) {
+      finish_select<BEAM>(p, fs, r, key, idx, vm, live);
+      return;
+    }
+    cur = next[0];
+    off = next[1];
+    if (live == carried) continue;  // nothing fresh beats the carry
+    // keep the exact top W seen so far (in index order)
+    const Cut cut = find_cut(fs.sh, key, vm, p.W);
+    const unsigned keep = cut_mask(fs.sh, key, vm, cut);
+    const Ordered o = ordered_plan(keep, fs.sh);
+    unsigned kmin = ~0u;
+    ordered_apply(keep, o, fs.sh, [&](int i, unsigned rank) {
+      fs.srt2[rank] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~idx[i]);
+      kmin = min(kmin, key[i]);
+    });
+    floor_key = block_reduce(fs.sh, 0u, kmin, 0u).lo;
+    carried = o.total;
+  }
 }
 
 unsigned pow2_ceil(unsigned x) {
@@ -665,10 +969,25 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
   if (cap > unsigned(kSelectChunk) / 4) cap = std::max(unsigned(kSelectChunk) / 4, pow2_ceil(W));
   plan->cap = cap;
   plan->group = unsigned(kSelectChunk) / cap;
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const unsigned nchunks = (N + kSelectChunk - 1) / kSelectChunk;
+  // Two-pass path: enough wave maxima (2048 candidates each) for a tight
+  // bound, few enough chunks for the one-workgroup gather.
+  if (N > unsigned(kSelectChunk) && uint64_t(N) >= uint64_t(2) * W * 2048u &&
+      nchunks <= unsigned(kSelectMaxGatherSlots)) {
+    plan->two_pass = true;
+    plan->nchunks = nchunks;
+    plan->nseg = nchunks * (kSelectThreads / 64);
+    plan->seg_off = 0;
+    plan->slot_off = up(size_t(R) * plan->nseg * sizeof(unsigned));
+    plan->cnt_off = plan->slot_off + up(size_t(R) * nchunks * cap * sizeof(uint2));
+    plan->total = plan->cnt_off + up(size_t(R) * nchunks * sizeof(uint2));
+    return true;
+  }
   size_t pairs[2] = {0, 0}, counts[2] = {0, 0};
   int s = 0;
   if (N > unsigned(kSelectChunk)) {
-    unsigned slots = (N + kSelectChunk - 1) / kSelectChunk;  // stage 0: raw chunks
+    unsigned slots = nchunks;  // stage 0: raw chunks
     plan->nwg[0] = slots;
     plan->nin[0] = N;
     pairs[0] = size_t(R) * slots * cap * sizeof(uint2);
@@ -689,7 +1008,6 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
     plan->final_in = N;
   }
   plan->stages = s;
-  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   size_t off = 0;
   for (int b = 0; b < 2; ++b) {
     plan->pair_off[b] = off;
@@ -720,6 +1038,28 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
   p.inv_v = 1.0 / double(vocab);
   char* ws = static_cast<char*>(workspace);
   const bool has_beam = beam != nullptr;
+  if (plan.two_pass) {
+    p.segmax = reinterpret_cast<unsigned*>(ws + plan.seg_off);
+    p.nseg = plan.nseg;
+    p.nwg = plan.nchunks;
+    p.cand_out = reinterpret_cast<uint2*>(ws + plan.slot_off);
+    p.cnt_out = reinterpret_cast<unsigned*>(ws + plan.cnt_off);
+    const unsigned blocks = unsigned(R) * plan.nchunks;
+    if (has_beam) select_segmax_kernel<true><<<blocks, kThreads, 0, st>>>(p);
+    else select_segmax_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (has_beam) select_filter_kernel<true><<<blocks, kThreads, 0, st>>>(p);
+    else select_filter_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    p.cand_in = p.cand_out;
+    p.cnt_in = p.cnt_out;
+    p.nslots_in = plan.nchunks;
+    if (has_beam) select_gather_kernel<true><<<R, kThreads, 0, st>>>(p);
+    else select_gather_kernel<false><<<R, kThreads, 0, st>>>(p);
+    return hipGetLastError();
+  }
   for (int s = 0; s < plan.stages; ++s) {
     const int in = (s - 1) & 1, out = s & 1;
     p.cand_in = s == 0 ? nullptr : reinterpret_cast<const uint2*>(ws + plan.pair_off[in]);

@@ -233,6 +233,10 @@ def make_select_inputs(R: int, prev_width: int, vocab: int, seed: int,
     shape = (R, prev_width, vocab)
     if kind == "ties":
         logp = rng.integers(-3, 4, size=shape).astype(np.float32)
+    elif kind == "rising":
+        # small spread inside a row, beam scores rising with the row: later
+        # candidates keep beating earlier ones
+        logp = (-rng.random(shape) * 0.5).astype(np.float32)
     else:
         x = rng.standard_normal(shape) * 2.0
         m = x.max(axis=-1, keepdims=True)
@@ -242,12 +246,15 @@ def make_select_inputs(R: int, prev_width: int, vocab: int, seed: int,
             specials = [-0.0, 0.0, np.inf, -np.inf, np.nan, -np.nan]
             for j, val in enumerate(specials):
                 logp[(u >= 0.02 * j) & (u < 0.02 * (j + 1))] = np.float32(val)
-        elif kind != "logsoftmax":
+        elif kind not in ("logsoftmax", "rising"):
             raise ValueError(kind)
     beam = None
     if with_beam:
         if kind == "ties":
             beam = rng.integers(-2, 3, size=(R, prev_width)).astype(np.float32)
+        elif kind == "rising":
+            beam = np.broadcast_to(np.arange(prev_width, dtype=np.float32),
+                                   (R, prev_width)).copy()
         else:
             b = -np.abs(rng.standard_normal((R, prev_width)) * 2.0)
             beam = (-np.sort(-b, axis=-1)).astype(np.float32)

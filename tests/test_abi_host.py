@@ -161,8 +161,14 @@ def _select_plan_bytes(R, P, V, W, chunk=16384):
     if cap > chunk // 4:
         cap = max(chunk // 4, p2(W))
     group = chunk // cap
-    pairs, counts = [0, 0], [0, 0]
+    up = lambda x: -(-x // 256) * 256
     n = P * V
+    nchunks = -(-n // chunk)
+    if n > chunk and n >= 2 * W * 2048 and nchunks <= 2048:
+        # two-pass path: wave maxima (one per 2048 candidates), one slot of
+        # `cap` pairs per chunk, one (count, largest key) pair per chunk
+        return up(R * nchunks * 8 * 4) + up(R * nchunks * cap * 8) + up(R * nchunks * 8)
+    pairs, counts = [0, 0], [0, 0]
     if n > chunk:
         slots = -(-n // chunk)
         pairs[0], counts[0] = R * slots * cap * 8, R * slots * 4
@@ -179,7 +185,8 @@ def _select_plan_bytes(R, P, V, W, chunk=16384):
 @pytest.mark.parametrize("R,P,V,W", [(1, 3, 5, 7), (2, 8, 2048, 4096), (1, 512, 8192, 512),
                                      (3, 37, 1001, 300), (1, 1024, 4096, 4096),
                                      (4, 1024, 4096, 1024), (1, 1, 16385, 17),
-                                     (7, 65536, 8192, 4096)])
+                                     (7, 65536, 8192, 4096), (1, 512, 8192, 64),
+                                     (2, 4096, 8192, 1), (1, 1023, 2048, 512)])
 def test_select_workspace_bytes(lib, R, P, V, W):
     assert ab.onela_select_workspace_bytes(R, P, V, W) == _select_plan_bytes(R, P, V, W)
 

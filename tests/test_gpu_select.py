@@ -27,6 +27,16 @@ CASES = [
     ("many_stages_w4096", 1, 1024, 4096, 4096, "ties", True),
     ("r4_w1024", 4, 1024, 4096, 1024, "logsoftmax", True),
     ("chunk_plus_one", 1, 1, 16385, 17, "ties", False),
+    # two-pass path (wave-maxima bound): heavy ties overflow one gather round
+    # and some chunks their slot; special values; ragged last chunk
+    ("two_pass_ties_rounds", 1, 512, SELECT_CODEBOOK, 512, "ties", True),
+    ("two_pass_ties_slot_overflow", 1, 512, SELECT_CODEBOOK, 64, "ties", True),
+    ("two_pass_special", 2, 600, 4096, 256, "special", True),
+    ("two_pass_ragged", 3, 1023, 2047, 500, "logsoftmax", True),
+    ("two_pass_width_one", 2, 700, 3000, 1, "logsoftmax", False),
+    # rising beam scores: many survivors, each gather round beats the last
+    ("two_pass_rising_rounds", 1, 512, SELECT_CODEBOOK, 512, "rising", True),
+    ("two_pass_rising_r2_w1024", 2, 1024, 4096, 1024, "rising", True),
 ]
 
 
