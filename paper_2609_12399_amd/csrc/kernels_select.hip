@@ -9,8 +9,11 @@
 // score (sign-magnitude flip; all NaNs map to 0), then on the flat index.
 //
 // The work is HBM-bound (N = W_prev * V fp32 scores per request, read once),
-// so it is organised as a reduction tree of filters rather than a global
-// sort.  A 512-thread workgroup holds 16384 candidates (32 per lane):
+// so it is organised as filters with provable bounds rather than a global
+// sort.  Large calls take the two-pass path (wave maxima, then one filter
+// pass, then one merging workgroup per request; described at its kernels
+// below); smaller ones a reduction tree.  A 512-thread workgroup holds 16384
+// candidates (32 per lane):
 //   * stage kernel: keeps a superset of its candidates' top min(W, n) and
 //     writes it, in index order, to an output slot of `cap` (key, index)
 //     pairs plus a count.  A 2048-bin histogram of the maxima of groups of

@@ -2,6 +2,7 @@
 
     python -m paper_2609_12399_amd.rocprof_summary trace <dir-or-file>
     python -m paper_2609_12399_amd.rocprof_summary pmc <FETCH_SIZE dir> <WRITE_SIZE dir>
+    python -m paper_2609_12399_amd.rocprof_summary mfma <counter dir> [<trace dir>]
 
 ``trace`` reads a ``--kernel-trace`` result (``*_kernel_trace.csv`` or a
 ``*_results.db``) and prints one markdown row per kernel instance (calls,
@@ -9,7 +10,13 @@ average / median / min duration).  ``pmc`` reads two ``--pmc FETCH_SIZE`` and
 ``--pmc WRITE_SIZE`` runs (``*_counter_collection.csv``) and prints the
 average KiB per dispatch of each counter and kernel, raw and scaled by the
 factors a plain copy of known size gives (the largest device copy in the
-same runs, whose true read and write sizes equal its byte count).
+same runs, whose true read and write sizes equal its byte count).  ``mfma``
+reads a ``--pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES
+GRBM_GUI_ACTIVE`` run and prints, per kernel, the bf16 MFMA flops per dispatch
+(MOPS x 512), the matrix-core busy fraction (busy cycles over active cycles
+times the 1024 SIMDs, rocprofv3's MfmaUtil; the CSV sums GRBM_GUI_ACTIVE over
+the 8 XCDs, so one XCD's active cycles are taken as that sum / 8) and, given a
+kernel trace of the same command, the achieved bf16 MFMA rate.
 """
 from __future__ import annotations
 
@@ -127,11 +134,61 @@ def summarize_pmc(fetch_dir: str, write_dir: str, copy_bytes: int | None = None)
     return "\n".join(out)
 
 
+SIMD_NUM = 1024  # MI355X: 256 CUs x 4 SIMDs
+XCD_NUM = 8
+
+
+def mfma_stats(counter_dir: str):
+    """{(kernel, workgroups): (dispatches, flops, busy cycles, active cycles)},
+    averages per dispatch."""
+    acc = defaultdict(lambda: defaultdict(list))
+    for name, grid, wg, cname, val in pmc_rows(counter_dir):
+        acc[(short_name(name), grid // max(wg, 1))][cname].append(val)
+    out = {}
+    for key, c in acc.items():
+        mops = c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", [])
+        busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", [])
+        gui = c.get("GRBM_GUI_ACTIVE", [])
+        if not (mops and busy and gui):
+            continue
+        avg = lambda v: sum(v) / len(v)
+        out[key] = (len(mops), avg(mops) * 512, avg(busy), avg(gui))
+    return out
+
+
+def mfma_util(busy: float, gui_sum: float) -> float:
+    """Per cent of SIMD cycles with the matrix core busy."""
+    return 100.0 * busy / (gui_sum / XCD_NUM * SIMD_NUM)
+
+
+def summarize_mfma(counter_dir: str, trace_dir: str | None = None) -> str:
+    durs = defaultdict(list)
+    if trace_dir:
+        for name, grid, wg, dur in trace_rows(trace_dir):
+            durs[(short_name(name), grid // max(wg, 1))].append(dur)
+    out = ["| kernel | workgroups | dispatches | bf16 MFMA GFLOP | MfmaUtil % | "
+           "avg us (trace) | bf16 MFMA TFLOP/s |",
+           "|---|---|---|---|---|---|---|"]
+    for (name, g), (n, flops, busy, gui) in sorted(mfma_stats(counter_dir).items(),
+                                                    key=lambda kv: -kv[1][1]):
+        if flops == 0:
+            continue
+        util = mfma_util(busy, gui)
+        d = durs.get((name, g))
+        us = sum(d) / len(d) / 1e3 if d else None
+        rate = f"{flops / (us * 1e-6) / 1e12:.1f}" if us else "-"
+        out.append(f"| {name} | {g} | {n} | {flops / 1e9:.3f} | {util:.2f} | "
+                   f"{'-' if us is None else f'{us:.2f}'} | {rate} |")
+    return "\n".join(out)
+
+
 if __name__ == "__main__":
     if len(sys.argv) >= 3 and sys.argv[1] == "trace":
         print(summarize_trace(sys.argv[2]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "pmc":
         print(summarize_pmc(sys.argv[2], sys.argv[3]))
+    elif len(sys.argv) >= 3 and sys.argv[1] == "mfma":
+        print(summarize_mfma(sys.argv[2], sys.argv[3] if len(sys.argv) > 3 else None))
     else:
         print(__doc__)
         sys.exit(2)
