@@ -613,12 +613,19 @@ __device__ inline void sort_emit(const SelectParams& p, FinalShared& fs, unsigne
   const float* logp_r = p.logp + size_t(r) * p.N;
   auto emit = [&](unsigned j, unsigned long long c) {
     const unsigned fi = ~unsigned(c);
+    const unsigned key = unsigned(c >> 32);
     const unsigned row = row_of(fi, p.V, p.inv_v);
     const size_t o2 = size_t(r) * p.W + j;
     p.parents[o2] = int(row);
     p.tokens[o2] = int(fi - row * p.V);
-    if constexpr (BEAM) p.scores[o2] = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
-    else p.scores[o2] = logp_r[fi];
+    // the key is the score's bit pattern for every number (no re-read); a NaN
+    // (key 0) is recomputed so that its own bits come out
+    float sc = __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+    if (key == 0u) {
+      if constexpr (BEAM) sc = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
+      else sc = logp_r[fi];
+    }
+    p.scores[o2] = sc;
   };
   __syncthreads();  // srt is written; the caller's reads of fs.sh are done
   const Red3 kr = block_reduce(fs.sh, 0u, klo, khi);
