@@ -460,8 +460,9 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     if (sb < W) {
       float4* dst = at<float4>(p.o, (((unsigned(r) * W + sb) * p.HV + hv) * DV + row0) * 4u);
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
-        dst[i] = make_float4(ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]);
+      for (int i = 0; i < MB; ++i)  // o is not read again: streaming stores
+        __builtin_nontemporal_store(f32x4{ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]},
+                                    reinterpret_cast<f32x4*>(dst + i));
       VR dw;
       float_to_delta<BF16>(dt, dw.w, RPL);
       dw.store(d_slab(NA), sb * vslot + row0 * IOB);

@@ -40,8 +40,8 @@ def short_name(name: str) -> str:
         dk, dv, mb, nblk, chain, bf16, fused = m.groups()
         mode = "fused" if fused == "true" else "decode"
         return f"decode_kernel<{mode}, d={dk}, chain={chain}, {'bf16' if bf16 == 'true' else 'f32'}>"
-    for k in ("resolve_kernel", "append_kernel", "prefill_kernel", "fullstate_kernel",
-              "clear_status_kernel"):
+    for k in ("resolve_kernel", "append_kernel", "prefill_kernel", "prefill_chunk_kernel",
+              "prefill_scan_kernel", "fullstate_kernel", "clear_status_kernel"):
         if k in name:
             return k
     m = re.search(r"(select_\w+_kernel)(<[^>]*>)?", name)
