@@ -21,7 +21,7 @@
 //     U^T [d_v][C] and g to the workspace.  No division: products of alpha
 //     are formed directly, so alpha = 0 is exact.
 //   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
-//     state rows) walks the chunks in order: X^T = W S^T, D^T = U^T - X^T,
+//     state rows; the row blocks of a head share one XCD) walks the chunks in order: X^T = W S^T, D^T = U^T - X^T,
 //     S^T <- g S^T + Kt^T D^T, on v_mfma_f32_16x16x4f32.  Wave w owns the
 //     state columns 16 w .. 16 w + 15 (a 16 x 16 fp32 accumulator tile that
 //     never leaves registers); the contraction orders are chosen so that the
@@ -52,6 +52,7 @@ struct PrefillParams {
   float* utb;         // [R*HV][nch][DV][C]
   float* gb;          // [R*HV][nch]
   int HK, HV, P, nch;
+  int xcd_map;  // phase 2: all row blocks of a unit on one XCD (units % 8 == 0)
 };
 
 // 8 consecutive io elements (16 B of bf16 or 32 B of fp32) at element i.
@@ -277,7 +278,20 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   __shared__ f32x4 xp[NW][4][64];  // partial X^T tiles of every wave
   __shared__ f32x4 xs[4][64];      // their sums
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int rb = blockIdx.x % (DV / 16), unit = blockIdx.x / (DV / 16);
+  // The DV / 16 row blocks of a (request, value head) read the same W and
+  // Kt of every chunk.  Workgroups are dispatched round-robin over the 8
+  // XCDs (block i on XCD i % 8), so when the unit count is a multiple of 8
+  // all row blocks of a unit are placed on one XCD and share its L2.
+  constexpr int NRB = DV / 16;
+  int rb, unit;
+  if (p.xcd_map) {
+    const int x = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    unit = x + 8 * (slot / NRB);
+    rb = slot % NRB;
+  } else {
+    rb = blockIdx.x % NRB;
+    unit = blockIdx.x / NRB;
+  }
   const int row0 = 16 * rb;
   const int lr = lane & 15, lq = lane >> 4;
   // st[i] = S^T(k = 16 w + 4 lq + i, n = lr) = S(row0 + lr, 16 w + 4 lq + i)
@@ -398,6 +412,7 @@ hipError_t launch_prefill_chunked(const Shape& s, int prompt_len, const void* k,
   prm.P = prompt_len;
   prm.nch = (prompt_len + kC - 1) / kC;
   const size_t units = size_t(s.R) * s.HV, nch = size_t(prm.nch);
+  prm.xcd_map = units % 8 == 0 ? 1 : 0;
   float* base = static_cast<float*>(workspace);
   prm.wb = base;
   prm.ktb = prm.wb + units * nch * kC * s.dk;
