@@ -25,15 +25,24 @@
 //
 // Work decomposition.  One workgroup = (request, value head, row slice of DVW
 // state rows, 16*NBLK beams), d_k/16 waves of 16*MB rows each (MB = DVW/d_k;
-// wide d_v is split into row slices, each folding its beams again).  Phase 1 (fold): LPB lanes per beam, each owning EPL
-// consecutive key elements; dot products are reduced across those lanes with
-// DPP.  The folded queries are written, split into hi/lo, to LDS directly in
-// MFMA B-fragment order; the fold scalars g_j go to LDS too.  Phase 2
-// (contract): wave w multiplies its 16*MB state rows (A fragments: split in
-// registers from fp32 S_ctx at step 0, stored split in the workspace for
-// later steps) by the beams' B fragments.  Phase 3
-// (epilogue): each lane holds 4*MB consecutive output rows of one beam, adds
-// sum_j g_j v_j[rows] and stores them as 16-byte vectors.
+// wide d_v is split into row slices, each folding its beams again).
+// Phase 1 (fold): LPB lanes per beam, each owning EPL consecutive key
+// elements and VPL = DVW/LPB consecutive value rows of its beam; dot products
+// are reduced across those lanes with DPP, and each lane accumulates
+// sum_j g_j v_j over its value rows as the g_j appear.  The folded queries
+// are written, split into hi/lo, to LDS directly in MFMA B-fragment order,
+// the value-term sums to LDS rows per beam.  Phase 2 (contract): wave w
+// multiplies its 16*MB state rows (A fragments: split in registers from fp32
+// S_ctx at step 0, stored split in the workspace for later steps) by the
+// beams' B fragments.  Phase 3 (epilogue): each lane holds 4*MB consecutive
+// output rows of one beam, adds the value-term sums of those rows from LDS
+// and stores them as 16-byte vectors.
+//
+// Every global load is made by the fold lane that owns the beam: whole
+// 128-byte lines of q, k and v per record, plus one parent index and one
+// ancestry row per beam.  A CU has a limited number of memory requests in
+// flight, so the number of requests per wave, not only the bytes, sets how
+// soon the second wave of each SIMD gets its data.
 //
 // Why 32 beams and 16 rows per wave: every workgroup streams its head's
 // whole shared state (64 KiB at d = 128) through the CU's vector memory pipe
@@ -108,15 +117,18 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   constexpr int LPB = NT / BEAMS;    // fold lanes per beam
   constexpr int EPL = DK / LPB;      // key elements per fold lane
   constexpr int C8 = EPL / 8;        // 8-element chunks per fold lane
+  constexpr int VPL = DVW / LPB;     // value rows per fold lane
+  constexpr int VS = DVW + 4;        // padded LDS row of the value-term sums
   constexpr int KS = DK / 32;        // MFMA k-steps
   constexpr int NA = CHAIN - 1;      // ancestral records (= step t)
   constexpr int NAX = NA > 0 ? NA : 1;
   constexpr unsigned IOB = BF16 ? 2 : 4;
   static_assert(EPL % 8 == 0 && EPL >= 8, "fold lanes must own 8-element chunks");
+  static_assert(VPL == 8 || VPL == 16, "fold lanes own 8 or 16 value rows");
   static_assert(LPB <= 64 && (LPB & (LPB - 1)) == 0, "fold lane group within a wave");
 
   __shared__ uint4 p_lds[2][NBLK][KS][4][16];  // folded queries, B-fragment order
-  __shared__ float g_lds[BEAMS][CHAIN];        // fold scalars g_j
+  __shared__ float v_lds[BEAMS][VS];           // sum_j g_j v_j per beam, this slice's rows
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -149,21 +161,18 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   const int W = p.W;
   const int wmax = p.wmax, tmax = p.tmax;
 
-  // fold lanes: beam fb of the tile, key elements [li*EPL, li*EPL + EPL)
+  // fold lanes: beam fb of the tile, key elements [li*EPL, li*EPL + EPL) and
+  // value rows DVW*slice + [li*VPL, li*VPL + VPL)
   const int fb = tid / LPB;
   const int li = tid - fb * LPB;
   const int fbeam = b0 + fb;
   const bool fvalid = fbeam < W;
   const int fbc = fvalid ? fbeam : 0;
+  const unsigned voff = (unsigned(DVW) * slice + unsigned(li) * VPL) * IOB;
   // epilogue lanes: beam (lane & 15) of block nb, rows row0 + [0, RPL)
   const int g4 = lane >> 4;
-  const unsigned row0 = DVW * slice + 16 * MB * w + RPL * g4;
-  int sbc[NBLK];
-#pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb) {
-    const int sb = b0 + nb * 16 + (lane & 15);
-    sbc[nb] = sb < W ? sb : 0;
-  }
+  const unsigned rloc = 16 * MB * w + RPL * g4;  // row within the slice
+  const unsigned row0 = DVW * slice + rloc;
 
   // uniform bases (per workgroup)
   const int* anc_r = p.anc_rd + long(r) * wmax * tmax;
@@ -199,36 +208,30 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     return ab_slab(j)[slot];
   };
 
-  // ---- round 1: indices (parents in FUSED mode, h_t otherwise), then every
-  // load that needs no index: the query and the beam's own step-t record
-  // (fold operands first, the v rows for the epilogue after them).
-  int fsrc[NAX], ssrc[NBLK][NAX];
-  bool fpok = true, spok[NBLK];
-  int fpar = 0, spar[NBLK];
-#pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb) spok[nb] = true;
+  // ---- round 1: indices (the parent in FUSED mode, the beam's row of h_t
+  // otherwise), then every load that needs no index: the query and the
+  // beam's own step-t record.  Each fold lane loads only its own beam's
+  // data, as whole 128-byte lines, which keeps the number of memory
+  // requests per wave small: a CU holds a limited number in flight, and
+  // requests beyond it wait for earlier ones to return.
+  int fsrc[NAX];
+  bool fpok = true;
+  int fpar = 0;
   if constexpr (NA > 0) {
     if constexpr (FUSED) {
-      const int* prow = p.parents + long(r) * W;
-      fpar = prow[fbc];
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb) spar[nb] = prow[sbc[nb]];
+      fpar = p.parents[long(r) * W + fbc];
     } else {
 #pragma unroll
       for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-        for (int j = 0; j < NA; ++j) ssrc[nb][j] = anc_r[sbc[nb] * tmax + j];
     }
   }
 
   using K8 = RawV<BF16, 8>;
-  using VR = RawV<BF16, RPL>;
+  using VR = RawV<BF16, VPL>;
   K8 qr[C8];
   K8 kr[CHAIN][C8];
   float2 abr[CHAIN];
-  VR vr[NBLK][CHAIN];
+  VR vr[CHAIN];
   {
     const unsigned qoff = ((unsigned(r) * W + fbc) * p.HK + hk) * kslot + li * EPL * IOB;
 #pragma unroll
@@ -238,18 +241,14 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       for (int c = 0; c < C8; ++c) kr[NA][c].load(p.k_in, qoff + c * K8::kBytes);
       const unsigned gi = (unsigned(r) * W + fbc) * p.HV + hv;
       abr[NA] = make_float2(p.alpha_in[gi], p.beta_in[gi]);
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb)
-        vr[nb][NA].load(p.v_in, ((unsigned(r) * W + sbc[nb]) * p.HV + hv) * vslot + row0 * IOB);
+      vr[NA].load(p.v_in, gi * vslot + voff);
     } else {
       const char* ks = k_slab(NA);
 #pragma unroll
       for (int c = 0; c < C8; ++c)
         kr[NA][c].load(ks, fbc * kstride + li * EPL * IOB + c * K8::kBytes);
       abr[NA] = load_ab(NA, fbc);
-      const char* vs = v_slab(NA);
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb) vr[nb][NA].load(vs, sbc[nb] * vstride + row0 * IOB);
+      vr[NA].load(v_slab(NA), fbc * vstride + voff);
     }
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -260,58 +259,33 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   // then the records of steps <= t-2 once that row is back.
   bool fok[CHAIN];
   fok[NA] = true;
-  auto load_fold_record = [&](int j, int slot) {
+  auto load_record = [&](int j, int slot) {
     const char* ks = k_slab(j);
 #pragma unroll
     for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kstride + li * EPL * IOB + c * K8::kBytes);
     abr[j] = load_ab(j, slot);
+    vr[j].load(v_slab(j), slot * vstride + voff);
   };
   if constexpr (FUSED && NA > 0) {
     fpok = unsigned(fpar) < unsigned(p.W_prev);
     const int pf = fpok ? fpar : 0;
     fsrc[NA - 1] = pf;
     fok[NA - 1] = fpok;
-    load_fold_record(NA - 1, pf);
-    int ps[NBLK];
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb) {
-      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
-      ps[nb] = spok[nb] ? spar[nb] : 0;
-      ssrc[nb][NA - 1] = ps[nb];
-      vr[nb][NA - 1].load(v_slab(NA - 1), ps[nb] * vstride + row0 * IOB);
-    }
+    load_record(NA - 1, pf);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps[nb] * tmax + j];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) {
       fok[j] = fpok && slot_ok(j, fsrc[j]);
-      load_fold_record(j, fok[j] ? fsrc[j] : 0);
+      load_record(j, fok[j] ? fsrc[j] : 0);
     }
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA - 1; ++j) {
-        const bool ok = spok[nb] && slot_ok(j, ssrc[nb][j]);
-        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vstride + row0 * IOB);
-      }
   } else {
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
       fok[j] = slot_ok(j, fsrc[j]);
-      load_fold_record(j, fok[j] ? fsrc[j] : 0);
+      load_record(j, fok[j] ? fsrc[j] : 0);
     }
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA; ++j) {
-        const bool ok = slot_ok(j, ssrc[nb][j]);
-        vr[nb][j].load(v_slab(j), (ok ? ssrc[nb][j] : 0) * vstride + row0 * IOB);
-      }
   }
 
   // ---- shared-state rows of this wave in MFMA A-fragment order, issued
@@ -349,10 +323,14 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- phase 1: fold the query newest -> oldest (scaled form)
+  // ---- phase 1: fold the query newest -> oldest (scaled form), and sum
+  // the value terms g_j v_j of this lane's rows as the g_j appear
   float pt[EPL];
 #pragma unroll
   for (int c = 0; c < C8; ++c) qr[c].to_float(pt + 8 * c);
+  float vs[VPL];
+#pragma unroll
+  for (int e = 0; e < VPL; ++e) vs[e] = 0.f;
   float scale = 1.f;
 #pragma unroll
   for (int j = NA; j >= 0; --j) {
@@ -369,7 +347,11 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     const float alpha = fok[j] ? abr[j].x : 1.f;
     const float beta = fok[j] ? abr[j].y : 0.f;
     const float gt = beta * cdot;
-    if (li == 0) g_lds[fb][j] = scale * gt;
+    const float gj = scale * gt;
+    float vf[VPL];
+    vr[j].to_float(vf);
+#pragma unroll
+    for (int e = 0; e < VPL; ++e) vs[e] = fmaf(gj, vf[e], vs[e]);
 #pragma unroll
     for (int e = 0; e < EPL; ++e) pt[e] = fmaf(-gt, kf[e], pt[e]);
     scale *= alpha;
@@ -385,6 +367,10 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     p_lds[0][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = hi;
     p_lds[1][fb >> 4][k0 >> 5][(k0 >> 3) & 3][fb & 15] = lo;
   }
+#pragma unroll
+  for (int e = 0; e < VPL; e += 4)
+    *reinterpret_cast<float4*>(&v_lds[fb][li * VPL + e]) =
+        make_float4(vs[e], vs[e + 1], vs[e + 2], vs[e + 3]);
 
   // ---- FUSED: index h_t and the step-t record into the context
   if constexpr (FUSED) {
@@ -408,12 +394,7 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       }
       if (!borrow && li == 0) ab_slab(NA)[fbeam] = abr[NA];
     }
-    if (!borrow) {
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb)
-        if (b0 + nb * 16 + (lane & 15) < W)
-          vr[nb][NA].store(v_slab(NA), sbc[nb] * vslot + row0 * IOB);
-    }
+    if (!borrow && fvalid) vr[NA].store(v_slab(NA), fbeam * vslot + voff);
   }
   __syncthreads();
 
@@ -461,21 +442,19 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       }
   }
 
-  // ---- phase 3: add the v-terms and store RPL consecutive rows per lane
+  // ---- phase 3: add the value terms and store RPL consecutive rows per lane
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
     const int bl = nb * 16 + (lane & 15);
     const int sb = b0 + bl;
     float ov[RPL];
 #pragma unroll
-    for (int e = 0; e < RPL; ++e) ov[e] = acx[nb][e >> 2][e & 3] + acc[nb][e >> 2][e & 3];
-#pragma unroll
-    for (int j = 0; j < CHAIN; ++j) {
-      const float gj = g_lds[bl][j];
-      float vf[RPL];
-      vr[nb][j].to_float(vf);
-#pragma unroll
-      for (int e = 0; e < RPL; ++e) ov[e] = fmaf(gj, vf[e], ov[e]);
+    for (int e = 0; e < RPL; e += 4) {
+      const float4 v4 = *reinterpret_cast<const float4*>(&v_lds[bl][rloc + e]);
+      ov[e] = acx[nb][e >> 2][0] + acc[nb][e >> 2][0] + v4.x;
+      ov[e + 1] = acx[nb][e >> 2][1] + acc[nb][e >> 2][1] + v4.y;
+      ov[e + 2] = acx[nb][e >> 2][2] + acc[nb][e >> 2][2] + v4.z;
+      ov[e + 3] = acx[nb][e >> 2][3] + acc[nb][e >> 2][3] + v4.w;
     }
     // o is written once and not read again by the step: non-temporal
     // (streaming) stores, about 0.5 us per launch faster than plain ones.
