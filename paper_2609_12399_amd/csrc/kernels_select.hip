@@ -122,6 +122,18 @@ __device__ inline Red3 wave_reduce(unsigned s, unsigned lo, unsigned hi) {
   return r;
 }
 
+// Bitwise OR over the 64 lanes, wave-uniform.
+__device__ inline unsigned wave_or(unsigned x) {
+  x |= dppu<0xB1>(x);   // quad_perm [1,0,3,2]
+  x |= dppu<0x4E>(x);   // quad_perm [2,3,0,1]
+  x |= dppu<0x141>(x);  // row_half_mirror
+  x |= dppu<0x140>(x);  // row_mirror
+  return unsigned(__builtin_amdgcn_readlane(int(x), 0)) |
+         unsigned(__builtin_amdgcn_readlane(int(x), 16)) |
+         unsigned(__builtin_amdgcn_readlane(int(x), 32)) |
+         unsigned(__builtin_amdgcn_readlane(int(x), 48));
+}
+
 // (sum, min, max) over the workgroup.
 __device__ inline Red3 block_reduce(SelShared& sh, unsigned s, unsigned lo, unsigned hi) {
   const Red3 w = wave_reduce(s, lo, hi);
@@ -181,12 +193,19 @@ struct Ordered {
 __device__ inline Ordered ordered_plan(unsigned f, SelShared& sh) {
   Ordered o;
   const unsigned lane = lane_id(), w = threadIdx.x >> 6;
+  // slots flagged anywhere in the wave (a filter pass flags few): the others
+  // skip their ballot
+  const unsigned any = wave_or(f);
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
-    const unsigned long long b = __ballot((f >> i) & 1u);
-    const unsigned m = mbcnt(b);
+    unsigned m = 0u, c = 0u;
+    if ((any >> i) & 1u) {
+      const unsigned long long b = __ballot((f >> i) & 1u);
+      m = mbcnt(b);
+      c = unsigned(__popcll(b));
+    }
     o.pre[i / 4] = (i % 4 == 0) ? m : (o.pre[i / 4] | (m << (8 * (i % 4))));
-    if (lane == 0) sh.tab[i * kWaves + w] = unsigned(__popcll(b));
+    if (lane == 0) sh.tab[i * kWaves + w] = c;
   }
   __syncthreads();
   if (w == 0) {
@@ -731,14 +750,20 @@ __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p)
   const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
   // wave maxima of the request; segment (chunk s / 8, wave s % 8) exists when
   // its first candidate does
+  // (only the rows i * kThreads < nseg are read: a workgroup-uniform bound,
+  // so no load is issued for the empty tail of the lanes' slots)
   unsigned mk[kNI], mvm = 0u;
   const unsigned* seg = p.segmax + size_t(r) * p.nseg;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) {
-    const unsigned s = unsigned(i) * kThreads + threadIdx.x;
-    const bool valid = s < p.nseg && (s / kWaves) * unsigned(kSelectChunk) + (s % kWaves) * 64u < p.N;
-    mk[i] = seg[valid ? s : 0u];
-    mvm |= unsigned(valid) << i;
+    mk[i] = 0u;
+    if (unsigned(i) * kThreads < p.nseg) {
+      const unsigned s = unsigned(i) * kThreads + threadIdx.x;
+      const bool valid =
+          s < p.nseg && (s / kWaves) * unsigned(kSelectChunk) + (s % kWaves) * 64u < p.N;
+      mk[i] = seg[valid ? s : 0u];
+      mvm |= unsigned(valid) << i;
+    }
   }
 #pragma unroll
   for (int i = 0; i < kNI; ++i) mk[i] = ((mvm >> i) & 1u) ? mk[i] : 0u;
