@@ -16,9 +16,11 @@
 // g = gamma_{C-1}.  U, W and Kt depend only on the chunk's own tokens.
 //
 //   phase 1 (prefill_chunk_kernel): one workgroup per (request, value head,
-//     chunk) forms Gamma, M, T (column-parallel forward substitution), W, U
-//     and Kt in LDS with fp32 FMAs and stores W [C][d_k], Kt^T [d_k][C],
-//     U^T [d_v][C] and g to the workspace.  No division: products of alpha
+//     chunk) forms the decay products Gamma from a doubling table (lane
+//     shuffles), M from K K^T, T by forward substitution (each column held in
+//     registers by a quad of lanes), then W, U and Kt, and stores W [C][d_k],
+//     Kt^T [d_k][C], U^T [d_v][C] and g to the workspace.  The three
+//     products run on v_mfma_f32_16x16x4f32.  No division: products of alpha
 //     are formed directly, so alpha = 0 is exact.
 //   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
 //     state rows; the row blocks of a head share one XCD) walks the chunks in order: X^T = W S^T, D^T = U^T - X^T,
@@ -110,43 +112,51 @@ __device__ inline void fill_rows(float* dst, const void* src, int n, int c0, Row
 template <int DK>
 struct P1Shared {
   float K[kC][DK + 1];    // the chunk's keys, fp32 (padding rows zero)
-  float T[kC][kC + 1];    // (I + M)^{-1}, then reused
+  float T[kC][kC + 1];    // (I + M)^{-1}
   float M[kC][kC + 1];
-  float X[kC][128 + 1];   // a 128-column block of beta V or beta gamma K
+  float X[kC][128 + 1];   // a 128-column block of beta V
+  float P[7][kC];         // P[k][t]: product of the 2^k decays ending at token t
   float al[kC], be[kC], gam[kC], sig[kC];
 };
 
-// out[t][c0 + j] = sum_s T[t][s] X[s][j] for j < ncols (<= 128), written by
-// fn(t, j, value).  Each thread computes an 8 x 4 block (rows t0 .. t0 + 7,
-// columns 4 j0 .. 4 j0 + 3): 12 LDS reads per 32 FMAs.
-template <typename Sh, typename F>
-__device__ inline void tri_times_block(const Sh& sh, int ncols, F&& fn) {
-  const int tid = threadIdx.x;
-  const int jb = tid & 31, tb = tid >> 5;  // 32 column groups x 8 row groups
-  if (4 * jb >= ncols) return;
-  float acc[8][4] = {};
-  for (int s = 0; s < kC; ++s) {
-    float x[4];
+// alpha_{i+1} ... alpha_t (t - i >= 0 factors; none: 1) from the doubling
+// table, in blocks of 2^k decays, largest first.  Products only, so a zero
+// decay gives an exact zero.
+__device__ inline float decay(const float (&P)[7][kC], int t, int i) {
+  float g = 1.f;
+  int pos = t;
+  const int L = t - i;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) x[q] = sh.X[s][4 * jb + q];
-#pragma unroll
-    for (int a = 0; a < 8; ++a) {
-      const float tv = sh.T[8 * tb + a][s];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc[a][q] = fmaf(tv, x[q], acc[a][q]);
+  for (int k = 6; k >= 0; --k)
+    if ((L >> k) & 1) {
+      g *= P[k][pos];
+      pos -= 1 << k;
     }
-  }
-#pragma unroll
-  for (int a = 0; a < 8; ++a)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) fn(8 * tb + a, 4 * jb + q, acc[a][q]);
+  return g;
 }
 
+// Sum over the 4 lanes of a quad.
+__device__ inline float quad_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1,
+                                                             0xF, 0xF, false));  // [1,0,3,2]
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x4E,
+                                                             0xF, 0xF, false));  // [2,3,0,1]
+  return x;
+}
+
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// The products of phase 1 run on v_mfma_f32_16x16x4f32 in 16 x 16 tiles: for
+// D = A B, lane l supplies A(l % 16, k) and B(k, l % 16) with k = l / 16 of
+// each 4-deep step and holds D(4 (l / 16) + r, l % 16), r = 0..3.
 template <int DK, int DV, bool BF16>
 __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
   P1Shared<DK>& sh = *reinterpret_cast<P1Shared<DK>*>(smem);
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, l4 = lane >> 4;
   const int c = blockIdx.x % p.nch, unit = blockIdx.x / p.nch;
   const int r = unit / p.HV, hv = unit - r * p.HV, hk = hv / (p.HV / p.HK);
   const int t0 = c * kC;
@@ -158,107 +168,116 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
                                [](int) { return 1.f; });
   if (tid < kC) {
     const bool in = tid < n;
-    sh.al[tid] = in ? p.alpha[(tok0 + tid) * p.HV + hv] : 1.f;
+    const float al = in ? p.alpha[(tok0 + tid) * p.HV + hv] : 1.f;
+    sh.al[tid] = al;
     sh.be[tid] = in ? p.beta[(tok0 + tid) * p.HV + hv] : 0.f;
+    // doubling table of decay products (lane t of wave 0 holds token t)
+    float v = al;
+    sh.P[0][tid] = v;
+#pragma unroll
+    for (int k = 1; k < 7; ++k) {
+      const float u = __shfl_up(v, 1 << (k - 1));
+      if (tid >= (1 << (k - 1))) v *= u;
+      sh.P[k][tid] = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    // gamma_t = alpha_0 ... alpha_t; sigma_t = alpha_{t+1} ... alpha_{C-1}
+    sh.gam[tid] = decay(sh.P, tid, -1);
+    sh.sig[tid] = decay(sh.P, kC - 1, tid);
+  }
+  // M is zero above its diagonal 16 x 16 tiles (the product below fills the
+  // rest)
+  for (int e = tid; e < kC * kC; e += kP1Threads) {
+    const int t = e / kC, i = e - t * kC;
+    if ((i >> 4) > (t >> 4)) sh.M[t][i] = 0.f;
   }
   __syncthreads();
-  if (tid == 0) {  // gamma_t = alpha_0 ... alpha_t
-    float g = 1.f;
+  // M(t, i) = beta_t Gamma(t, i) (k_t . k_i) for i < t, 0 for i >= t: the ten
+  // tiles on or below the diagonal of K K^T
+  for (int x = w; x < 10; x += 4) {
+    const int a = (x >= 1) + (x >= 3) + (x >= 6), b = x - a * (a + 1) / 2;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int ks = 0; ks < DK / 4; ++ks)
+      acc = mfma4(sh.K[16 * a + l16][4 * ks + l4], sh.K[16 * b + l16][4 * ks + l4], acc);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = 16 * a + 4 * l4 + q, i = 16 * b + l16;
+      const float g = decay(sh.P, t, i < t ? i : t);  // (no factor on or above the diagonal)
+      sh.M[t][i] = i < t ? sh.be[t] * g * acc[q] : 0.f;
+    }
+  }
+  __syncthreads();
+  // T = (I + M)^{-1} by forward substitution, T(t, j) = -sum_{i<t} M(t, i)
+  // T(i, j) for t > j: column j = 16 w + lane / 4 is held in registers by the
+  // quad of lanes 4 (j % 16) .. + 3, lane sub summing the rows i = sub mod 4
+  {
+    const int j = 16 * w + (lane >> 2), sub = lane & 3;
+    float x[kC / 4];
+#pragma unroll
+    for (int m = 0; m < kC / 4; ++m) x[m] = 0.f;
+#pragma unroll
     for (int t = 0; t < kC; ++t) {
-      g *= sh.al[t];
-      sh.gam[t] = g;
-    }
-  } else if (tid == 64) {  // sigma_t = alpha_{t+1} ... alpha_{C-1}
-    float s = 1.f;
-    for (int t = kC - 1; t >= 0; --t) {
-      sh.sig[t] = s;
-      s *= sh.al[t];
-    }
-  }
-  __syncthreads();
-  // Gamma(t, i) = alpha_{i+1} ... alpha_t for i < t, column i by thread i
-  // (held in T until T is formed)
-  if (tid < kC) {
-    const int i = tid;
-    float gm = 1.f;
-    for (int t = i + 1; t < kC; ++t) {
-      gm *= sh.al[t];
-      sh.T[t][i] = gm;
-    }
-  }
-  __syncthreads();
-  // M(t, i) = beta_t Gamma(t, i) (k_t . k_i) for i < t: a 4 x 4 block of
-  // (t, i) per thread.
-  {
-    const int ib = tid & 15, tb = tid >> 4;
-    float acc[4][4] = {};
-    for (int kk = 0; kk < DK; ++kk) {
-      float kt[4], ki[4];
+      float s0 = 0.f, s1 = 0.f;  // rows not computed yet hold 0
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        kt[a] = sh.K[4 * tb + a][kk];
-        ki[a] = sh.K[4 * ib + a][kk];
+      for (int m = 0; m < (t + 3) / 4; ++m) {
+        const float mv = sh.M[t][sub + 4 * m];
+        if (m & 1) s1 = fmaf(mv, x[m], s1);
+        else s0 = fmaf(mv, x[m], s0);
       }
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = fmaf(kt[a], ki[b], acc[a][b]);
+      const float s = quad_sum(s0 + s1);
+      const float val = t == j ? 1.f : (t > j ? -s : 0.f);
+      if (sub == (t & 3)) x[t >> 2] = val;
     }
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int t = 4 * tb + a, i = 4 * ib + b;
-        sh.M[t][i] = i < t ? sh.be[t] * sh.T[t][i] * acc[a][b] : 0.f;
-      }
-  }
-  __syncthreads();
-  // T = (I + M)^{-1}: column j by the 4 lanes 4j .. 4j + 3 (one wave holds
-  // 16 columns); T(t, j) = -sum_{j <= i < t} M(t, i) T(i, j) for t > j.
-  {
-    const int j = tid >> 2, sub = tid & 3;
-    for (int t = sub; t < kC; t += 4) sh.T[t][j] = t == j ? 1.f : 0.f;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    for (int t = 1; t < kC; ++t) {
-      float s = 0.f;
-      if (t > j)
-        for (int i = j + sub; i < t; i += 4) s = fmaf(sh.M[t][i], sh.T[i][j], s);
-      s += __shfl_xor(s, 1);
-      s += __shfl_xor(s, 2);
-      if (t > j && sub == 0) sh.T[t][j] = -s;
-      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    }
+    for (int m = 0; m < kC / 4; ++m) sh.T[sub + 4 * m][j] = x[m];
   }
   __syncthreads();
 
   const long cu = long(unit) * p.nch + c;
-  // W = T diag(beta gamma) K  -> wb [C][DK];  Kt^T = (diag(sigma) K)^T -> ktb [DK][C]
+  // W = T diag(beta gamma) K -> wb [C][DK];  Kt^T = (diag(sigma) K)^T -> ktb [DK][C]
   float* wdst = p.wb + cu * kC * DK;
   float* ktdst = p.ktb + cu * DK * kC;
   for (int i = tid; i < kC * DK; i += kP1Threads) {
     const int kk = i / kC, t = i - kk * kC;
     ktdst[i] = sh.sig[t] * sh.K[t][kk];
   }
-  for (int cb = 0; cb < DK; cb += 128) {
-    const int nc = DK - cb < 128 ? DK - cb : 128;
-    for (int i = tid; i < kC * nc; i += kP1Threads) {
-      const int t = i / nc, jj = i - t * nc;
-      sh.X[t][jj] = sh.be[t] * sh.gam[t] * sh.K[t][cb + jj];
+  // (T is lower triangular: row block a needs k < 16 (a + 1))
+  constexpr int NBW = DK / 16;
+  for (int x = w; x < 4 * NBW; x += 4) {
+    const int a = x / NBW, b = x - a * NBW;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int kk = 4 * (ks + u) + l4;
+        acc = mfma4(sh.T[16 * a + l16][kk], sh.be[kk] * sh.gam[kk] * sh.K[kk][16 * b + l16], acc);
+      }
     }
-    __syncthreads();
-    tri_times_block(sh, nc, [&](int t, int jj, float x) { wdst[t * DK + cb + jj] = x; });
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wdst[(16 * a + 4 * l4 + q) * DK + 16 * b + l16] = acc[q];
   }
-  // U = T diag(beta) V -> utb [DV][C]
+  // U = T diag(beta) V -> utb [DV][C] (4 consecutive tokens per lane and tile)
   float* udst = p.utb + cu * DV * kC;
   constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
+  constexpr int NBU = VC / 16;
   for (int cb = 0; cb < DV; cb += VC) {
-    const int nc = VC;
     fill_rows<VC, 129, BF16>(&sh.X[0][0], p.v, n, cb,
                              [&](int t) { return ((tok0 + t) * p.HV + hv) * DV; },
                              [&](int t) { return sh.be[t]; });
     __syncthreads();
-    tri_times_block(sh, nc, [&](int t, int jj, float x) { udst[(cb + jj) * kC + t] = x; });
+    for (int x = w; x < 4 * NBU; x += 4) {
+      const int a = x / NBU, b = x - a * NBU;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kk = 4 * (ks + u) + l4;
+          acc = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc);
+        }
+      }
+      *reinterpret_cast<f32x4*>(udst + (cb + 16 * b + l16) * kC + 16 * a + 4 * l4) = acc;
+    }
     __syncthreads();
   }
   if (tid == 0) p.gb[cu] = sh.gam[kC - 1];
