@@ -315,6 +315,11 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   const int lr = lane & 15, lq = lane >> 4;
   // st[i] = S^T(k = 16 w + 4 lq + i, n = lr) = S(row0 + lr, 16 w + 4 lq + i)
   f32x4 st = {0.f, 0.f, 0.f, 0.f};
+  float* dst = p.s_out + (long(unit) * DV + row0 + lr) * DK + 16 * w + 4 * lq;
+  if (p.nch == 0) {  // empty prompt: S = 0, and there is no chunk to read
+    *reinterpret_cast<f32x4*>(dst) = st;
+    return;
+  }
   // Loads are unconditional (past the end they re-read the last chunk) so
   // the compiler can count them and wait only for the set about to be used.
   auto load = [&](int c, ScanOps& o) {
@@ -386,7 +391,6 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
     __builtin_amdgcn_sched_barrier(0);
     step(c + 2, c3);
   }
-  float* dst = p.s_out + (long(unit) * DV + row0 + lr) * DK + 16 * w + 4 * lq;
   *reinterpret_cast<f32x4*>(dst) = st;
 }
 
