@@ -13,23 +13,28 @@
 //   D = U - W S_0^T,   U = T diag(beta) V,   W = T diag(beta gamma) K,
 // and the state after the chunk is
 //   S_C = g S_0 + D^T Kt,   Kt = diag(sigma) K,  sigma_t = Gamma(C - 1, t),
-// g = gamma_{C-1}.  U, W and Kt depend only on the chunk's own tokens.
+// g = gamma_{C-1}.  U, W and Kt depend only on the chunk's own tokens.  The
+// workspace holds them as W' = diag(sigma) W, U' = diag(sigma) U and the plain
+// keys K: with D' = diag(sigma) D = U' - W' S_0^T the update is
+// S_C = g S_0 + D'^T K, and the keys keep their io encoding (bf16 keys are
+// stored exactly, in half the bytes of fp32 sigma-scaled keys).
 //
 //   phase 1 (prefill_chunk_kernel): one workgroup per (request, value head,
 //     chunk) forms the decay products Gamma from a doubling table (lane
 //     shuffles), M from K K^T, T by forward substitution (each column held in
-//     registers by a quad of lanes), then W, U and Kt, and stores W [C][d_k],
-//     Kt^T [d_k][C], U^T [d_v][C] and g to the workspace.  The three
-//     products run on v_mfma_f32_16x16x4f32.  No division: products of alpha
-//     are formed directly, so alpha = 0 is exact.
+//     registers by a quad of lanes), then W and U, and stores W' [C][d_k],
+//     K^T [d_k][C] (io dtype), U'^T [d_v][C] and g to the workspace.  The
+//     three products run on v_mfma_f32_16x16x4f32.  No division: products of
+//     alpha are formed directly, so alpha = 0 is exact.
 //   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
-//     state rows; the row blocks of a head share one XCD) walks the chunks in order: X^T = W S^T, D^T = U^T - X^T,
-//     S^T <- g S^T + Kt^T D^T, on v_mfma_f32_16x16x4f32.  Wave w owns the
-//     state columns 16 w .. 16 w + 15 (a 16 x 16 fp32 accumulator tile that
-//     never leaves registers); the contraction orders are chosen so that the
-//     tile is directly the B operand of the next chunk's X and X's output is
-//     directly the B operand of the update.  The partial X of the waves are
-//     summed through LDS.
+//     state rows; the row blocks of a head share one XCD) walks the chunks in
+//     order: X^T = W' S^T, D'^T = U'^T - X^T, S^T <- g S^T + K^T D'^T, on
+//     v_mfma_f32_16x16x4f32.  Wave w owns the state columns 16 w .. 16 w + 15
+//     (a 16 x 16 fp32 accumulator tile that never leaves registers); the
+//     contraction orders are chosen so that the tile is directly the B
+//     operand of the next chunk's X and X's output is directly the B operand
+//     of the update.  The partial X of the waves are summed through LDS by the
+//     wave that forms the D' tile, so each U' tile is read by one wave only.
 // A ragged last chunk is padded with alpha = 1, beta = 0, k = v = 0, which
 // leaves the state unchanged.
 #include <type_traits>
@@ -49,9 +54,9 @@ struct PrefillParams {
   const float* alpha; // [R][P][HV]
   const float* beta;
   float* s_out;       // [R][HV][DV][DK]
-  float* wb;          // [R*HV][nch][C][DK]
-  float* ktb;         // [R*HV][nch][DK][C]
-  float* utb;         // [R*HV][nch][DV][C]
+  float* wb;          // [R*HV][nch][C][DK]   W' = diag(sigma) W
+  void* ktb;          // [R*HV][nch][DK][C]   K^T, io dtype
+  float* utb;         // [R*HV][nch][DV][C]   U'^T = (diag(sigma) U)^T
   float* gb;          // [R*HV][nch]
   int HK, HV, P, nch;
   int xcd_map;  // phase 2: all row blocks of a unit on one XCD (units % 8 == 0)
@@ -235,12 +240,15 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   __syncthreads();
 
   const long cu = long(unit) * p.nch + c;
-  // W = T diag(beta gamma) K -> wb [C][DK];  Kt^T = (diag(sigma) K)^T -> ktb [DK][C]
+  // W' = diag(sigma) T diag(beta gamma) K -> wb [C][DK];  K^T -> ktb [DK][C] in the io
+  // dtype (the keys' own bits: bf16 keys stay exact)
   float* wdst = p.wb + cu * kC * DK;
-  float* ktdst = p.ktb + cu * DK * kC;
   for (int i = tid; i < kC * DK; i += kP1Threads) {
     const int kk = i / kC, t = i - kk * kC;
-    ktdst[i] = sh.sig[t] * sh.K[t][kk];
+    if constexpr (BF16)
+      static_cast<__bf16*>(p.ktb)[cu * DK * kC + i] = static_cast<__bf16>(sh.K[t][kk]);
+    else
+      static_cast<float*>(p.ktb)[cu * DK * kC + i] = sh.K[t][kk];
   }
   // (T is lower triangular: row block a needs k < 16 (a + 1))
   constexpr int NBW = DK / 16;
@@ -255,9 +263,13 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
       }
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wdst[(16 * a + 4 * l4 + q) * DK + 16 * b + l16] = acc[q];
+    for (int q = 0; q < 4; ++q) {
+      const int t = 16 * a + 4 * l4 + q;
+      wdst[t * DK + 16 * b + l16] = sh.sig[t] * acc[q];
+    }
   }
-  // U = T diag(beta) V -> utb [DV][C] (4 consecutive tokens per lane and tile)
+  // U' = diag(sigma) T diag(beta) V -> utb [DV][C] (4 consecutive tokens per lane and
+  // tile)
   float* udst = p.utb + cu * DV * kC;
   constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
   constexpr int NBU = VC / 16;
@@ -276,7 +288,8 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
           acc = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc);
         }
       }
-      *reinterpret_cast<f32x4*>(udst + (cb + 16 * b + l16) * kC + 16 * a + 4 * l4) = acc;
+      const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
+      *reinterpret_cast<f32x4*>(udst + (cb + 16 * b + l16) * kC + 16 * a + 4 * l4) = sg * acc;
     }
     __syncthreads();
   }
@@ -286,16 +299,30 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
 // ---- phase 2 ----------------------------------------------------------------
 
 // Operands of one chunk for one lane (see prefill_scan_kernel).
+// Operands of one chunk for one lane (see prefill_scan_kernel).  The keys
+// stay in their io encoding until they are used, so that a load issued for a
+// later chunk is not waited for early.
+template <bool BF16, int NU>
 struct ScanOps {
-  f32x4 w[4], k[4], u[4];
+  f32x4 w[4], u[NU];
+  typename std::conditional<BF16, uint2, f32x4>::type k[4];
   float g;
+  __device__ float key(int mt, int j) const {
+    if constexpr (BF16) {
+      const unsigned h = j < 2 ? k[mt].x : k[mt].y;
+      return __uint_as_float((j & 1) ? (h & 0xffff0000u) : (h << 16));
+    } else {
+      return k[mt][j];
+    }
+  }
 };
 
-template <int DK, int DV>
+template <int DK, int DV, bool BF16>
 __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   constexpr int NW = DK / 16;  // waves: state columns 16 w .. 16 w + 15
+  constexpr int NU = (4 + NW - 1) / NW;  // D tiles a wave forms (tiles w, w + NW, ..)
   __shared__ f32x4 xp[NW][4][64];  // partial X^T tiles of every wave
-  __shared__ f32x4 xs[4][64];      // their sums
+  __shared__ f32x4 ds[4][64];      // D'^T tiles: U'^T minus the sums of the partials
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   // The DV / 16 row blocks of a (request, value head) read the same W and
   // Kt of every chunk.  Workgroups are dispatched round-robin over the 8
@@ -322,23 +349,32 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   }
   // Loads are unconditional (past the end they re-read the last chunk) so
   // the compiler can count them and wait only for the set about to be used.
-  auto load = [&](int c, ScanOps& o) {
+  auto load = [&](int c, ScanOps<BF16, NU>& o) {
     const long cu = long(unit) * p.nch + (c < p.nch ? c : p.nch - 1);
     const float* wc = p.wb + cu * kC * DK;
-    const float* kt = p.ktb + cu * DK * kC;
+    const void* kt = static_cast<const char*>(p.ktb) + cu * DK * kC * (BF16 ? 2 : 4);
     const float* ut = p.utb + cu * DV * kC;
     o.g = p.gb[cu];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       // A of X: W(t = 16 mt + lr, k = 16 w + 4 lq + i), i = 0..3
       o.w[mt] = *reinterpret_cast<const f32x4*>(wc + (16 * mt + lr) * DK + 16 * w + 4 * lq);
-      // A of the update: Kt^T(k = 16 w + lr, t = 16 mt + 4 lq + j), j = 0..3
-      o.k[mt] = *reinterpret_cast<const f32x4*>(kt + (16 * w + lr) * kC + 16 * mt + 4 * lq);
-      // U^T(row0 + lr, t = 16 mt + 4 lq + j)
-      o.u[mt] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
+      // A of the update: K^T(k = 16 w + lr, t = 16 mt + 4 lq + j), j = 0..3
+      const long ko = (16 * w + lr) * kC + 16 * mt + 4 * lq;
+      if constexpr (BF16)
+        o.k[mt] = *reinterpret_cast<const uint2*>(static_cast<const __bf16*>(kt) + ko);
+      else
+        o.k[mt] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(kt) + ko);
+    }
+    // U'^T(row0 + lr, t = 16 mt + 4 lq + j) of the tiles this wave forms (a wave
+    // without one re-reads tile 3)
+#pragma unroll
+    for (int i = 0; i < NU; ++i) {
+      const int mt = w + NW * i < 4 ? w + NW * i : 3;
+      o.u[i] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
     }
   };
-  auto step = [&](int c, const ScanOps& o) {
+  auto step = [&](int c, const ScanOps<BF16, NU>& o) {
     if (c >= p.nch) return;
     // partial X^T(t, n) over this wave's 16 state columns
 #pragma unroll
@@ -350,31 +386,38 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
       xp[w][mt][lane] = acc;
     }
     __syncthreads();
-    for (int mt = w; mt < 4; mt += NW) {  // wave w sums tiles w, w + NW, .. over the waves
-      f32x4 x = xp[0][mt][lane];
+    // wave w forms the tiles w, w + NW, .. of
+    // D'^T(t = 16 mt + 4 lq + j, n = lr) = U'^T - sum over the waves of X^T
 #pragma unroll
-      for (int v = 1; v < NW; ++v) x += xp[v][mt][lane];
-      xs[mt][lane] = x;
+    for (int i = 0; i < NU; ++i) {
+      const int mt = w + NW * i;
+      if (mt < 4) {
+        f32x4 x = xp[0][mt][lane];
+#pragma unroll
+        for (int v = 1; v < NW; ++v) x += xp[v][mt][lane];
+        ds[mt][lane] = o.u[i] - x;
+      }
     }
     __syncthreads();
-    // D^T(t = 16 mt + 4 lq + j, n = lr) = U^T - X^T
-    f32x4 dt[4];
+    // S^T <- g S^T + K^T D'^T: one independent chain per token block, summed
+    f32x4 up[4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) dt[mt] = o.u[mt] - xs[mt][lane];
-    // S^T <- g S^T + Kt^T D^T
-    st *= o.g;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < 4; ++mt) {
+      const f32x4 d = ds[mt][lane];
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        st = __builtin_amdgcn_mfma_f32_16x16x4f32(o.k[mt][j], dt[mt][j], st, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(o.key(mt, j), d[j], acc, 0, 0, 0);
+      up[mt] = acc;
+    }
+    st = o.g * st + ((up[0] + up[1]) + (up[2] + up[3]));
   };
   // Three operand sets in flight: chunk c + 2 is requested before chunk c is
-  // processed.  (xp and xs are rewritten only after the next chunk's first
+  // processed.  (xp and ds are rewritten only after the next chunk's first
   // barrier, which every wave reaches after reading them.)
   // The scheduling barriers keep every load group in program order, so the
   // wait before a step covers only its own (oldest) group.
-  ScanOps a, b, c3;
+  ScanOps<BF16, NU> a, b, c3;
   load(0, a);
   load(1, b);
   for (int c = 0; c < p.nch; c += 3) {
@@ -407,7 +450,7 @@ hipError_t launch_t(const Shape& s, const PrefillParams& prm, hipStream_t st) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  prefill_scan_kernel<DK, DV><<<units * unsigned(DV / 16), 4 * DK, 0, st>>>(prm);
+  prefill_scan_kernel<DK, DV, BF16><<<units * unsigned(DV / 16), 4 * DK, 0, st>>>(prm);
   return hipGetLastError();
 }
 
@@ -438,8 +481,9 @@ hipError_t launch_prefill_chunked(const Shape& s, int prompt_len, const void* k,
   prm.xcd_map = units % 8 == 0 ? 1 : 0;
   float* base = static_cast<float*>(workspace);
   prm.wb = base;
-  prm.ktb = prm.wb + units * nch * kC * s.dk;
-  prm.utb = prm.ktb + units * nch * kC * s.dk;
+  float* const kt_base = prm.wb + units * nch * kC * s.dk;  // K^T region (fp32-sized)
+  prm.ktb = kt_base;
+  prm.utb = kt_base + units * nch * kC * s.dk;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   prm.gb = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                     up(units * nch * size_t(kC) * (2 * s.dk + s.dv) * 4));
