@@ -114,14 +114,26 @@ __device__ inline void fill_rows(float* dst, const void* src, int n, int c0, Row
 
 // ---- phase 1 ----------------------------------------------------------------
 
-template <int DK>
+// Rows are padded to a multiple of 4 words plus 4 (bf16 keys: 8 elements), so
+// that the 16 rows x 4 columns an MFMA operand read touches fall in distinct
+// banks.  bf16 keys stay in their encoding (exact, half the space), which lets
+// two workgroups share a CU.
+template <int DK, bool BF16>
 struct P1Shared {
-  float K[kC][DK + 1];    // the chunk's keys, fp32 (padding rows zero)
-  float T[kC][kC + 1];    // (I + M)^{-1}
-  float M[kC][kC + 1];
-  float X[kC][128 + 1];   // a 128-column block of beta V
+  using KT = typename std::conditional<BF16, uint16_t, float>::type;
+  static constexpr int KLD = BF16 ? DK + 8 : DK + 4;
+  KT K[kC][KLD];          // the chunk's keys (padding rows zero)
+  float T[kC][kC + 4];    // (I + M)^{-1}
+  union {
+    float M[kC][kC + 4];  // until T is formed
+    float X[kC][128 + 4]; // then a 128-column block of beta V
+  };
   float P[7][kC];         // P[k][t]: product of the 2^k decays ending at token t
   float al[kC], be[kC], gam[kC], sig[kC];
+  __device__ float key(int t, int c) const {
+    if constexpr (BF16) return __uint_as_float(unsigned(K[t][c]) << 16);
+    else return K[t][c];
+  }
 };
 
 // alpha_{i+1} ... alpha_t (t - i >= 0 factors; none: 1) from the doubling
@@ -159,7 +171,8 @@ __device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
 template <int DK, int DV, bool BF16>
 __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
-  P1Shared<DK>& sh = *reinterpret_cast<P1Shared<DK>*>(smem);
+  using Sh = P1Shared<DK, BF16>;
+  Sh& sh = *reinterpret_cast<Sh*>(smem);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, l4 = lane >> 4;
   const int c = blockIdx.x % p.nch, unit = blockIdx.x / p.nch;
@@ -168,9 +181,27 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   const int n = min(kC, p.P - t0);
   const long tok0 = long(r) * p.P + t0;
 
-  fill_rows<DK, DK + 1, BF16>(&sh.K[0][0], p.k, n, 0,
-                               [&](int t) { return ((tok0 + t) * p.HK + hk) * DK; },
-                               [](int) { return 1.f; });
+  if constexpr (BF16) {  // raw 16-byte copies of the key rows (zero past the prompt)
+    constexpr int NV = kC * DK / 8, PER = (NV + kP1Threads - 1) / kP1Threads;
+    uint4 buf[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int vi = tid + q * kP1Threads, t = vi / (DK / 8), cc = (vi - t * (DK / 8)) * 8;
+      buf[q] = make_uint4(0u, 0u, 0u, 0u);
+      if (vi < NV && t < n)
+        buf[q] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.k) +
+                                                 ((tok0 + t) * p.HK + hk) * DK + cc);
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int vi = tid + q * kP1Threads, t = vi / (DK / 8), cc = (vi - t * (DK / 8)) * 8;
+      if (vi < NV) *reinterpret_cast<uint4*>(&sh.K[t][cc]) = buf[q];
+    }
+  } else {
+    fill_rows<DK, Sh::KLD, false>(&sh.K[0][0], p.k, n, 0,
+                                  [&](int t) { return ((tok0 + t) * p.HK + hk) * DK; },
+                                  [](int) { return 1.f; });
+  }
   if (tid < kC) {
     const bool in = tid < n;
     const float al = in ? p.alpha[(tok0 + tid) * p.HV + hv] : 1.f;
@@ -201,10 +232,12 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   // tiles on or below the diagonal of K K^T
   for (int x = w; x < 10; x += 4) {
     const int a = (x >= 1) + (x >= 3) + (x >= 6), b = x - a * (a + 1) / 2;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc4[4] = {};  // four independent chains over the key dimension
 #pragma unroll 8
     for (int ks = 0; ks < DK / 4; ++ks)
-      acc = mfma4(sh.K[16 * a + l16][4 * ks + l4], sh.K[16 * b + l16][4 * ks + l4], acc);
+      acc4[ks & 3] = mfma4(sh.key(16 * a + l16, 4 * ks + l4), sh.key(16 * b + l16, 4 * ks + l4),
+                           acc4[ks & 3]);
+    const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int t = 16 * a + 4 * l4 + q, i = 16 * b + l16;
@@ -223,14 +256,10 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
     for (int m = 0; m < kC / 4; ++m) x[m] = 0.f;
 #pragma unroll
     for (int t = 0; t < kC; ++t) {
-      float s0 = 0.f, s1 = 0.f;  // rows not computed yet hold 0
+      float sp[4] = {0.f, 0.f, 0.f, 0.f};  // rows not computed yet hold 0
 #pragma unroll
-      for (int m = 0; m < (t + 3) / 4; ++m) {
-        const float mv = sh.M[t][sub + 4 * m];
-        if (m & 1) s1 = fmaf(mv, x[m], s1);
-        else s0 = fmaf(mv, x[m], s0);
-      }
-      const float s = quad_sum(s0 + s1);
+      for (int m = 0; m < (t + 3) / 4; ++m) sp[m & 3] = fmaf(sh.M[t][sub + 4 * m], x[m], sp[m & 3]);
+      const float s = quad_sum((sp[0] + sp[1]) + (sp[2] + sp[3]));
       const float val = t == j ? 1.f : (t > j ? -s : 0.f);
       if (sub == (t & 3)) x[t >> 2] = val;
     }
@@ -246,7 +275,7 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   for (int i = tid; i < kC * DK; i += kP1Threads) {
     const int kk = i / kC, t = i - kk * kC;
     if constexpr (BF16)
-      static_cast<__bf16*>(p.ktb)[cu * DK * kC + i] = static_cast<__bf16>(sh.K[t][kk]);
+      static_cast<uint16_t*>(p.ktb)[cu * DK * kC + i] = sh.K[t][kk];
     else
       static_cast<float*>(p.ktb)[cu * DK * kC + i] = sh.K[t][kk];
   }
@@ -254,14 +283,16 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   constexpr int NBW = DK / 16;
   for (int x = w; x < 4 * NBW; x += 4) {
     const int a = x / NBW, b = x - a * NBW;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc4[4] = {};
     for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int kk = 4 * (ks + u) + l4;
-        acc = mfma4(sh.T[16 * a + l16][kk], sh.be[kk] * sh.gam[kk] * sh.K[kk][16 * b + l16], acc);
+        acc4[u] = mfma4(sh.T[16 * a + l16][kk], sh.be[kk] * sh.gam[kk] * sh.key(kk, 16 * b + l16),
+                        acc4[u]);
       }
     }
+    const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int t = 16 * a + 4 * l4 + q;
@@ -274,20 +305,21 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
   constexpr int NBU = VC / 16;
   for (int cb = 0; cb < DV; cb += VC) {
-    fill_rows<VC, 129, BF16>(&sh.X[0][0], p.v, n, cb,
+    fill_rows<VC, 128 + 4, BF16>(&sh.X[0][0], p.v, n, cb,
                              [&](int t) { return ((tok0 + t) * p.HV + hv) * DV; },
                              [&](int t) { return sh.be[t]; });
     __syncthreads();
     for (int x = w; x < 4 * NBU; x += 4) {
       const int a = x / NBU, b = x - a * NBU;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      f32x4 acc4[4] = {};
       for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int kk = 4 * (ks + u) + l4;
-          acc = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc);
+          acc4[u] = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc4[u]);
         }
       }
+      const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
       const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
       *reinterpret_cast<f32x4*>(udst + (cb + 16 * b + l16) * kC + 16 * a + 4 * l4) = sg * acc;
     }
@@ -440,7 +472,7 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
 template <int DK, int DV, bool BF16>
 hipError_t launch_t(const Shape& s, const PrefillParams& prm, hipStream_t st) {
   const unsigned units = unsigned(s.R * s.HV);
-  const size_t lds = sizeof(P1Shared<DK>);
+  const size_t lds = sizeof(P1Shared<DK, BF16>);
   auto k1 = prefill_chunk_kernel<DK, DV, BF16>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k1),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
