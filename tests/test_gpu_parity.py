@@ -275,6 +275,12 @@ WIDE = [
     W.WorkloadSpec("k256_v512_gqa", 1, 2, 4, 256, 512, 48, (32, 20, 32, 17), "bf16", "uniform",
                    seed=34),
     W.WorkloadSpec("k64_v64_f32", 2, 2, 4, 64, 64, 48, (24, 30, 24), "f32", "uniform", seed=35),
+    # every other compiled instance: small heads with bf16 io, d = 128 with fp32 io
+    W.WorkloadSpec("k32_v32_bf16", 2, 2, 4, 32, 32, 100, (40, 33, 40), "bf16", "zipf", 1.1,
+                   seed=36),
+    W.WorkloadSpec("k64_v64_bf16", 1, 2, 2, 64, 64, 70, (48, 17, 48), "bf16", "uniform", seed=37),
+    W.WorkloadSpec("k128_v128_f32", 1, 2, 2, 128, 128, 65, (36, 36, 20), "f32", "zipf", 1.5,
+                   seed=38),
 ]
 
 

@@ -91,7 +91,7 @@ def test_chunked_prefill_zero_decay_tokens():
 
 @pytest.mark.parametrize("dk,dv,io", [(128, 256, "bf16"), (128, 512, "bf16"), (256, 256, "bf16"),
                                        (256, 512, "bf16"), (32, 32, "f32"), (64, 64, "f32"),
-                                       (128, 128, "f32")])
+                                       (128, 128, "f32"), (32, 32, "bf16"), (64, 64, "bf16")])
 def test_chunked_prefill_geometries(dk, dv, io):
     spec = W.WorkloadSpec(f"pf_{dk}_{dv}", 2, 2, 4, dk, dv, 200, (8,), io, "uniform", seed=3)
     wl = W.make_workload(spec)
