@@ -20,8 +20,11 @@
 // stored split by step 0).  The difference is the order of dependencies:
 // the contraction S_ctx [q_t | k_t] needs no record, so after one barrier
 // (the B fragments of q_t and k_t staged in LDS) the MFMAs run while the
-// ancestral records are still arriving; the record dots follow, a second
-// barrier publishes the per-beam scalars, and the epilogue applies Eq. 4.
+// ancestral records are still arriving; the record dots follow.  As in the
+// input-record kernel, every load is made by the fold lanes of the beam as
+// whole lines: each lane forms sum_j w_j delta_j for both projections over its
+// value rows and stages them, with v_t, in LDS; a second barrier publishes
+// them, and the epilogue applies Eq. 4 in the MFMA output layout.
 //
 // delta is stored in fp16 for bf16 inputs (fp32 for fp32 inputs): the paper's
 // record is a 32-bit decay with 16-bit delta and key vectors; bf16 would cost
@@ -95,6 +98,8 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   constexpr int LPB = NT / BEAMS;    // fold lanes per beam
   constexpr int EPL = DK / LPB;      // key elements per fold lane
   constexpr int C8 = EPL / 8;
+  constexpr int VPL = DVW / LPB;     // value rows per fold lane
+  constexpr int VS = DVW + 4;        // padded LDS row per beam
   constexpr int KS = DK / 32;
   constexpr int NA = CHAIN - 1;
   constexpr int NAX = NA > 0 ? NA : 1;
@@ -102,10 +107,12 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   constexpr int HL = BF16 ? 1 : 2;   // bf16 inputs are exact in bf16: no low half
   static_assert(MB * DK == DVW && NS * DVW == DV && EPL % 8 == 0, "tiling");
   static_assert(LPB <= 64 && (LPB & (LPB - 1)) == 0, "fold lane group within a wave");
+  static_assert(VPL == 8 || VPL == 16, "fold lanes own 8 or 16 value rows");
 
   __shared__ uint4 b_lds[2][HL][NBLK][KS][4][16];  // [q | k_t][hi | lo] B fragments
-  constexpr int NSC = 4 + 2 * NAX;
-  __shared__ float sc_lds[BEAMS][NSC];             // decay, alpha_t, beta_t, k_t.q, w_q[], w_k[]
+  __shared__ float sc_lds[BEAMS][4];               // decay, alpha_t, beta_t, k_t.q
+  // per beam and row of this slice: sum_j w_q,j delta_j, sum_j w_k,j delta_j, v_t
+  __shared__ float rq_lds[BEAMS][VS], rk_lds[BEAMS][VS], vt_lds[BEAMS][VS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -138,14 +145,10 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   const int fbeam = b0 + fb;
   const bool fvalid = fbeam < W;
   const int fbc = fvalid ? fbeam : 0;
+  const unsigned voff = (unsigned(DVW) * slice + unsigned(li) * VPL) * IOB;
   const int g4 = lane >> 4;
-  const unsigned row0 = DVW * slice + 16 * MB * w + RPL * g4;
-  int sbc[NBLK];
-#pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb) {
-    const int sb = b0 + nb * 16 + (lane & 15);
-    sbc[nb] = sb < W ? sb : 0;
-  }
+  const unsigned rloc = 16 * MB * w + RPL * g4;  // row within the slice
+  const unsigned row0 = DVW * slice + rloc;
 
   const int* anc_r = p.anc_rd + long(r) * wmax * tmax;
   const unsigned kslot = DK * IOB, vslot = DV * IOB;
@@ -160,35 +163,29 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   };
   auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
 
-  // ---- round 1: indices, then query and the beam's step-t inputs
-  int fsrc[NAX], ssrc[NBLK][NAX];
-  bool fpok = true, spok[NBLK];
-  int fpar = 0, spar[NBLK];
-#pragma unroll
-  for (int nb = 0; nb < NBLK; ++nb) spok[nb] = true;
+  // ---- round 1: indices, then query and the beam's step-t inputs.  Every
+  // load is made by the fold lanes of the beam, as whole lines (see the
+  // input-record kernel).
+  int fsrc[NAX];
+  bool fpok = true;
+  int fpar = 0;
   if constexpr (NA > 0) {
     if constexpr (FUSED) {
-      const int* prow = p.parents + long(r) * W;
-      fpar = prow[fbc];
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb) spar[nb] = prow[sbc[nb]];
+      fpar = p.parents[long(r) * W + fbc];
     } else {
 #pragma unroll
       for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-        for (int j = 0; j < NA; ++j) ssrc[nb][j] = anc_r[sbc[nb] * tmax + j];
     }
   }
   using K8 = RawV<BF16, 8>;
   using VR = RawV<BF16, RPL>;
+  using VL = RawV<BF16, VPL>;
   K8 qr[C8], kt[C8];
   K8 kr[NAX][C8];
   float alr[NAX];
   float2 abt;
-  VR vt[NBLK];
-  VR dr[NBLK][NAX];
+  VL vt;
+  VL dr[NAX];
   {
     const unsigned qoff = ((unsigned(r) * W + fbc) * p.HK + hk) * kslot + li * EPL * IOB;
 #pragma unroll
@@ -198,30 +195,27 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       for (int c = 0; c < C8; ++c) kt[c].load(p.k_in, qoff + c * K8::kBytes);
       const unsigned gi = (unsigned(r) * W + fbc) * p.HV + hv;
       abt = make_float2(p.alpha_in[gi], p.beta_in[gi]);
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb)
-        vt[nb].load(p.v_in, ((unsigned(r) * W + sbc[nb]) * p.HV + hv) * vslot + row0 * IOB);
+      vt.load(p.v_in, gi * vslot + voff);
     } else {
       const char* ks = k_slab(NA);
 #pragma unroll
       for (int c = 0; c < C8; ++c)
         kt[c].load(ks, fbc * kslot + li * EPL * IOB + c * K8::kBytes);
       abt = ab_slab(NA)[fbc];
-      const char* vs = v_slab(NA);
-#pragma unroll
-      for (int nb = 0; nb < NBLK; ++nb) vt[nb].load(vs, sbc[nb] * vslot + row0 * IOB);
+      vt.load(v_slab(NA), fbc * vslot + voff);
     }
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- ancestral records: keys and decays for the dots (fold lanes), delta
-  // rows for the epilogue.  FUSED: the parent's own step-(t-1) record first.
+  // ---- ancestral records: keys, decays and this lane's delta rows.  FUSED:
+  // the parent's own step-(t-1) record first.
   bool fok[NAX];
   auto load_rec = [&](int j, int slot) {
     const char* ks = k_slab(j);
 #pragma unroll
     for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
     alr[j] = ab_slab(j)[slot].x;
+    dr[j].load(d_slab(j), slot * vslot + voff);
   };
   if constexpr (FUSED && NA > 0) {
     fpok = unsigned(fpar) < unsigned(p.W_prev);
@@ -229,46 +223,20 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     fsrc[NA - 1] = pf;
     fok[NA - 1] = fpok;
     load_rec(NA - 1, pf);
-    int ps[NBLK];
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb) {
-      spok[nb] = unsigned(spar[nb]) < unsigned(p.W_prev);
-      ps[nb] = spok[nb] ? spar[nb] : 0;
-      ssrc[nb][NA - 1] = ps[nb];
-      dr[nb][NA - 1].load(d_slab(NA - 1), ps[nb] * vslot + row0 * IOB);
-    }
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA - 1; ++j) ssrc[nb][j] = anc_r[ps[nb] * tmax + j];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) {
       fok[j] = fpok && unsigned(fsrc[j]) < unsigned(wmax);
       load_rec(j, fok[j] ? fsrc[j] : 0);
     }
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA - 1; ++j) {
-        const bool ok = spok[nb] && unsigned(ssrc[nb][j]) < unsigned(wmax);
-        dr[nb][j].load(d_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
-      }
   } else {
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
       fok[j] = unsigned(fsrc[j]) < unsigned(wmax);
       load_rec(j, fok[j] ? fsrc[j] : 0);
     }
-#pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb)
-#pragma unroll
-      for (int j = 0; j < NA; ++j) {
-        const bool ok = unsigned(ssrc[nb][j]) < unsigned(wmax);
-        dr[nb][j].load(d_slab(j), (ok ? ssrc[nb][j] : 0) * vslot + row0 * IOB);
-      }
   }
 
   // ---- shared-state rows (A fragments), as in the input-record kernel
@@ -385,15 +353,36 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       cq[j] = group_sum<LPB>(a0 + a1);
       ck[j] = group_sum<LPB>(b0v + b1v);
     }
-    if (li == 0) {
-      float decay = 1.f;  // prod of the decays of records newer than j
+    // the record terms of both projections over this lane's rows:
+    // w_j = (k_j . x) * prod of the decays of records newer than j
+    float rq[VPL], rk[VPL];
 #pragma unroll
-      for (int j = NA - 1; j >= 0; --j) {
-        const float aj = fok[j] ? alr[j] : 1.f;
-        sc_lds[fb][4 + j] = fok[j] ? decay * cq[j] : 0.f;
-        sc_lds[fb][4 + NAX + j] = fok[j] ? decay * ck[j] : 0.f;
-        decay *= aj;
+    for (int e = 0; e < VPL; ++e) rq[e] = rk[e] = 0.f;
+    float decay = 1.f;
+#pragma unroll
+    for (int j = NA - 1; j >= 0; --j) {
+      const float wq = fok[j] ? decay * cq[j] : 0.f, wk = fok[j] ? decay * ck[j] : 0.f;
+      float dj[VPL];
+      delta_to_float<BF16>(dr[j].w, dj, VPL);
+#pragma unroll
+      for (int e = 0; e < VPL; ++e) {
+        rq[e] = fmaf(wq, dj[e], rq[e]);
+        rk[e] = fmaf(wk, dj[e], rk[e]);
       }
+      decay *= fok[j] ? alr[j] : 1.f;
+    }
+    float vf[VPL];
+    vt.to_float(vf);
+#pragma unroll
+    for (int e = 0; e < VPL; e += 4) {
+      *reinterpret_cast<float4*>(&rq_lds[fb][li * VPL + e]) =
+          make_float4(rq[e], rq[e + 1], rq[e + 2], rq[e + 3]);
+      *reinterpret_cast<float4*>(&rk_lds[fb][li * VPL + e]) =
+          make_float4(rk[e], rk[e + 1], rk[e + 2], rk[e + 3]);
+      *reinterpret_cast<float4*>(&vt_lds[fb][li * VPL + e]) =
+          make_float4(vf[e], vf[e + 1], vf[e + 2], vf[e + 3]);
+    }
+    if (li == 0) {
       sc_lds[fb][0] = decay;
       sc_lds[fb][1] = abt.x;
       sc_lds[fb][2] = abt.y;
@@ -433,25 +422,14 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     const int sb = b0 + bl;
     const float decay = sc_lds[bl][0], at_ = sc_lds[bl][1], bt = sc_lds[bl][2],
                 cqt = sc_lds[bl][3];
-    float uq[RPL], uk[RPL];
+    float uq[RPL], uk[RPL], vf[RPL];
 #pragma unroll
     for (int e = 0; e < RPL; ++e) {
-      uq[e] = decay * accq[nb][e >> 2][e & 3];
-      uk[e] = decay * acck[nb][e >> 2][e & 3];
+      uq[e] = fmaf(decay, accq[nb][e >> 2][e & 3], rq_lds[bl][rloc + e]);
+      uk[e] = fmaf(decay, acck[nb][e >> 2][e & 3], rk_lds[bl][rloc + e]);
+      vf[e] = vt_lds[bl][rloc + e];
     }
-#pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      const float wq = sc_lds[bl][4 + j], wk = sc_lds[bl][4 + NAX + j];
-      float dj[RPL];
-      delta_to_float<BF16>(dr[nb][j].w, dj, RPL);
-#pragma unroll
-      for (int e = 0; e < RPL; ++e) {
-        uq[e] = fmaf(wq, dj[e], uq[e]);
-        uk[e] = fmaf(wk, dj[e], uk[e]);
-      }
-    }
-    float vf[RPL], dt[RPL], ov[RPL];
-    vt[nb].to_float(vf);
+    float dt[RPL], ov[RPL];
 #pragma unroll
     for (int e = 0; e < RPL; ++e) {
       dt[e] = bt * (vf[e] - at_ * uk[e]);
