@@ -157,6 +157,26 @@ def kernel_alg_bytes(wl, t, variant):
     return fused_alg_bytes(wl, t, borrow=variant == "borrow")
 
 
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32
+
+
+def prefill_chunked_flops(spec):
+    """fp32 flops of onela_prefill_state_chunked as implemented: per chunk of
+    C = 64 tokens and (request, value head), the lower ten of the sixteen
+    16 x 16 tiles of K K^T, the two products with the unit lower-triangular T
+    (row block a needs k < 16 (a + 1): 10/16 of the dense product), then the
+    scan's X = W' S^T and K^T D' over the whole chunk."""
+    C = 64
+    nch = -(-spec.P // C)
+    tri = 10 / 16
+    per_chunk = (2 * C * C * spec.dk * tri          # K K^T
+                 + 2 * C * C * spec.dk * tri        # T (diag(beta gamma) K)
+                 + 2 * C * C * spec.dv * tri        # T (diag(beta) V)
+                 + 2 * C * spec.dk * spec.dv        # W' S^T
+                 + 2 * C * spec.dk * spec.dv)       # K^T D'
+    return spec.R * spec.HV * nch * per_chunk
+
+
 def step_alg_bytes(wl, fused=True, variant="borrow"):
     """Algorithmic bytes of one whole step (T decode steps; init moves none)."""
     s = wl.spec
@@ -508,11 +528,19 @@ def main():
         seq_ms = time_ms(lambda: ab.onela_prefill_state(cfg_p, spec.P, *dw0.prompt, s_tmp), 3)
         chk_ms = time_ms(lambda: ab.onela_prefill_state_chunked(cfg_p, spec.P, *dw0.prompt, s_tmp,
                                                                 pf_ws, pf_bytes), 10)
+        flops = prefill_chunked_flops(spec)
         result["prefill"] = {
             "prompt_tokens": spec.P, "requests": spec.R,
             "sequential_ms": seq_ms, "chunked_ms": chk_ms,
             "chunked_tokens_per_s": spec.R * spec.P / (chk_ms / 1e3),
             "chunked_workspace_bytes": pf_bytes,
+            "roofline": {"bound": "mfma", "achieved": flops / (chk_ms / 1e3) / 1e12,
+                         "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": flops / (chk_ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS,
+                         "flops": flops,
+                         "count": "the fp32 products of the chunked method as computed: "
+                                  "K K^T, T.(diag(beta gamma) K), T.(diag(beta) V) per "
+                                  "chunk, W' S^T and K^T D' per chunk and 16-row block"},
             "note": "onela_prefill_state (token by token) vs onela_prefill_state_chunked "
                     "(64-token chunks); setup work, not part of `value`"}
         log(f"[bench] prefill {spec.P} tokens: sequential {seq_ms:.2f} ms, chunked {chk_ms:.3f} ms")
