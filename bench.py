@@ -13,7 +13,8 @@ Inputs are resident in HBM when timing starts: the bench keeps ``--batches``
 independent copies of every input, workspace and output, and step i uses
 batch i % batches, so a batch's data was last touched far more than the
 256 MiB Infinity Cache ago.  Timed steps are replayed from HIP graphs (one
-captured graph per batch) so host launch cost does not pace the GPU.
+captured graph per batch, and one per run of ``--graph-group`` consecutive
+batches) so host launch cost does not pace the GPU.
 
 Printed: one JSON line with the whole-job throughput (beam-tokens/s), the
 per-kernel roofline of the fused step kernel (algorithmic bytes / average
@@ -241,6 +242,8 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--batches", type=int, default=32)
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--graph-group", type=int, default=8,
+                    help="consecutive batches captured into one graph (1: one graph per step)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--skip-fullstate", action="store_true")
@@ -323,19 +326,34 @@ def main():
         torch.cuda.synchronize()
         return g
 
+    G = max(1, min(args.graph_group, NB))
+
     def timed_steps(fused, K, warmup, kind):
-        """Exactly K steps (step i on batch i % NB); returns ms per step."""
-        graphs = None
+        """Exactly K steps (step i on batch i % NB); returns ms per step.
+        Batches G*g .. G*g + G - 1 are also captured into one graph, replayed
+        when a run of G steps starts at such a batch, so that the per-graph
+        launch cost is paid once per G steps."""
+        graphs = groups = None
         if not args.no_graph:
             graphs = [capture(lambda b=b: one_step(b, fused, kind)) for b in batches]
+            if G > 1:
+                groups = [capture(lambda g=g: [one_step(batches[k], fused, kind)
+                                               for k in range(G * g, G * g + G)])
+                          for g in range(NB // G)]
 
         def run(n, start):
-            for i in range(n):
+            i = 0
+            while i < n:
                 k = (start + i) % NB
-                if graphs is not None:
-                    graphs[k].replay()
-                else:
+                if graphs is None:
                     one_step(batches[k], fused, kind)
+                    i += 1
+                elif groups is not None and k % G == 0 and k + G <= NB and n - i >= G:
+                    groups[k // G].replay()
+                    i += G
+                else:
+                    graphs[k].replay()
+                    i += 1
 
         run(warmup, 0)
         torch.cuda.synchronize()
@@ -444,7 +462,7 @@ def main():
                                "delta": "(alpha, delta fp16, k) transition records"}[kind],
                    "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
                                   "fp32 accum",
-                   "variant": kind, "graph": not args.no_graph, "batches": NB},
+                   "variant": kind, "graph": not args.no_graph, "graph_group": G, "batches": NB},
         "decode_step_us": {"per_t": [round(float(x), 3) for x in dec_us],
                            "mean": round(float(dec_us.mean()), 3)},
         "beam_tokens_per_step": beam_tokens_per_step,

@@ -72,6 +72,9 @@
 namespace onela {
 namespace {
 
+// Ancestry entries (previous beams x steps <= t-2) a fused step at t >= 2
+// stages in LDS; larger tables are read row by row from global memory.
+constexpr int kAncTable = 2048;
 
 struct DecodeParams {
   const void* q;
@@ -129,6 +132,11 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
 
   __shared__ uint4 p_lds[2][NBLK][KS][4][16];  // folded queries, B-fragment order
   __shared__ float v_lds[BEAMS][VS];           // sum_j g_j v_j per beam, this slice's rows
+  // FUSED, t >= 2: columns 0..t-2 of the request's h_{t-1}, all previous beams
+  constexpr bool kTab = FUSED && NA >= 2;
+  constexpr int NL = NT < 256 ? NT : 256;      // table-loading threads (at most 4 waves)
+  constexpr int NTV = kAncTable / NL;          // table entries per loading lane
+  __shared__ int anc_lds[kTab ? kAncTable : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -225,6 +233,27 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
       for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
     }
   }
+  // FUSED, t >= 2: the ancestry rows of all previous beams (their first t-1
+  // entries, when they fit kAncTable) are loaded by the first four waves
+  // right behind the parent indices and staged in LDS, so that the records
+  // of steps <= t-2 are addressed as soon as a beam's parent is known rather
+  // than one dependent memory round trip later.  Only the first wave of each
+  // SIMD loads: the second receives its data about one round trip later.
+  const int ntab = kTab ? p.W_prev * (NA - 1) : 0;
+  const bool tab = kTab && ntab <= kAncTable;
+  int tv[kTab ? NTV : 1];
+  if constexpr (kTab) {
+    if (tab && tid < NL) {
+#pragma unroll
+      for (int i = 0; i < NTV; ++i)
+        if (i * NL < ntab) {
+          const int e = tid + NL * i;
+          const int ec = e < ntab ? e : 0;
+          const int pb = ec / (NA - 1);
+          tv[i] = anc_r[pb * tmax + (ec - pb * (NA - 1))];
+        }
+    }
+  }
 
   using K8 = RawV<BF16, 8>;
   using VR = RawV<BF16, VPL>;
@@ -252,6 +281,18 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     }
   }
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kTab) {
+    if (tab) {
+      if (tid < NL) {
+#pragma unroll
+        for (int i = 0; i < NTV; ++i) {
+          const int e = tid + NL * i;
+          if (i * NL < ntab && e < ntab) anc_lds[e] = tv[i];
+        }
+      }
+      __syncthreads();
+    }
+  }
 
   // ---- ancestral records.  DECODE: all of them once h_t is back.  FUSED:
   // the parent's own step-(t-1) record as soon as the parent index is back
@@ -272,8 +313,17 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
     fsrc[NA - 1] = pf;
     fok[NA - 1] = fpok;
     load_record(NA - 1, pf);
+    if (tab) {
 #pragma unroll
-    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+      for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_lds[pf * (NA - 1) + j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+      // The row is the last load issued, and the records below need it:
+      // wait here, inside the branch, so that the join does not make the
+      // staged-table path wait for the parent's record as well.
+      if constexpr (NA >= 2) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) {
