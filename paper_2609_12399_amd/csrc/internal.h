@@ -11,6 +11,9 @@ namespace onela {
 
 // Maximum records in one beam's chain (decode steps 0 .. kMaxSteps-1).
 constexpr int kMaxSteps = 8;
+// Ancestry entries (previous beams x steps <= t-2) a fused decode step at
+// t >= 2 stages in LDS; larger tables are read row by row from global memory.
+constexpr int kAncTable = 2048;
 
 // Decode tiling: 16-beam MFMA column blocks per workgroup.
 constexpr int kDecodeBeamBlocks = 2;

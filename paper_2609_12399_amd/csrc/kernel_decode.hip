@@ -72,9 +72,6 @@
 namespace onela {
 namespace {
 
-// Ancestry entries (previous beams x steps <= t-2) a fused step at t >= 2
-// stages in LDS; larger tables are read row by row from global memory.
-constexpr int kAncTable = 2048;
 
 struct DecodeParams {
   const void* q;
@@ -107,7 +104,7 @@ struct DecodeParams {
   int xcd_map;  // 1: XCD-aware block order (units % 8 == 0)
 };
 
-template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED>
+template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED, bool BORROW>
 __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   constexpr int MB = DVW / DK;       // 16-row MFMA blocks per wave
   constexpr int NS = DV / DVW;       // row slices (workgroups) per (request, head, tile)
@@ -141,6 +138,34 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+
+  // The arguments the first loads depend on, in scalar registers together:
+  // left alone, the compiler loads each in the basic block that first uses
+  // it, and the first memory requests wait for several dependent rounds of
+  // argument loads (about 0.2 us each).
+  // Fused with borrowed records: also the record pointers of the three
+  // latest ancestral steps (and with them the argument cache lines of the
+  // older ones), needed as soon as the parent is known.
+  constexpr int J1 = NA > 0 ? NA - 1 : 0, J2 = NA > 1 ? NA - 2 : J1, J3 = NA > 2 ? NA - 3 : J2;
+  if constexpr (FUSED && BORROW && NA > 0)
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.W_prev), "s"(p.parents),
+                 "s"(p.k_in), "s"(p.v_in), "s"(p.alpha_in), "s"(p.beta_in), "s"(p.bk[J1]),
+                 "s"(p.bv[J1]), "s"(p.balpha[J1]), "s"(p.bbeta[J1]), "s"(p.bk[J2]), "s"(p.bv[J2]),
+                 "s"(p.balpha[J2]), "s"(p.bbeta[J2]), "s"(p.bk[J3]), "s"(p.bv[J3]),
+                 "s"(p.balpha[J3]), "s"(p.bbeta[J3]));
+  else if constexpr (FUSED)
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.W_prev), "s"(p.parents),
+                 "s"(p.k_in), "s"(p.v_in), "s"(p.alpha_in), "s"(p.beta_in), "s"(p.anc_wr));
+  else if constexpr (BORROW)
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.bk[NA]),
+                 "s"(p.bv[NA]), "s"(p.balpha[NA]), "s"(p.bbeta[NA]), "s"(p.bw[NA]));
+  else
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.ak), "s"(p.av),
+                 "s"(p.ab));
 
   // A new beam search starts at step 0: no parent can be flagged yet, so the
   // step-0 launch zeroes the sticky status word.
@@ -187,18 +212,20 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   const unsigned kslot = DK * IOB, vslot = DV * IOB;
   // Record rows of step j: slot s of (r, j, head) at slab(j) + s * stride.
   // Arena: head-major slabs, stride one row.  Borrowed: the caller's step-j
-  // buffers, beam-major, stride one beam.
-  const bool borrow = p.borrow != 0;
+  // buffers, beam-major, stride one beam.  The storage is a template
+  // parameter so that each record's addresses are straight-line code, whose
+  // argument loads the compiler issues in one round.
+  constexpr bool borrow = BORROW;
   const unsigned kstride = borrow ? unsigned(p.HK) * kslot : kslot;
   const unsigned vstride = borrow ? unsigned(p.HV) * vslot : vslot;
   auto k_slab = [&](int j) -> char* {
-    if (borrow)
+    if constexpr (borrow)
       return const_cast<char*>(static_cast<const char*>(p.bk[j])) +
              (long(r) * p.bw[j] * p.HK + hk) * long(kslot);
     return static_cast<char*>(p.ak) + ((long(r) * tmax + j) * p.HK + hk) * wmax * long(kslot);
   };
   auto v_slab = [&](int j) -> char* {
-    if (borrow)
+    if constexpr (borrow)
       return const_cast<char*>(static_cast<const char*>(p.bv[j])) +
              (long(r) * p.bw[j] * p.HV + hv) * long(vslot);
     return static_cast<char*>(p.av) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
@@ -206,10 +233,11 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
   // slot bound of step j's records (borrowed buffers hold exactly w[j] beams)
   auto slot_ok = [&](int j, int sl) {
-    return unsigned(sl) < unsigned(borrow ? p.bw[j] : wmax);
+    if constexpr (borrow) return unsigned(sl) < unsigned(p.bw[j]);
+    return unsigned(sl) < unsigned(wmax);
   };
   auto load_ab = [&](int j, int slot) -> float2 {
-    if (borrow) {
+    if constexpr (borrow) {
       const long i = (long(r) * p.bw[j] + slot) * p.HV + hv;
       return make_float2(p.balpha[j][i], p.bbeta[j][i]);
     }
@@ -518,14 +546,14 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
   }
 }
 
-template <int DK, int DV, int DVW, bool BF16, bool FUSED>
+template <int DK, int DV, int DVW, bool BF16, bool FUSED, bool BORROW>
 hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hipStream_t st) {
   constexpr int NBLK = kDecodeBeamBlocks;
   constexpr int threads = 4 * DK;
   switch (chain) {
-#define ONELA_CHAIN_CASE(C)                                                              \
-  case C:                                                                               \
-    decode_kernel<DK, DV, DVW, NBLK, C, BF16, FUSED><<<blocks, threads, 0, st>>>(prm);  \
+#define ONELA_CHAIN_CASE(C)                                                                      \
+  case C:                                                                                       \
+    decode_kernel<DK, DV, DVW, NBLK, C, BF16, FUSED, BORROW><<<blocks, threads, 0, st>>>(prm);  \
     break;
     ONELA_CHAIN_CASE(1)
     ONELA_CHAIN_CASE(2)
@@ -542,6 +570,12 @@ hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hip
   return hipGetLastError();
 }
 
+template <int DK, int DV, int DVW, bool BF16, bool FUSED>
+hipError_t launch_storage(int chain, const DecodeParams& prm, unsigned blocks, hipStream_t st) {
+  return prm.borrow ? launch_chain<DK, DV, DVW, BF16, FUSED, true>(chain, prm, blocks, st)
+                    : launch_chain<DK, DV, DVW, BF16, FUSED, false>(chain, prm, blocks, st);
+}
+
 // Supported (d_k, d_v) pairs and the state rows one workgroup covers:
 // DVW = min(d_v, 256) rows in 16*MB-row blocks per wave, MB = DVW / d_k.
 template <bool FUSED>
@@ -551,13 +585,13 @@ hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsign
 #define ONELA_SHAPE(DK, DV, DVW)                                                          \
   if (s.dk == DK && s.dv == DV) {                                                        \
     const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
-    return s.bf16 ? launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st)      \
-                  : launch_chain<DK, DV, DVW, false, FUSED>(chain, prm, blocks, st);    \
+    return s.bf16 ? launch_storage<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st)    \
+                  : launch_storage<DK, DV, DVW, false, FUSED>(chain, prm, blocks, st);  \
   }
 #define ONELA_SHAPE_BF16(DK, DV, DVW)                                                     \
   if (s.dk == DK && s.dv == DV && s.bf16) {                                              \
     const unsigned blocks = units * unsigned(DV / DVW) * unsigned(prm.ntiles);            \
-    return launch_chain<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st);               \
+    return launch_storage<DK, DV, DVW, true, FUSED>(chain, prm, blocks, st);             \
   }
   ONELA_SHAPE(32, 32, 32)
   ONELA_SHAPE(64, 64, 64)

@@ -113,10 +113,26 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   __shared__ float sc_lds[BEAMS][4];               // decay, alpha_t, beta_t, k_t.q
   // per beam and row of this slice: sum_j w_q,j delta_j, sum_j w_k,j delta_j, v_t
   __shared__ float rq_lds[BEAMS][VS], rk_lds[BEAMS][VS], vt_lds[BEAMS][VS];
+  // FUSED, t >= 2: columns 0..t-2 of the request's h_{t-1}, all previous beams
+  constexpr bool kTab = FUSED && NA >= 2;
+  constexpr int NL = NT < 256 ? NT : 256;  // table-loading threads (at most 4 waves)
+  constexpr int NTV = kAncTable / NL;      // table entries per loading lane
+  __shared__ int anc_lds[kTab ? kAncTable : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
+  // the arguments the first loads depend on, in scalar registers together
+  // (one round of argument loads; see the input-record kernel)
+  if constexpr (FUSED)
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.W_prev), "s"(p.parents),
+                 "s"(p.k_in), "s"(p.v_in), "s"(p.alpha_in), "s"(p.beta_in), "s"(p.ak), "s"(p.ad),
+                 "s"(p.ab));
+  else
+    asm volatile("" ::"s"(p.ntiles), "s"(p.xcd_map), "s"(p.HK), "s"(p.HV), "s"(p.G), "s"(p.W),
+                 "s"(p.wmax), "s"(p.tmax), "s"(p.anc_rd), "s"(p.q), "s"(p.ak), "s"(p.av),
+                 "s"(p.ad), "s"(p.ab));
   if constexpr (NA == 0) {
     if (blockIdx.x == 0 && tid == 0) p.status[0] = 0;
   }
@@ -177,6 +193,23 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       for (int j = 0; j < NA; ++j) fsrc[j] = anc_r[fbc * tmax + j];
     }
   }
+  // FUSED, t >= 2: the previous beams' ancestry rows staged in LDS by the
+  // first four waves (as in the input-record kernel).
+  const int ntab = kTab ? p.W_prev * (NA - 1) : 0;
+  const bool tab = kTab && ntab <= kAncTable;
+  int tv[kTab ? NTV : 1];
+  if constexpr (kTab) {
+    if (tab && tid < NL) {
+#pragma unroll
+      for (int i = 0; i < NTV; ++i)
+        if (i * NL < ntab) {
+          const int e = tid + NL * i;
+          const int ec = e < ntab ? e : 0;
+          const int pb = ec / (NA - 1);
+          tv[i] = anc_r[pb * tmax + (ec - pb * (NA - 1))];
+        }
+    }
+  }
   using K8 = RawV<BF16, 8>;
   using VR = RawV<BF16, RPL>;
   using VL = RawV<BF16, VPL>;
@@ -206,6 +239,18 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     }
   }
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kTab) {
+    if (tab) {
+      if (tid < NL) {
+#pragma unroll
+        for (int i = 0; i < NTV; ++i) {
+          const int e = tid + NL * i;
+          if (i * NL < ntab && e < ntab) anc_lds[e] = tv[i];
+        }
+      }
+      __syncthreads();
+    }
+  }
 
   // ---- ancestral records: keys, decays and this lane's delta rows.  FUSED:
   // the parent's own step-(t-1) record first.
@@ -223,8 +268,15 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     fsrc[NA - 1] = pf;
     fok[NA - 1] = fpok;
     load_rec(NA - 1, pf);
+    if (tab) {
 #pragma unroll
-    for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+      for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_lds[pf * (NA - 1) + j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NA - 1; ++j) fsrc[j] = anc_r[pf * tmax + j];
+      // wait inside the branch (see the input-record kernel)
+      if constexpr (NA >= 2) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NA - 1; ++j) {
