@@ -31,15 +31,17 @@ import sys
 from collections import defaultdict
 
 DECODE_RE = re.compile(r"decode_kernel<(\d+), (\d+), (\d+), (\d+), (\d+), (true|false), "
-                       r"(true|false)>")
+                       r"(true|false)(?:, (true|false))?>")
 
 
 def short_name(name: str) -> str:
     m = DECODE_RE.search(name)
     if m:
-        dk, dv, mb, nblk, chain, bf16, fused = m.groups()
+        dk, dv, mb, nblk, chain, bf16, fused, borrow = m.groups()
         mode = "fused" if fused == "true" else "decode"
-        return f"decode_kernel<{mode}, d={dk}, chain={chain}, {'bf16' if bf16 == 'true' else 'f32'}>"
+        records = "" if borrow is None else (", borrowed" if borrow == "true" else ", arena")
+        return (f"decode_kernel<{mode}, d={dk}, chain={chain}, "
+                f"{'bf16' if bf16 == 'true' else 'f32'}{records}>")
     for k in ("resolve_kernel", "append_kernel", "prefill_kernel", "prefill_chunk_kernel",
               "prefill_scan_kernel", "fullstate_kernel", "clear_status_kernel"):
         if k in name:
