@@ -42,6 +42,9 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kNI = kSelectChunk / kThreads;  // candidates per lane
 constexpr int kSortCap = 4096;                // survivors the final kernel sorts
 constexpr int kMaxSlotsPerGroup = 256;
+constexpr int kRankCap = 4096;                // survivors the rank kernel orders
+constexpr int kRankPer = kThreads / 16;       // survivors ranked per workgroup (16 lanes each)
+constexpr int kRankBlocks = kRankCap / kRankPer;
 static_assert(kNI == 32, "validity masks are 32-bit");
 
 struct SelectParams {
@@ -622,6 +625,28 @@ struct FinalShared {
   RadixShared rsh;
 };
 
+// Writes the composite c (key, ~index) as pick j of request r: parent beam,
+// token and score.
+template <bool BEAM>
+__device__ inline void emit_pick(const SelectParams& p, unsigned r, unsigned j,
+                                 unsigned long long c) {
+  const unsigned fi = ~unsigned(c);
+  const unsigned key = unsigned(c >> 32);
+  const unsigned row = row_of(fi, p.V, p.inv_v);
+  const size_t o2 = size_t(r) * p.W + j;
+  p.parents[o2] = int(row);
+  p.tokens[o2] = int(fi - row * p.V);
+  // the key is the score's bit pattern for every number (no re-read); a NaN
+  // (key 0) is recomputed so that its own bits come out
+  float sc = __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+  if (key == 0u) {
+    const float* logp_r = p.logp + size_t(r) * p.N;
+    if constexpr (BEAM) sc = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
+    else sc = logp_r[fi];
+  }
+  p.scores[o2] = sc;
+}
+
 // Sorts the m (key, ~index) pairs in fs.srt (in index order, written before
 // the call by any thread) best first and writes the first W to
 // parents / tokens / scores of request r.  klo / khi: this thread's share of
@@ -629,23 +654,7 @@ struct FinalShared {
 template <bool BEAM>
 __device__ inline void sort_emit(const SelectParams& p, FinalShared& fs, unsigned r, unsigned m,
                                  unsigned klo, unsigned khi) {
-  const float* logp_r = p.logp + size_t(r) * p.N;
-  auto emit = [&](unsigned j, unsigned long long c) {
-    const unsigned fi = ~unsigned(c);
-    const unsigned key = unsigned(c >> 32);
-    const unsigned row = row_of(fi, p.V, p.inv_v);
-    const size_t o2 = size_t(r) * p.W + j;
-    p.parents[o2] = int(row);
-    p.tokens[o2] = int(fi - row * p.V);
-    // the key is the score's bit pattern for every number (no re-read); a NaN
-    // (key 0) is recomputed so that its own bits come out
-    float sc = __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
-    if (key == 0u) {
-      if constexpr (BEAM) sc = p.beam[size_t(r) * p.W_prev + row] + logp_r[fi];
-      else sc = logp_r[fi];
-    }
-    p.scores[o2] = sc;
-  };
+  auto emit = [&](unsigned j, unsigned long long c) { emit_pick<BEAM>(p, r, j, c); };
   __syncthreads();  // srt is written; the caller's reads of fs.sh are done
   const Red3 kr = block_reduce(fs.sh, 0u, klo, khi);
   const unsigned long long* sorted = radix_sort_desc(fs.srt, fs.srt2, m, kr.lo, kr.hi, fs.rsh);
@@ -717,13 +726,19 @@ __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) 
 //     index order, in its chunk's slot of `cap` (>= W) pairs, with the count
 //     and the chunk's largest key; a chunk with more survivors than the slot
 //     holds keeps their exact top W;
-//   gather: one workgroup per request walks the slots in chunk order (index
-//     order), 16384 candidates at a time, keeping the exact top W of what it
-//     has seen in LDS between rounds, and finishes like the final kernel.
-//     Every later candidate has a higher index than the kept ones, so once W
-//     are kept it can only enter with a key above their smallest: slots whose
-//     largest key is not above it are skipped whole, and so are such
-//     candidates.
+//   rank: up to kRankCap survivors (the usual case), workgroups of the whole
+//     chip each load every survivor of the request into LDS and rank 32 of
+//     them: a survivor's place in the result is the number of survivors
+//     before it in the total order (composite (key, ~index) compared as one
+//     64-bit integer, unique per candidate), and those placed below W are
+//     written out directly: no sort and no single-workgroup pass;
+//   gather (more survivors): one workgroup per request walks the slots in
+//     chunk order (index order), 16384 candidates at a time, keeping the
+//     exact top W of what it has seen in LDS between rounds, and finishes
+//     like the final kernel.  Every later candidate has a higher index than
+//     the kept ones, so once W are kept it can only enter with a key above
+//     their smallest: slots whose largest key is not above it are skipped
+//     whole, and so are such candidates.
 // For smooth score distributions about W candidates survive the bound.
 
 template <bool BEAM>
@@ -801,17 +816,18 @@ __device__ inline unsigned wave_scan_max(unsigned x) {
   return x;
 }
 
+// The multi-round gather of request r (fs, next: the workgroup's LDS;
+// next[] holds the (slot, offset) where the next round starts).
 template <bool BEAM>
-__global__ __launch_bounds__(kThreads) void select_gather_kernel(SelectParams p) {
-  __shared__ FinalShared fs;
-  __shared__ unsigned next[2];  // (slot, offset) where the next round starts
+__device__ inline void gather_rounds(const SelectParams& p, FinalShared& fs, unsigned (&next)[2],
+                                     unsigned r) {
   // Round position q -> 1 + (index of its pair in the request's slots) - q,
   // in fs.rsh.flat (the radix sort's counters are idle until the last
   // round).  Within a live slot that difference is constant, and it does not
   // decrease from slot to slot (a slot holds at most cap pairs), so writing
   // it at each slot's first position and taking a running maximum fills the
   // map.
-  const unsigned r = blockIdx.x, ns = p.nslots_in;
+  const unsigned ns = p.nslots_in;
   const unsigned lane = lane_id(), w = threadIdx.x >> 6;
   const uint2* slots = p.cand_in + size_t(r) * ns * p.cap;
   unsigned c4[4], m4[4];  // count and largest key of slots 4t .. 4t + 3 (ns <= 4 * kThreads)
@@ -984,6 +1000,91 @@ __global__ __launch_bounds__(kThreads) void select_gather_kernel(SelectParams p)
   }
 }
 
+// LDS of the rank kernel's usual path.
+struct RankShared {
+  unsigned start[kSelectMaxGatherSlots + 1];  // slot s holds positions [start[s], start[s+1])
+  alignas(16) unsigned long long all[kRankCap];  // every survivor's composite, by position
+  unsigned red[kWaves];
+};
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
+  __shared__ union {
+    RankShared rk;
+    FinalShared fs;
+  } u;
+  __shared__ unsigned next[2];
+  const unsigned r = blockIdx.x / kRankBlocks, b = blockIdx.x - r * kRankBlocks;
+  const unsigned ns = p.nslots_in, t = threadIdx.x;
+  const unsigned lane = lane_id(), w = t >> 6;
+  // slot counts (thread t: slots 4t .. 4t + 3) and their exclusive prefix
+  unsigned c4[4], sum = 0u;
+  {
+    const uint2* cm = reinterpret_cast<const uint2*>(p.cnt_in) + size_t(r) * ns;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const unsigned sl = 4u * t + unsigned(q);
+      c4[q] = sl < ns ? cm[sl].x : 0u;
+      sum += c4[q];
+    }
+  }
+  const unsigned inc = wave_scan(sum);
+  if (lane == 63) u.rk.red[w] = inc;
+  __syncthreads();
+  unsigned run = inc - sum, total = 0u;
+#pragma unroll
+  for (int w2 = 0; w2 < kWaves; ++w2) {
+    const unsigned x = u.rk.red[w2];
+    total += x;
+    run += unsigned(w2) < w ? x : 0u;
+  }
+  if (total > unsigned(kRankCap)) {  // rare: the multi-round gather, one workgroup
+    if (b == 0) {
+      __syncthreads();  // u.rk has been read
+      gather_rounds<BEAM>(p, u.fs, next, r);
+    }
+    return;
+  }
+  if (b * unsigned(kRankPer) >= total) return;  // nothing of this request to rank here
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const unsigned sl = 4u * t + unsigned(q);
+    if (sl < ns) u.rk.start[sl] = run;
+    run += c4[q];
+  }
+  if (t == 0) u.rk.start[ns] = total;
+  __syncthreads();
+  // every survivor into LDS: position q lies in the last slot whose start is
+  // <= q (empty slots share the next one's start, which is then > q)
+  const uint2* slots = p.cand_in + size_t(r) * ns * p.cap;
+  for (unsigned q = t; q < total; q += kThreads) {
+    unsigned lo = 0u, hi = ns;  // start[lo] <= q < start[hi]
+    while (hi - lo > 1u) {
+      const unsigned mid = (lo + hi) >> 1;
+      if (u.rk.start[mid] <= q) lo = mid;
+      else hi = mid;
+    }
+    const uint2 e = slots[size_t(lo) * p.cap + (q - u.rk.start[lo])];
+    u.rk.all[q] = (static_cast<unsigned long long>(e.x) << 32) | unsigned(~e.y);
+  }
+  __syncthreads();
+  // survivor i = 32 b + t / 16: its rank is the number of larger composites,
+  // counted by 16 lanes over interleaved pairs of positions
+  const unsigned i = b * unsigned(kRankPer) + (t >> 4), sub = t & 15u;
+  const unsigned long long mine = u.rk.all[i < total ? i : 0u];
+  unsigned cnt = 0u;
+  for (unsigned j = 2u * sub; j < total; j += 32u) {
+    const ulonglong2 x = *reinterpret_cast<const ulonglong2*>(&u.rk.all[j]);
+    cnt += unsigned(x.x > mine);
+    cnt += unsigned(j + 1u < total && x.y > mine);
+  }
+  cnt += dppu<0xB1>(cnt);   // quad_perm [1,0,3,2]
+  cnt += dppu<0x4E>(cnt);   // quad_perm [2,3,0,1]
+  cnt += dppu<0x141>(cnt);  // row_half_mirror
+  cnt += dppu<0x140>(cnt);  // row_mirror
+  if (sub == 0u && i < total && cnt < p.W) emit_pick<BEAM>(p, r, cnt, mine);
+}
+
 unsigned pow2_ceil(unsigned x) {
   unsigned y = 1;
   while (y < x) y <<= 1;
@@ -1091,8 +1192,9 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
     p.cand_in = p.cand_out;
     p.cnt_in = p.cnt_out;
     p.nslots_in = plan.nchunks;
-    if (has_beam) select_gather_kernel<true><<<R, kThreads, 0, st>>>(p);
-    else select_gather_kernel<false><<<R, kThreads, 0, st>>>(p);
+    const unsigned rblocks = unsigned(R) * kRankBlocks;
+    if (has_beam) select_rank_kernel<true><<<rblocks, kThreads, 0, st>>>(p);
+    else select_rank_kernel<false><<<rblocks, kThreads, 0, st>>>(p);
     return hipGetLastError();
   }
   for (int s = 0; s < plan.stages; ++s) {
