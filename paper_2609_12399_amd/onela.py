@@ -76,6 +76,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"libonela.so not built at {path}; run "
                           "`python -m paper_2609_12399_amd.build`")
+    # torch ships its own HIP runtime; it must be loaded before the library so
+    # that the library binds to that runtime (loaded first, the library would
+    # bring in a second runtime in which torch's device pointers are invalid).
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     cfgp = ctypes.POINTER(onela_config_t)
     sig = {
