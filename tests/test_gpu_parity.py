@@ -448,3 +448,25 @@ def test_fused_wide_beams(storage, widths):
     for t in range(spec.T):
         assert np.array_equal(g[t], anc[t])
         assert rel_err(o[t], ref[t]) <= REL_TOL
+
+
+@pytest.mark.parametrize("dk,widths,io,storage", [
+    (32, (8, 65536, 65536), "f32", "borrow"),     # the largest beam count the library accepts
+    (32, (8, 65536, 65536), "f32", "copy"),
+    (128, (8, 8192, 8192), "bf16", "borrow"),     # 256 beam tiles, per-wave scalar parents
+])
+def test_fused_max_beams(dk, widths, io, storage):
+    """Maximum sizes: max_beams = 65536 (the limit onela_check_config accepts)
+    at d = 32, and 8192 beams at d = 128; the previous beams' ancestry
+    (W_prev x (t - 1) entries) is far beyond the staged table, so each beam's
+    row is read from memory."""
+    log(f"[max-beams] d={dk} widths={widths} io={io} storage={storage}")
+    spec = W.WorkloadSpec("max_beams", 1, 1, 1, dk, dk, 16, widths, io, "uniform", seed=29)
+    wl = W.make_workload(spec)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    anc = oracle_ancestry(wl)
+    o, g = run_gpu(wl, s0, fused=True, storage=storage)
+    for t in range(spec.T):
+        assert np.array_equal(g[t], anc[t])
+        assert rel_err(o[t], ref[t]) <= REL_TOL
