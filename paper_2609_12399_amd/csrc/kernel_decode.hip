@@ -24,8 +24,9 @@
 // per product; the dropped S_lo P_lo term is ~2^-17 relative).
 //
 // Work decomposition.  One workgroup = (request, value head, row slice of DVW
-// state rows, 16*NBLK beams), d_k/16 waves of 16*MB rows each (MB = DVW/d_k;
-// wide d_v is split into row slices, each folding its beams again).
+// state rows, 16*NBLK beams), min(d_k, DVW)/16 waves of 16*MB rows each
+// (MB = DVW/d_k when DVW >= d_k, else 1; wide d_v and d_k = 256 are split into
+// row slices, each folding its beams again).
 // Phase 1 (fold): LPB lanes per beam, each owning EPL consecutive key
 // elements and VPL = DVW/LPB consecutive value rows of its beam; dot products
 // are reduced across those lanes with DPP, and each lane accumulates
@@ -104,14 +105,20 @@ struct DecodeParams {
   int xcd_map;  // 1: XCD-aware block order (units % 8 == 0)
 };
 
+// Threads of a decode workgroup covering DVW state rows at key dimension DK:
+// one wave per 16*MB rows.
+constexpr int decode_rows_per_wave(int dk, int dvw) { return 16 * (dvw >= dk ? dvw / dk : 1); }
+constexpr int decode_threads(int dk, int dvw) { return 64 * (dvw / decode_rows_per_wave(dk, dvw)); }
+
 template <int DK, int DV, int DVW, int NBLK, int CHAIN, bool BF16, bool FUSED, bool BORROW>
-__global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
-  constexpr int MB = DVW / DK;       // 16-row MFMA blocks per wave
+__global__ __launch_bounds__(decode_threads(DK, DVW)) void decode_kernel(DecodeParams p) {
+  constexpr int MB = decode_rows_per_wave(DK, DVW) / 16;  // 16-row MFMA blocks per wave
   constexpr int NS = DV / DVW;       // row slices (workgroups) per (request, head, tile)
-  constexpr int NW = DVW / (16 * MB);// waves per workgroup (= DK / 16)
+  constexpr int NW = DVW / (16 * MB);// waves per workgroup (= min(DK, DVW) / 16)
   constexpr int RPL = 4 * MB;        // consecutive output rows per epilogue lane
-  static_assert(MB * DK == DVW && NS * DVW == DV && (MB == 1 || MB == 2 || MB == 4),
-                "state rows per workgroup must be 1, 2 or 4 times d_k");
+  static_assert((DVW >= DK ? MB * DK == DVW : DVW % 16 == 0) && NS * DVW == DV &&
+                    (MB == 1 || MB == 2 || MB == 4),
+                "state rows per workgroup: 1, 2 or 4 times d_k, or 16-row blocks below d_k");
   constexpr int NT = NW * 64;        // threads per workgroup
   constexpr int BEAMS = 16 * NBLK;   // beams per workgroup
   constexpr int LPB = NT / BEAMS;    // fold lanes per beam
@@ -578,7 +585,7 @@ __global__ __launch_bounds__(4 * DK) void decode_kernel(DecodeParams p) {
 template <int DK, int DV, int DVW, bool BF16, bool FUSED, bool BORROW>
 hipError_t launch_chain(int chain, const DecodeParams& prm, unsigned blocks, hipStream_t st) {
   constexpr int NBLK = kDecodeBeamBlocks;
-  constexpr int threads = 4 * DK;
+  constexpr int threads = decode_threads(DK, DVW);
   switch (chain) {
 #define ONELA_CHAIN_CASE(C)                                                                      \
   case C:                                                                                       \
@@ -606,7 +613,10 @@ hipError_t launch_storage(int chain, const DecodeParams& prm, unsigned blocks, h
 }
 
 // Supported (d_k, d_v) pairs and the state rows one workgroup covers:
-// DVW = min(d_v, 256) rows in 16*MB-row blocks per wave, MB = DVW / d_k.
+// DVW = min(d_v, 256) rows in 16*MB-row blocks per wave, MB = DVW / d_k, for
+// d_k <= 128; at d_k = 256, 128-row slices of 8 waves with 16 rows each (a
+// 256-row workgroup of 16 waves would launch half as many workgroups, each
+// streaming twice the shared state, with 128 registers per lane).
 template <bool FUSED>
 hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsigned units,
                        hipStream_t st) {
@@ -627,8 +637,8 @@ hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsign
   ONELA_SHAPE(128, 128, 128)
   ONELA_SHAPE_BF16(128, 256, 256)
   ONELA_SHAPE_BF16(128, 512, 256)
-  ONELA_SHAPE_BF16(256, 256, 256)
-  ONELA_SHAPE_BF16(256, 512, 256)
+  ONELA_SHAPE_BF16(256, 256, 128)
+  ONELA_SHAPE_BF16(256, 512, 128)
 #undef ONELA_SHAPE
 #undef ONELA_SHAPE_BF16
   return hipErrorInvalidValue;

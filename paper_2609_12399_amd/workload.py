@@ -64,7 +64,7 @@ def _spec(name, R, HK, HV, d, P, W, T, io, parents, s=1.1, mu=-3.0, seed=0):
     return WorkloadSpec(name, R, HK, HV, d, d, P, (W,) * T, io, parents, s, mu, seed)
 
 
-# The five workload shapes used throughout (tests and benchmark).
+# The workload shapes used throughout (tests and benchmark).
 SPECS = {
     # 1 layer, 2 heads, d = 32, fp32, 64-token prompt, 8 beams, 3 steps.
     "tiny_h2_d32_w8": _spec("tiny_h2_d32_w8", 1, 2, 2, 32, 64, 8, 3, "f32",
@@ -82,6 +82,14 @@ SPECS = {
     # 5 steps, Zipf(1.5) parents, alpha near 1.
     "gqa_h16x32_d128_w1024": _spec("gqa_h16x32_d128_w1024", 1, 16, 32, 128, 8192,
                                    1024, 5, "bf16", "zipf", 1.5, -5.0, seed=1004),
+    # Wider heads of the paper's operator suite (key dim up to 256, value dim up
+    # to 512, grouped heads): 8 heads with d_k = d_v = 256, 512 beams, 4 steps.
+    "h8_k256_v256_w512": WorkloadSpec("h8_k256_v256_w512", 1, 8, 8, 256, 256, 2048,
+                                      (512,) * 4, "bf16", "zipf", 1.1, seed=1005),
+    # 4 query/key heads of d_k = 256 shared by 8 value heads of d_v = 512,
+    # 256 beams, 4 steps.
+    "h4x8_k256_v512_w256": WorkloadSpec("h4x8_k256_v512_w256", 1, 4, 8, 256, 512, 2048,
+                                        (256,) * 4, "bf16", "uniform", seed=1006),
 }
 
 HEADLINE = "h16_d128_w512"
