@@ -27,6 +27,7 @@ struct Shape {
   bool bf16;  // q/k/v stored as bf16 bits (else fp32)
   bool delta;  // records are (alpha, delta, k) transition records (else step inputs)
   bool borrow;  // step-input records stay in the caller's buffers (no arena copy)
+  int cus = 0;  // compute units of the context's device (0: not known)
   int io_bytes() const { return bf16 ? 2 : 4; }
 };
 

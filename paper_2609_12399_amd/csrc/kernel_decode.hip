@@ -614,7 +614,8 @@ hipError_t launch_storage(int chain, const DecodeParams& prm, unsigned blocks, h
 
 // Supported (d_k, d_v) pairs and the state rows one workgroup covers:
 // DVW = min(d_v, 256) rows in 16*MB-row blocks per wave, MB = DVW / d_k, for
-// d_k <= 128; at d_k = 256, 128-row slices of 8 waves with 16 rows each (a
+// d_k <= 128 (d = 128 launches that would leave most compute units idle use
+// 64-row slices); at d_k = 256, 128-row slices of 8 waves with 16 rows each (a
 // 256-row workgroup of 16 waves would launch half as many workgroups, each
 // streaming twice the shared state, with 128 registers per lane).
 template <bool FUSED>
@@ -634,6 +635,16 @@ hipError_t launch_mode(const Shape& s, int step, const DecodeParams& prm, unsign
   }
   ONELA_SHAPE(32, 32, 32)
   ONELA_SHAPE(64, 64, 64)
+  // d = 128 launches with fewer workgroups than half the compute units (128
+  // beams x 16 heads: 64): 64-row slices of 4 waves, twice the workgroups.
+  // Both slice widths hold 16 rows per wave, so the split state that step 0
+  // stores has the same layout for either.
+  if (s.dk == 128 && s.dv == 128 &&
+      2u * units * unsigned(prm.ntiles) <= unsigned(s.cus > 0 ? s.cus : 256)) {
+    const unsigned blocks = units * 2u * unsigned(prm.ntiles);
+    return s.bf16 ? launch_storage<128, 128, 64, true, FUSED>(chain, prm, blocks, st)
+                  : launch_storage<128, 128, 64, false, FUSED>(chain, prm, blocks, st);
+  }
   ONELA_SHAPE(128, 128, 128)
   ONELA_SHAPE_BF16(128, 256, 256)
   ONELA_SHAPE_BF16(128, 512, 256)

@@ -2,6 +2,7 @@
 // protocol bookkeeping and kernel launches.  Every check that can fail runs
 // before anything is enqueued, so a rejected call leaves no device work and
 // no change in the context.
+#include <atomic>
 #include <cstdint>
 #include <cstdlib>
 #include <new>
@@ -118,6 +119,23 @@ size_t onela_workspace_bytes(const onela_config_t* cfg) {
   return onela::layout_of(s).total;
 }
 
+namespace {
+// Compute units of the current device, queried once per device (a host-side
+// attribute query; nothing is enqueued).  0 if it cannot be read.
+int device_compute_units() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v <= 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v > 0 ? v : 0;
+}
+}  // namespace
+
 onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
                           void* workspace, size_t workspace_bytes, void* stream,
                           onela_ctx_t* out) {
@@ -128,6 +146,7 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   if ((reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return ONELA_EINVAL;
   const Layout l = onela::layout_of(s);
   if (workspace_bytes < l.total) return ONELA_ECAPACITY;
+  s.cus = device_compute_units();
 
   onela_ctx_s* c = new (std::nothrow) onela_ctx_s();
   if (!c) return ONELA_ENOMEM;
