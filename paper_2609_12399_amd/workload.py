@@ -82,6 +82,10 @@ SPECS = {
     # 5 steps, Zipf(1.5) parents, alpha near 1.
     "gqa_h16x32_d128_w1024": _spec("gqa_h16x32_d128_w1024", 1, 16, 32, 128, 8192,
                                    1024, 5, "bf16", "zipf", 1.5, -5.0, seed=1004),
+    # The shape of the paper's recurrent-state-path breakdown: 4 requests x 512
+    # beams, 16 heads, d = 128, 6 decode steps (7 output tokens), 1024-token prompts.
+    "r4_h16_d128_w512_t6": _spec("r4_h16_d128_w512_t6", 4, 16, 16, 128, 1024, 512, 6,
+                                 "bf16", "zipf", 1.1, seed=1007),
     # Wider heads of the paper's operator suite (key dim up to 256, value dim up
     # to 512, grouped heads): 8 heads with d_k = d_v = 256, 512 beams, 4 steps.
     "h8_k256_v256_w512": WorkloadSpec("h8_k256_v256_w512", 1, 8, 8, 256, 256, 2048,
