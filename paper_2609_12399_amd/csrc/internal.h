@@ -14,6 +14,8 @@ constexpr int kMaxSteps = 8;
 // Ancestry entries (previous beams x steps <= t-2) a fused decode step at
 // t >= 2 stages in LDS; larger tables are read row by row from global memory.
 constexpr int kAncTable = 2048;
+// The staged table's limit from chains of 5 records on (t >= 4).
+constexpr int kAncTableLong = 1024;
 
 // Decode tiling: 16-beam MFMA column blocks per workgroup.
 constexpr int kDecodeBeamBlocks = 2;

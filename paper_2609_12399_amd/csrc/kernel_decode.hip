@@ -297,8 +297,12 @@ __global__ __launch_bounds__(decode_threads(DK, DVW)) void decode_kernel(DecodeP
   // of steps <= t-2 are addressed as soon as a beam's parent is known rather
   // than one dependent memory round trip later.  Only the first wave of each
   // SIMD loads: the second receives its data about one round trip later.
+  // Every workgroup loads its request's whole table, so the table's cost
+  // grows with its size while what it saves (one dependent round) does not:
+  // from chains of 5 (t >= 4) on, tables beyond 1024 entries are read row by
+  // row (at 4 requests x 512 beams: 22.6 -> 20.2 us at t = 4).
   const int ntab = kTab ? p.W_prev * (NA - 1) : 0;
-  const bool tab = kTab && ntab <= kAncTable;
+  const bool tab = kTab && ntab <= (NA >= 4 ? kAncTableLong : kAncTable);
   int tv[kTab ? NTV : 1];
   if constexpr (kTab) {
     if (tab && tid < NL) {

@@ -431,14 +431,16 @@ def test_borrowed_records_bad_parent_contained(fused):
     (8, 2100, 2100, 2100),                    # 66 beam tiles, ragged last one
     (8, 1000, 1024, 1024),                    # staged ancestry: 1000, then exactly 2048 entries
     (8, 1024, 1025, 700),                     # 1024 staged, then 2050: read row by row
-    (8, 64, 300, 341, 200, 409, 300, 292),    # chains of 8; 409 x 5 = 2045 staged
+    (8, 64, 300, 341, 200, 409, 300, 292),    # chains of 8; from t = 4 on row by row
     (8, 64, 300, 341, 200, 410, 300, 292),    # 410 x 5 = 2050 read row by row
+    (8, 64, 300, 341, 256, 300, 257, 100),    # t = 4: 1023, t = 5: 1024 staged; t >= 6 not
 ])
 @pytest.mark.parametrize("storage", ["copy", "borrow"])
 def test_fused_wide_beams(storage, widths):
     """Wide and changing beam counts over fused steps: the ancestry of the
     previous beams (W_prev x (t - 1) entries) is staged in LDS up to 2048
-    entries and read row by row beyond; both sides of that limit."""
+    entries (1024 from t = 4 on) and read row by row beyond; both sides of
+    both limits."""
     spec = W.WorkloadSpec("wide_beam", 1, 2, 2, 32, 32, 16, widths, "f32", "uniform", seed=17)
     wl = W.make_workload(spec)
     s0 = oracle_s0(wl)
