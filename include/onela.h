@@ -117,7 +117,9 @@ size_t onela_workspace_bytes(const onela_config_t* cfg);
 
 /* Creates a decode context and binds the shared post-prefill state
  * (Sec. 3.1: S_ctx is stored once per request and shared by all beams).
- * Host bookkeeping only: nothing is enqueued.
+ * Host bookkeeping only: nothing is enqueued.  The current device's
+ * compute-unit count is read once per device (a host attribute query) and
+ * chooses the decode tiling of launches that would leave most units idle.
  *   s0        device, fp32 [R][H_V][d_v][d_k]; borrowed until onela_destroy
  *             (read by the step-0 launch of every beam search), owned by the
  *             caller
