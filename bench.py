@@ -25,6 +25,7 @@ fp64 CPU oracle timed on this host.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -37,7 +38,19 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_12399_amd", "csrc", "kernel_decode.hip")
+# The sources the fused decode kernel is compiled from (its traffic profile is
+# tied to their combined hash).
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_12399_amd", "csrc", f)
+               for f in ("kernel_decode.hip", "device_common.h", "internal.h")]
+
+
+def kernel_sources_sha256() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_fused_h16_d128_w512_traffic.md")
 
 
@@ -46,10 +59,9 @@ def measured_traffic(workload: str, variant: str):
     (FETCH_SIZE and WRITE_SIZE runs, copy-calibrated), or None when the
     summary is missing, is for another workload or record variant, or was
     taken on a different kernel source than the one built now."""
-    import hashlib
     if not os.path.exists(TRAFFIC_PROFILE):
         return None
-    want = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    want = kernel_sources_sha256()
     for line in open(TRAFFIC_PROFILE):
         if line.startswith("bench-traffic: "):
             rec = json.loads(line[len("bench-traffic: "):])

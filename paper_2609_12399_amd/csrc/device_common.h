@@ -6,7 +6,9 @@
 namespace onela {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // Pointer to a byte offset from a base (32-bit offsets keep per-lane address
 // arithmetic in 32 bits; every region is smaller than 2 GiB).
@@ -62,9 +64,12 @@ struct RawV {
   }
 };
 
+// Two floats rounded to bf16 (round to nearest even), a in the low half.  The
+// pair is converted as one vector so that it becomes a single two-source
+// v_cvt_pk_bf16_f32; converted one by one, each takes its own conversion
+// plus a shift and a merge.
 __device__ inline unsigned pack_bf16x2(float a, float b) {
-  return unsigned(__builtin_bit_cast(unsigned short, static_cast<__bf16>(a))) |
-         (unsigned(__builtin_bit_cast(unsigned short, static_cast<__bf16>(b))) << 16);
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
 __device__ inline float bf16_lo_to_float(unsigned u) { return __uint_as_float(u << 16); }
