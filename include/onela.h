@@ -202,7 +202,9 @@ onela_status_t onela_decode_step_fused(onela_ctx_t ctx, int32_t step, int32_t wi
 
 /* Synchronises the context's stream, returns and clears the sticky device
  * error (ONELA_OK or ONELA_EPARENT), or ONELA_EHIP.  The error covers the
- * current beam search: the step-0 launch of each search zeroes it. */
+ * current beam search: the step-0 decode launch of each search zeroes it,
+ * and when a search resolves step 1 without having decoded step 0, the
+ * resolve call zeroes it first (one extra launch). */
 onela_status_t onela_get_device_status(onela_ctx_t ctx);
 
 /* Frees the host-side context (the workspace stays the caller's). */

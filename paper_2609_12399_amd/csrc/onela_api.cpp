@@ -19,7 +19,8 @@ struct onela_ctx_s {
   Arena arena;
   hipStream_t stream;
   int resolved;  // last step whose ancestry was resolved (-1: none)
-  bool status_live;  // a step-0 launch (which zeroes the status word) was enqueued
+  bool status_live;  // a launch that zeroes the status word was enqueued (ever)
+  bool search_zeroed;  // ... in the current beam search (since init / reset)
   int appended;  // last step whose records were appended (-1: none)
   int widths[onela::kMaxSteps];
 };
@@ -173,6 +174,7 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   c->arena.d = s.delta ? p : nullptr;
 
   c->status_live = false;
+  c->search_zeroed = false;
   *out = c;
   return ONELA_OK;
 }
@@ -181,6 +183,7 @@ onela_status_t onela_reset(onela_ctx_t c) {
   if (!c) return ONELA_EINVAL;
   c->resolved = -1;
   c->appended = -1;
+  c->search_zeroed = false;
   return ONELA_OK;
 }
 
@@ -195,6 +198,15 @@ onela_status_t onela_resolve_ancestry(onela_ctx_t c, int32_t step, int32_t width
   if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
   if (gather_out && !aligned4(gather_out)) return ONELA_EINVAL;
   if (step > 0) {
+    // The step-0 decode launch zeroes the status word of a new search.  When
+    // the caller resolves step 1 without having decoded step 0, zero it here
+    // first, so that what the resolve kernel flags is not mixed with a word
+    // that was never cleared (or still holds an earlier search's error).
+    if (!c->search_zeroed) {
+      if (!launch_ok(onela::launch_clear_status(c->arena.status, c->stream))) return ONELA_EHIP;
+      c->search_zeroed = true;
+      c->status_live = true;
+    }
     hipError_t e = onela::launch_resolve(s, step, width, c->widths[step - 1], parents,
                                          c->arena.anc[(step - 1) & 1],
                                          c->arena.anc[step & 1], gather_out,
@@ -235,7 +247,7 @@ onela_status_t onela_decode_step(onela_ctx_t c, int32_t step, const void* q, flo
                      : onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
                                             c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
-  if (step == 0) c->status_live = true;
+  if (step == 0) c->status_live = c->search_zeroed = true;
   return ONELA_OK;
 }
 
@@ -265,7 +277,7 @@ onela_status_t onela_decode_step_fused(onela_ctx_t c, int32_t step, int32_t widt
   if (s.borrow) borrow_step(c, step, k, v, alpha, beta);
   c->resolved = step;
   c->appended = step;
-  if (step == 0) c->status_live = true;
+  if (step == 0) c->status_live = c->search_zeroed = true;
   return ONELA_OK;
 }
 

@@ -205,6 +205,41 @@ def test_bad_parent_is_reported_and_contained(fused):
     dec.close()
 
 
+def test_bad_parent_reported_when_step0_not_decoded():
+    """resolve(0), append(0), then resolve(1) with a bad parent and no
+    decode(0): the status word was never zeroed by a step-0 launch, so the
+    resolve call zeroes it first and the bad parent is still reported; a
+    stale error of an earlier search does not leak into the next one."""
+    spec = _small(widths=(16, 16, 16), seed=23)
+    wl = W.make_workload(spec)
+    wl.steps[1].parents[0, 4] = 16  # == W_0: out of range
+    s0 = oracle_s0(wl)
+    dw = runner.to_device(wl, DEV, with_prompt=False)
+    dec = runner.Decoder(spec, torch.from_numpy(s0).to(DEV), DEV)
+    st0, st1 = dw.steps[0], dw.steps[1]
+    g1 = torch.zeros((1, 16, 1), dtype=torch.int32, device=DEV)
+    ab.onela_resolve_ancestry(dec.ctx, 0, 16, None)
+    ab.onela_append_records(dec.ctx, 0, st0.k, st0.v, st0.alpha, st0.beta)
+    ab.onela_resolve_ancestry(dec.ctx, 1, 16, st1.parents, g1)
+    assert dec.status() == ab.ONELA_EPARENT
+    assert g1.cpu().numpy()[0, 4, 0] == -1
+    assert dec.status() == ab.ONELA_OK
+    # a search whose bad parent is never queried, then a clean search that
+    # skips decode(0): the stale error is cleared by the new search
+    dec.reset()
+    ab.onela_resolve_ancestry(dec.ctx, 0, 16, None)
+    ab.onela_append_records(dec.ctx, 0, st0.k, st0.v, st0.alpha, st0.beta)
+    ab.onela_resolve_ancestry(dec.ctx, 1, 16, st1.parents)
+    dec.reset()
+    good = st1.parents.clone()
+    good[0, 4] = 0
+    ab.onela_resolve_ancestry(dec.ctx, 0, 16, None)
+    ab.onela_append_records(dec.ctx, 0, st0.k, st0.v, st0.alpha, st0.beta)
+    ab.onela_resolve_ancestry(dec.ctx, 1, 16, good)
+    assert dec.status() == ab.ONELA_OK
+    dec.close()
+
+
 def test_protocol_order_enforced():
     wl = W.make_workload(_small())
     s0 = oracle_s0(wl)
