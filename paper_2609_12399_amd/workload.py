@@ -86,6 +86,10 @@ SPECS = {
     # beams, 16 heads, d = 128, 6 decode steps (7 output tokens), 1024-token prompts.
     "r4_h16_d128_w512_t6": _spec("r4_h16_d128_w512_t6", 4, 16, 16, 128, 1024, 512, 6,
                                  "bf16", "zipf", 1.1, seed=1007),
+    # The widest value-head count of the paper's operator suite (H_V = 64):
+    # 64 value heads over 16 query/key heads, d = 128, 256 beams, 4 steps.
+    "gqa_h16x64_d128_w256": _spec("gqa_h16x64_d128_w256", 1, 16, 64, 128, 2048, 256, 4,
+                                  "bf16", "zipf", 1.1, seed=1008),
     # Wider heads of the paper's operator suite (key dim up to 256, value dim up
     # to 512, grouped heads): 8 heads with d_k = d_v = 256, 512 beams, 4 steps.
     "h8_k256_v256_w512": WorkloadSpec("h8_k256_v256_w512", 1, 8, 8, 256, 256, 2048,
