@@ -10,11 +10,15 @@ d_k = d_v = 128, bf16 inputs, a 4096-token prompt, 512 beams, 4 decode steps,
 Zipf(1.1) parents.
 
 Inputs are resident in HBM when timing starts: the bench keeps ``--batches``
-independent copies of every input, workspace and output, and step i uses
-batch i % batches, so a batch's data was last touched far more than the
-256 MiB Infinity Cache ago.  Timed steps are replayed from HIP graphs (one
-captured graph per batch, and one per run of ``--graph-group`` consecutive
-batches) so host launch cost does not pace the GPU.
+independent copies of every input, workspace and output.  Steps run in groups
+of G consecutive batches (G = the largest divisor of the timed step count K
+not above ``--graph-group``), interleaved by decode step: every batch of the
+group is initialised, then step t runs for every batch of the group before
+step t + 1 runs for any, so a launch never directly follows the previous step
+of its own batch, whose data is G - 1 launches (about G x 13 MB at the
+headline) old.  Each group is one captured HIP graph, replayed whole: the
+timed region is always K / G whole groups, so the figure does not depend on
+K, and the graph-launch cost is paid once per G steps.
 
 Printed: one JSON line with the whole-job throughput (beam-tokens/s), the
 per-kernel roofline of the fused step kernel (algorithmic bytes / average
@@ -205,30 +209,60 @@ def step_alg_bytes(wl, fused=True, variant="borrow"):
     return total
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (``/proc/cpuinfo``), or "unknown"."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_threads() -> int:
+    """Threads the CPU oracle runs with: the process's CPU affinity, capped by
+    OMP_NUM_THREADS when the environment sets it (a shared host's share)."""
+    n = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n)
+
+
 def cpu_baseline(wl, min_seconds, gpu_outs=None):
     """The fp64 oracle (materialised per-beam states) timed on this host's
-    cores over whole decodes of one request of the same workload.  With the
-    GPU's outputs of that request (``gpu_outs``: list over t of [W_t][HV][dv])
-    it also reports their max normwise relative error against the oracle,
-    which builds S_ctx with its own fp64 prefill."""
+    cores over whole decodes of one request of the same workload, with all
+    the threads it may use and with one thread.  With the GPU's outputs of
+    that request (``gpu_outs``: list over t of [W_t][HV][dv]) it also reports
+    their max normwise relative error against the oracle, which builds S_ctx
+    with its own fp64 prefill."""
     from oracle import oracle as orc
     s = wl.spec
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    threads = oracle_threads()
     r = 0
+    t0 = time.perf_counter()
     s0 = orc.prefill(wl.prompt_k.f64[r], wl.prompt_v.f64[r], wl.prompt_alpha.f64[r],
                      wl.prompt_beta.f64[r], nthreads=threads).astype(np.float32)
+    prefill_s = time.perf_counter() - t0
     args = (s0.astype(np.float64), [x.q.f64[r] for x in wl.steps],
             [x.k.f64[r] for x in wl.steps], [x.v.f64[r] for x in wl.steps],
             [x.alpha.f64[r] for x in wl.steps], [x.beta.f64[r] for x in wl.steps],
             [x.parents[r] for x in wl.steps[1:]])
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        orc.decode(*args, nthreads=threads)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= min_seconds or reps >= 200:
-            break
-    beam_tokens = reps * sum(s.widths)
+
+    def timed(nthreads, seconds, max_reps):
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            orc.decode(*args, nthreads=nthreads)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or reps >= max_reps:
+                return reps, el
+
+    reps, el = timed(threads, min_seconds, 200)
+    # one thread: at least one whole decode, about a third of the budget
+    reps1, el1 = timed(1, min_seconds / 3, 200)
+    beam_tokens = sum(s.widths)
     err = None
     if gpu_outs is not None:
         ref = orc.decode(*args, nthreads=threads)
@@ -239,12 +273,21 @@ def cpu_baseline(wl, min_seconds, gpu_outs=None):
             den = np.maximum(np.max(np.abs(ref[t]), axis=-1), 1e-30)
             errs.append(np.max(num / den))
         err = float(np.max(errs))  # a NaN anywhere propagates
-    return {"value": beam_tokens / el, "unit": "beam-tokens/s", "cores": threads,
+    return {"value": reps * beam_tokens / el, "unit": "beam-tokens/s", "cores": threads,
+            "ms_per_step": 1e3 * el / reps,
+            "one_thread": {"value": reps1 * beam_tokens / el1, "unit": "beam-tokens/s",
+                           "cores": 1, "ms_per_step": 1e3 * el1 / reps1,
+                           "sample": f"{reps1} decodes, {el1:.1f} s"},
+            "affinity_cpus": len(os.sched_getaffinity(0)),
+            "omp_num_threads_env": os.environ.get("OMP_NUM_THREADS"),
+            "cpu_model": cpu_model(),
+            "prefill_s": prefill_s,
             "max_rel_err_gpu_vs_oracle": err,
             "kind": "oracle",
             "sample": f"{reps} full {s.T}-step decodes of one request "
-                      f"({s.HV} heads, {s.W} beams, S_ctx given), {el:.1f} s, "
-                      f"fp64 materialised per-beam states"}
+                      f"({s.HV} heads, {s.W} beams, S_ctx given), {el:.1f} s on {threads} "
+                      f"threads, fp64 materialised per-beam states; S_ctx prefill "
+                      f"({s.P} tokens) timed separately"}
 
 
 def main():
@@ -253,10 +296,11 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None)
-    ap.add_argument("--batches", type=int, default=32)
+    ap.add_argument("--batches", type=int, default=40)
     ap.add_argument("--no-graph", action="store_true")
-    ap.add_argument("--graph-group", type=int, default=8,
-                    help="consecutive batches captured into one graph (1: one graph per step)")
+    ap.add_argument("--graph-group", type=int, default=20,
+                    help="largest number of batches interleaved step by step in one graph "
+                         "(the group is the largest divisor of --steps not above it)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--skip-fullstate", action="store_true")
@@ -266,6 +310,8 @@ def main():
                          "delta records (the others are timed as an A/B)")
     ap.add_argument("--skip-ab", action="store_true")
     ap.add_argument("--skip-select", action="store_true")
+    ap.add_argument("--skip-loop", action="store_true",
+                    help="skip the closed-loop leg (fused decode + beam selection per step)")
     ap.add_argument("--skip-prefill", action="store_true")
     ap.add_argument("--select-vocab", type=int, default=None,
                     help="codebook size of the beam-selection measurement")
@@ -317,18 +363,22 @@ def main():
                     [getattr(st, f) for st in b["steps"] for f in ("q", "k", "v", "alpha", "beta")])
     log(f"[bench] {NB} batches, {footprint / 2**20:.0f} MiB resident")
 
-    def one_step(b, fused, kind):
-        """init + T x (resolve, append, decode) on the current stream."""
-        ctx = ab.onela_init(cfgs[kind], b["s0"], b["ws"], ws_bytes, None)
-        for t, st in enumerate(b["steps"]):
-            if fused:
-                ab.onela_decode_step_fused(ctx, t, st.width, st.parents, st.k, st.v, st.alpha,
-                                           st.beta, st.q, b["outs"][t])
-            else:
-                ab.onela_resolve_ancestry(ctx, t, st.width, st.parents, None)
-                ab.onela_append_records(ctx, t, st.k, st.v, st.alpha, st.beta)
-                ab.onela_decode_step(ctx, t, st.q, b["outs"][t])
-        ab.onela_destroy(ctx)
+    def group_steps(bs, fused, kind):
+        """One whole step (init + T decode steps) of every batch in ``bs``,
+        interleaved by decode step, on the current stream."""
+        ctxs = [ab.onela_init(cfgs[kind], b["s0"], b["ws"], ws_bytes, None) for b in bs]
+        for t in range(T):
+            for ctx, b in zip(ctxs, bs):
+                st = b["steps"][t]
+                if fused:
+                    ab.onela_decode_step_fused(ctx, t, st.width, st.parents, st.k, st.v,
+                                               st.alpha, st.beta, st.q, b["outs"][t])
+                else:
+                    ab.onela_resolve_ancestry(ctx, t, st.width, st.parents, None)
+                    ab.onela_append_records(ctx, t, st.k, st.v, st.alpha, st.beta)
+                    ab.onela_decode_step(ctx, t, st.q, b["outs"][t])
+        for ctx in ctxs:
+            ab.onela_destroy(ctx)
 
     def capture(fn):
         fn()  # eager once before capture
@@ -339,40 +389,37 @@ def main():
         torch.cuda.synchronize()
         return g
 
-    G = max(1, min(args.graph_group, NB))
+    def group_size(K):
+        """Largest divisor of K that is at most --graph-group and the batch count."""
+        cap = max(1, min(args.graph_group, NB))
+        return max(g for g in range(1, cap + 1) if K % g == 0)
+
+    G = group_size(args.steps)
+    NG = NB // G  # groups of distinct batches, replayed round robin
 
     def timed_steps(fused, K, warmup, kind):
-        """Exactly K steps (step i on batch i % NB); returns ms per step.
-        Batches G*g .. G*g + G - 1 are also captured into one graph, replayed
-        when a run of G steps starts at such a batch, so that the per-graph
-        launch cost is paid once per G steps."""
-        graphs = groups = None
+        """Exactly K steps as K / G whole groups (group i uses batches
+        G*(i % NG) .. G*(i % NG) + G - 1); the warm-up is rounded up to whole
+        groups.  Returns ms per step."""
+        groups = [batches[G * g:G * g + G] for g in range(NG)]
+        graphs = None
         if not args.no_graph:
-            graphs = [capture(lambda b=b: one_step(b, fused, kind)) for b in batches]
-            if G > 1:
-                groups = [capture(lambda g=g: [one_step(batches[k], fused, kind)
-                                               for k in range(G * g, G * g + G)])
-                          for g in range(NB // G)]
+            graphs = [capture(lambda bs=bs: group_steps(bs, fused, kind)) for bs in groups]
 
-        def run(n, start):
-            i = 0
-            while i < n:
-                k = (start + i) % NB
+        def run(ngroups, start):
+            for i in range(ngroups):
+                g = (start + i) % NG
                 if graphs is None:
-                    one_step(batches[k], fused, kind)
-                    i += 1
-                elif groups is not None and k % G == 0 and k + G <= NB and n - i >= G:
-                    groups[k // G].replay()
-                    i += G
+                    group_steps(groups[g], fused, kind)
                 else:
-                    graphs[k].replay()
-                    i += 1
+                    graphs[g].replay()
 
-        run(warmup, 0)
+        nw = -(-warmup // G)
+        run(nw, 0)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        run(K, warmup)
+        run(K // G, nw)
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
@@ -460,7 +507,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": ("bf16 in, f32 accum" if spec.io_dtype == "bf16" else "f32"),
         "data": "synthetic",
         "config": {"workload": name, "requests": spec.R, "qk_heads": spec.HK,
                    "v_heads": spec.HV, "d_k": spec.dk, "d_v": spec.dv, "prompt": spec.P,
@@ -475,7 +522,9 @@ def main():
                                "delta": "(alpha, delta fp16, k) transition records"}[kind],
                    "contraction": "S_ctx.P on bf16 MFMA, hi/lo split in registers, 3 products, "
                                   "fp32 accum",
-                   "variant": kind, "graph": not args.no_graph, "graph_group": G, "batches": NB},
+                   "variant": kind, "graph": not args.no_graph, "graph_group": G, "batches": NB,
+                   "protocol": f"K / {G} whole groups of {G} batches, each group one HIP graph "
+                               f"with the batches' steps interleaved by decode step"},
         "decode_step_us": {"per_t": [round(float(x), 3) for x in dec_us],
                            "mean": round(float(dec_us.mean()), 3)},
         "beam_tokens_per_step": beam_tokens_per_step,
@@ -629,6 +678,81 @@ def main():
         log(f"[bench] beam selection {sel_us:.1f} us/call ({wp}x{vocab} -> {wp}), "
             f"torch.topk {topk_us:.1f} us")
         del sel, gsel, logp_d, beam_d, flat
+
+    # ---- closed decode loop (supplementary, not part of `value`): after every
+    # fused decode step the global top-W selection over the step's beams x the
+    # codebook, whose parents the next step takes and whose candidate scores
+    # are the next selection's beam scores (Sec. 2.1, Fig. 1; Sec. 3.3).  The
+    # log-probabilities are seeded synthetic inputs (the model producing them
+    # is not part of the path).  Batches interleaved by step as above.
+    if not args.skip_loop:
+        vocab = args.select_vocab or Wm.SELECT_CODEBOOK
+        GL = max(1, min(8, NB // 2))
+        nlb = 2 * GL
+        lb = []
+        for i in range(nlb):
+            b = batches[i]
+            L = dict(b=b, logp=[], par=[None], tok=[], sc=[], ws=None, ws_bytes=0)
+            for t in range(T):
+                wt = spec.widths[t]
+                wn = spec.widths[t + 1] if t + 1 < T else spec.widths[t]
+                logp_np, _ = Wm.make_select_inputs(spec.R, wt, vocab, seed=spec.seed + 31 * t + i,
+                                                   with_beam=False)
+                L["logp"].append(torch.from_numpy(logp_np).to(dev))
+                L["par"].append(torch.zeros((spec.R, wn), dtype=torch.int32, device=dev))
+                L["tok"].append(torch.empty((spec.R, wn), dtype=torch.int32, device=dev))
+                L["sc"].append(torch.empty((spec.R, wn), dtype=torch.float32, device=dev))
+                L["ws_bytes"] = max(L["ws_bytes"],
+                                    ab.onela_select_workspace_bytes(spec.R, wt, vocab, wn))
+            L["ws"] = torch.zeros(max(L["ws_bytes"], 1), dtype=torch.uint8, device=dev)
+            lb.append(L)
+        torch.cuda.synchronize()
+
+        def loop_group(ls):
+            ctxs = [ab.onela_init(cfgs[kind], L["b"]["s0"], L["b"]["ws"], ws_bytes, None)
+                    for L in ls]
+            for t in range(T):
+                wt = spec.widths[t]
+                wn = spec.widths[t + 1] if t + 1 < T else wt
+                for ctx, L in zip(ctxs, ls):
+                    st = L["b"]["steps"][t]
+                    ab.onela_decode_step_fused(ctx, t, wt, L["par"][t], st.k, st.v, st.alpha,
+                                               st.beta, st.q, L["b"]["outs"][t])
+                for L in ls:
+                    ab.onela_select_beams(spec.R, wt, vocab, wn, L["logp"][t],
+                                          L["sc"][t - 1] if t > 0 else None, L["par"][t + 1],
+                                          L["tok"][t], L["sc"][t], L["ws"], L["ws_bytes"])
+            for ctx in ctxs:
+                ab.onela_destroy(ctx)
+
+        lgroups = [lb[GL * g:GL * g + GL] for g in range(2)]
+        lgraphs = [capture(lambda ls=ls: loop_group(ls)) for ls in lgroups]
+        for gr in lgraphs:
+            gr.replay()
+        torch.cuda.synchronize()
+        nrep = 10
+        le0, le1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        le0.record()
+        for i in range(nrep):
+            lgraphs[i % 2].replay()
+        le1.record()
+        torch.cuda.synchronize()
+        loop_ms = le0.elapsed_time(le1) / (nrep * GL)
+        # the same graphs without the selections, for the split
+        result["closed_loop"] = {
+            "ms_per_search": loop_ms,
+            "us_per_step": loop_ms * 1e3 / T,
+            "beam_tokens_per_s": beam_tokens_per_step / (loop_ms / 1e3),
+            "decode_only_ms_per_search": ms_per_step,
+            "selection_share": max(0.0, 1.0 - ms_per_step / loop_ms),
+            "codebook": vocab,
+            "step": f"per decode step t: onela_decode_step_fused, then onela_select_beams "
+                    f"over W_t x {vocab} candidates -> W_(t+1) (parents of step t + 1, "
+                    f"scores = next beam scores); {T} steps per search",
+            "protocol": f"{nrep} graph replays of {GL} batches interleaved by step"}
+        log(f"[bench] closed loop: {loop_ms * 1e3:.1f} us per {T}-step search "
+            f"({loop_ms * 1e3 / T:.1f} us per decode + select)")
+        del lb, lgraphs
 
     # ---- practical HBM ceiling: a plain device copy (torch copy_, 16-byte
     # vector blit) of the same size as the dominant kernel's traffic, and of
