@@ -291,6 +291,25 @@ onela_status_t onela_select_beams(int32_t num_requests, int32_t prev_width, int3
                                   int32_t* tokens_out, float* scores_out, void* workspace,
                                   size_t workspace_bytes, void* stream);
 
+/* ---- Beam selection without a workspace ---------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * selection, arguments, order and result as onela_select_beams, with the
+ * workspace taken from a device array of the library instead of an argument.
+ * Each GPU the library runs on holds its own 32 MiB array until the process
+ * ends (its address is looked up once per device, on the first call with
+ * that device current).  Calls whose workspace (onela_select_workspace_bytes)
+ * would exceed 32 MiB return ONELA_ECAPACITY and enqueue nothing.  Nothing
+ * is allocated by this call.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (different streams, or host threads) race
+ * and must be serialised by the caller; consecutive calls on one stream are
+ * safe.  Errors: ONELA_EINVAL, ONELA_ECAPACITY, ONELA_EHIP. */
+onela_status_t onela_select_beams_noalloc(int32_t num_requests, int32_t prev_width,
+                                          int32_t vocab, int32_t width, const float* logp,
+                                          const float* beam_scores, int32_t* parents_out,
+                                          int32_t* tokens_out, float* scores_out,
+                                          void* stream);
+
 /* ---- Capacity model (host only) -----------------------------------------
  * Persistent recurrent-state bytes after `steps` decode steps for one GDN
  * layer (Sec. 4.4): one S_ctx per request and value head (state_bytes per

@@ -124,6 +124,10 @@ struct SelectPlan {
   size_t seg_off, slot_off, cnt_off;
 };
 bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan);
+// Size of the per-device scratch array of the allocation-free selection
+// entry point, and its device address on the current device.
+constexpr size_t kSelectScratchBytes = size_t(32) << 20;
+hipError_t select_scratch(void** out);
 hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int vocab, int width,
                          const float* logp, const float* beam, int* parents, int* tokens,
                          float* scores, void* workspace, hipStream_t st);

@@ -31,8 +31,16 @@
 // ranges, so position order inside a workgroup is index order, which is what
 // the tie rule needs.
 #include <algorithm>
+#include <mutex>
 
 #include "internal.h"
+
+// Device scratch of the allocation-free entry point (onela_select_beams_noalloc):
+// the workspace of a selection call, held by every GPU the library runs on
+// until the process ends.  Host code never uses this name as an address (in
+// host code it is a host-side stand-in): the device address comes from
+// hipGetSymbolAddress, once per device, in select_scratch below.
+static __device__ __align__(256) unsigned char scratch[onela::kSelectScratchBytes];
 
 namespace onela {
 namespace {
@@ -1232,6 +1240,28 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
     else select_final_kernel<false, false><<<R, kThreads, 0, st>>>(p);
   }
   return hipGetLastError();
+}
+
+// Device address of this GPU's scratch array (looked up once per device, with
+// that device current; each GPU holds its own copy at its own address).
+hipError_t select_scratch(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* cache[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cache[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    cache[dev] = p;
+  }
+  *out = cache[dev];
+  return hipSuccess;
 }
 
 }  // namespace onela

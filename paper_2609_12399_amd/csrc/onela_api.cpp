@@ -429,4 +429,29 @@ onela_status_t onela_select_beams(int32_t num_requests, int32_t prev_width, int3
   return e == hipSuccess ? ONELA_OK : ONELA_EHIP;
 }
 
+onela_status_t onela_select_beams_noalloc(int32_t num_requests, int32_t prev_width,
+                                          int32_t vocab, int32_t width, const float* logp,
+                                          const float* beam_scores, int32_t* parents_out,
+                                          int32_t* tokens_out, float* scores_out,
+                                          void* stream) {
+  size_t need = 0;
+  const onela_status_t st =
+      onela_select_workspace_bytes(num_requests, prev_width, vocab, width, &need);
+  if (st != ONELA_OK) return st;
+  if (need > onela::kSelectScratchBytes) return ONELA_ECAPACITY;
+  if (!logp || !parents_out || !tokens_out || !scores_out || !aligned4(logp) ||
+      !aligned4(parents_out) || !aligned4(tokens_out) || !aligned4(scores_out))
+    return ONELA_EINVAL;
+  if (beam_scores && !aligned4(beam_scores)) return ONELA_EINVAL;
+  void* ws = nullptr;
+  if (onela::select_scratch(&ws) != hipSuccess) return ONELA_EHIP;
+  onela::SelectPlan plan;
+  onela::select_plan(num_requests, unsigned(prev_width) * unsigned(vocab), unsigned(width),
+                     &plan);
+  const hipError_t e = onela::launch_select(plan, num_requests, prev_width, vocab, width, logp,
+                                            beam_scores, parents_out, tokens_out, scores_out,
+                                            ws, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ONELA_OK : ONELA_EHIP;
+}
+
 }  // extern "C"

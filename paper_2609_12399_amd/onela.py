@@ -32,7 +32,7 @@ EXPORTED = ["onela_status_str", "onela_check_config", "onela_workspace_bytes", "
             "onela_decode_step", "onela_decode_step_fused", "onela_get_device_status", "onela_destroy",
             "onela_prefill_state", "onela_fullstate_workspace_bytes", "onela_fullstate_step",
             "onela_capacity_bytes", "onela_fullstate_capacity_bytes",
-            "onela_select_workspace_bytes", "onela_select_beams",
+            "onela_select_workspace_bytes", "onela_select_beams", "onela_select_beams_noalloc",
             "onela_prefill_workspace_bytes", "onela_prefill_state_chunked"]
 
 
@@ -102,6 +102,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "onela_fullstate_capacity_bytes": ([_I32] * 6, ctypes.c_uint64),
         "onela_select_workspace_bytes": ([_I32] * 4 + [ctypes.POINTER(ctypes.c_size_t)], _I32),
         "onela_select_beams": ([_I32] * 4 + [_P] * 6 + [ctypes.c_size_t, _P], _I32),
+        "onela_select_beams_noalloc": ([_I32] * 4 + [_P] * 6, _I32),
         "onela_prefill_workspace_bytes": ([cfgp, _I32], ctypes.c_size_t),
         "onela_prefill_state_chunked": ([cfgp, _I32] + [_P] * 6 + [ctypes.c_size_t, _P], _I32),
     }
@@ -261,6 +262,16 @@ def onela_select_beams(num_requests: int, prev_width: int, vocab: int, width: in
         _dev(tokens_out, "tokens_out"), _dev(scores_out, "scores_out"),
         _dev(workspace, "workspace", optional=True), int(workspace_bytes), _stream(stream)),
         "onela_select_beams")
+
+
+def onela_select_beams_noalloc(num_requests: int, prev_width: int, vocab: int, width: int,
+                               logp, beam_scores, parents_out, tokens_out, scores_out,
+                               stream=None):
+    _check(load_library().onela_select_beams_noalloc(
+        num_requests, prev_width, vocab, width, _dev(logp, "logp"),
+        _dev(beam_scores, "beam_scores", optional=True), _dev(parents_out, "parents_out"),
+        _dev(tokens_out, "tokens_out"), _dev(scores_out, "scores_out"), _stream(stream)),
+        "onela_select_beams_noalloc")
 
 
 def onela_prefill_workspace_bytes(cfg: onela_config_t, prompt_len: int) -> int:
