@@ -275,12 +275,18 @@ onela_status_t onela_fullstate_step(const onela_config_t* cfg, int32_t step,
  *   tokens_out   device int32 [R][W]: its codebook entry v
  *   scores_out   device fp32 [R][W]: its candidate score (bit-exact)
  *   workspace    device, >= the size from onela_select_workspace_bytes,
- *                256-byte aligned (may be NULL when that size is 0); owned
- *                by the caller, used only during the enqueued work
+ *                256-byte aligned; owned by the caller.  It must be
+ *                zero-filled before its first use (e.g. one hipMemsetAsync
+ *                when it is allocated): its first 1 KiB holds per-request
+ *                counters that workgroups of one launch use to exchange a
+ *                bound, and every call leaves them at zero again, so a
+ *                workspace may serve any number of calls of any shape, one
+ *                at a time
  *   stream       hipStream_t (NULL: the default stream)
  * Limits: 1 <= R <= 65536, 1 <= W <= min(4096, W_prev * V),
  * W_prev * V <= 2^29.  All pointers 4-byte aligned.  Enqueued asynchronously;
- * the inputs must stay valid until the work has run.
+ * the inputs must stay valid until the work has run.  Calls sharing one
+ * workspace must not overlap (one stream, or the caller serialises them).
  * Errors: ONELA_EINVAL (limits, pointers), ONELA_ECAPACITY (workspace too
  * small), ONELA_EHIP. */
 onela_status_t onela_select_workspace_bytes(int32_t num_requests, int32_t prev_width,

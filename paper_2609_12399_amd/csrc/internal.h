@@ -104,6 +104,8 @@ constexpr int kSelectMaxWidth = 4096;          // W kept per request
 constexpr int kSelectMaxStages = 16;           // reduction stages before the final one
 constexpr unsigned kSelectMaxCandidates = 1u << 29;  // W_prev * V per request
 constexpr int kSelectMaxGatherSlots = 2048;          // chunks per request, two-pass path
+constexpr int kSelectOnePassMaxRequests = 64;        // requests of a one-pass call
+constexpr size_t kSelectCtlBytes = 1024;             // one-pass control block, workspace start
 
 // Launch plan (tree path).  Stage 0 reads the raw scores in nwg[0] chunks of
 // kSelectChunk per request; stage s >= 1 reads the nin[s] output slots of

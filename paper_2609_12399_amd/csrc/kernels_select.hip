@@ -53,6 +53,10 @@ constexpr int kMaxSlotsPerGroup = 256;
 constexpr int kRankCap = 4096;                // survivors the rank kernel orders
 constexpr int kRankPer = kThreads / 16;       // survivors ranked per workgroup (16 lanes each)
 constexpr int kRankBlocks = kRankCap / kRankPer;
+constexpr int kOnePassRankMax = 1024;         // widest result of the one-pass path
+constexpr int kOnePassFinalParts = 16;       // workgroups per request placing survivors
+constexpr int kOnePassSegPer = 8;             // wave summaries per thread of the bound:
+                                              // chunks <= kOnePassSegPer * kThreads / 8
 static_assert(kNI == 32, "validity masks are 32-bit");
 
 struct SelectParams {
@@ -73,7 +77,20 @@ struct SelectParams {
   unsigned nseg;
   unsigned nwg;             // workgroups per request
   double inv_v;             // 1 / V
+  // one-pass path
+  struct OnePassCtl* ctl;   // per-request counters and bound word
+  uint4* ex;                // [R][nseg] per wave: (M, m, kM, 0), see the one-pass path
+  unsigned long long wait_ticks;  // how long a workgroup waits for the bound (wall clock)
 };
+
+// Per-request cross-workgroup state of the one-pass path, at the start of the
+// workspace.  Zero when a call starts; the call's final kernel zeroes its
+// entries again.
+struct OnePassCtl {
+  unsigned arrive[kSelectOnePassMaxRequests];  // workgroups that published their summaries
+  unsigned long long bound[kSelectOnePassMaxRequests];  // (1 << 32) | bound, once known
+};
+static_assert(sizeof(OnePassCtl) <= kSelectCtlBytes, "control block fits its region");
 
 struct alignas(16) SelShared {
   unsigned hist[2048];  // exact cut: one 2048-bin histogram; bound: 8 x 256 bins
@@ -1093,11 +1110,558 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
   if (sub == 0u && i < total && cnt < p.W) emit_pick<BEAM>(p, r, cnt, mine);
 }
 
+// ---- one-pass path ---------------------------------------------------------
+// The two-pass path reads every score twice (wave maxima, then the filter).
+// When all R * nchunks workgroups of a call can be resident at once (and
+// R <= kSelectOnePassMaxRequests, W <= kOnePassRankMax), one pass over the
+// scores does the filtering, each chunk held in registers from its single
+// read, and a small second launch places the survivors:
+//   1. every wave publishes (M, m, kM): its largest key M, the smallest of
+//      its live lanes' largest keys m, and the number kM of lanes whose
+//      largest key is M.  Each lane's largest key is a distinct candidate,
+//      so the wave guarantees kM candidates at keys <= M and all its nl live
+//      lanes' candidates at keys <= m.  The workgroup then counts itself in
+//      the request's arrival counter;
+//   2. the workgroup that arrives last reads every wave's summary and takes
+//      as bound B a key at which the guaranteed count reaches W, so that no
+//      member of the top W lies below it: the floor of the bin where the
+//      count from the top reaches W after two 11-bit histogram passes (to
+//      2^-22 of the key range), raised to the next summary key.  It also finds the first chunk c* at which
+//      the chunks' guaranteed counts at B, summed in index order, reach W:
+//      a candidate of a later chunk whose key equals B has W better ones
+//      (equal or higher keys at lower indices), so it cannot be kept (this
+//      keeps tied scores from surviving in every chunk).  The others wait
+//      for the bound word for a bounded time; one that gives up keeps its
+//      chunk's exact top W instead (slower, never wrong);
+//   3. every workgroup keeps its candidates above B, or equal to B in a
+//      chunk up to c*, in its chunk's slot, in index order (the chunk's
+//      exact top W when they overflow it), with the count and the chunk's
+//      largest key;
+//   4. the final kernel places the survivors: each one's place is the number
+//      of larger (key, ~index) composites, counted through a key histogram
+//      (up to kRankCap survivors, staged in LDS by each of the request's
+//      kOnePassFinalParts workgroups, which place a share each); with more,
+//      one workgroup finds their exact top W first (radix cut, ties in index
+//      order, re-reading the slots on every pass).  It also returns the
+//      request's counters to zero.
+// The lane-level summaries make the bound tight also when the scores rise
+// with the beam (the top W all in the last rows): wave maxima alone then
+// guarantee only one candidate per wave.
+
+// Waits (thread 0) for the bound word of a request; 0 after `ticks`.
+__device__ inline unsigned long long wait_bound(unsigned long long* word,
+                                                unsigned long long ticks) {
+  const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
+  for (;;) {
+    const unsigned long long v = __hip_atomic_load(word, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+    if (v >> 32) return v;
+    if (static_cast<unsigned long long>(wall_clock64()) - t0 > ticks) return 0ull;
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// Data that crosses workgroups of one pass launch (the XCDs' L2 caches are
+// not coherent with each other) is written and read with agent-scope atomic
+// accesses: such stores write through to memory and such
+// loads bypass the compute unit's and the XCD's caches, so no cache-wide
+// write-back or invalidation (an agent-scope fence, several microseconds
+// with 256 workgroups issuing them) is needed.  A writer waits for its
+// stores to complete (vmcnt(0), the vector memory counter also covers
+// stores on this architecture) before it updates a counter.
+__device__ inline void st_agent(uint2* at, uint2 v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(at),
+                     (static_cast<unsigned long long>(v.y) << 32) | v.x, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint2 ld_agent(const uint2* at) {
+  const unsigned long long v =
+      __hip_atomic_load(const_cast<unsigned long long*>(reinterpret_cast<const unsigned long long*>(at)),
+                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_uint2(unsigned(v), unsigned(v >> 32));
+}
+__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+// Live lanes of wave w of chunk c (lanes holding at least one candidate).
+__device__ inline unsigned wave_live_lanes(const SelectParams& p, unsigned c, unsigned w) {
+  const unsigned nc = min(p.N - c * unsigned(kSelectChunk), unsigned(kSelectChunk));
+  const unsigned first = 64u * w;
+  return nc > first ? min(nc - first, 64u) : 0u;
+}
+
+// Bound word of request r from every wave's summary (see step 2 above):
+// ((c* + 1) << 32) | B.  All of a thread's summaries are loaded in one round
+// (nseg <= kOnePassSegPer * kThreads).
+__device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
+                                                   unsigned r) {
+  const unsigned nseg = p.nwg * unsigned(kWaves);
+  const uint2* ex = reinterpret_cast<const uint2*>(p.ex + size_t(r) * nseg);
+  const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
+  uint2 e[kOnePassSegPer], f[kOnePassSegPer];  // (M, m), (kM, -)
+#pragma unroll
+  for (int i = 0; i < kOnePassSegPer; ++i)
+    if (unsigned(i) * kThreads < nseg) {  // workgroup-uniform
+      const unsigned s = unsigned(i) * kThreads + t;
+      const unsigned sc = s < nseg ? s : 0u;
+      e[i] = ld_agent(ex + 2u * sc);
+      f[i] = ld_agent(ex + 2u * sc + 1u);
+    }
+  unsigned nl[kOnePassSegPer], lo = ~0u, hi = 0u;
+#pragma unroll
+  for (int i = 0; i < kOnePassSegPer; ++i) {
+    nl[i] = 0u;
+    if (unsigned(i) * kThreads < nseg) {
+      const unsigned s = unsigned(i) * kThreads + t;
+      nl[i] = s < nseg ? wave_live_lanes(p, s / kWaves, s % kWaves) : 0u;
+      if (nl[i] > 0u) {
+        lo = min(lo, e[i].y);
+        hi = max(hi, e[i].x);
+      }
+    }
+  }
+  const Red3 rr = block_reduce(sh, 0u, lo, hi);
+  unsigned B = rr.lo;
+  if (rr.lo < rr.hi) {
+    // radix passes over key - lo, each within the bin the previous one chose
+    int shift = bit_width(rr.hi - rr.lo);
+    unsigned prefix = 0u, need = p.W;
+    for (int pass = 0; pass < 2 && shift > 0; ++pass) {
+      const int bits = shift < 11 ? shift : 11;
+      shift -= bits;
+      const unsigned mask = (1u << bits) - 1u;
+      reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kOnePassSegPer; ++i)
+        if (nl[i] > 0u) {
+          const unsigned rm = e[i].x - rr.lo, rl = e[i].y - rr.lo;
+          if (shr(rm, shift + bits) == prefix) atomicAdd(&sh.hist[(rm >> shift) & mask], f[i].x);
+          if (nl[i] > f[i].x && shr(rl, shift + bits) == prefix)
+            atomicAdd(&sh.hist[(rl >> shift) & mask], nl[i] - f[i].x);
+        }
+      __syncthreads();
+      find_bin(sh, need);  // the live lanes (>= N / 32 >= W) always reach W
+      prefix = (prefix << bits) | sh.digit;
+      need = sh.need;
+    }
+    B = rr.lo + (prefix << shift);
+    // raise B to the smallest summary key at or above it: no guarantee
+    // changes in between, and a tie at the top then sits exactly at B
+    unsigned nb = ~0u;
+#pragma unroll
+    for (int i = 0; i < kOnePassSegPer; ++i)
+      if (nl[i] > 0u) {
+        if (e[i].x >= B) nb = min(nb, e[i].x);
+        if (e[i].y >= B) nb = min(nb, e[i].y);
+      }
+    B = block_reduce(sh, 0u, nb, 0u).lo;
+  }
+  // c*: guaranteed count of each chunk at B, summed in chunk order (chunk
+  // 4t + q in thread t, nchunks <= 4 * kThreads)
+  unsigned* gc = sh.hist;
+  reinterpret_cast<uint4*>(gc)[t] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kOnePassSegPer; ++i)
+    if (nl[i] > 0u) {
+      const unsigned g = e[i].y >= B ? nl[i] : (e[i].x >= B ? f[i].x : 0u);
+      if (g > 0u) atomicAdd(&gc[(unsigned(i) * kThreads + t) / kWaves], g);
+    }
+  __syncthreads();
+  const uint4 g4 = reinterpret_cast<const uint4*>(gc)[t];
+  const unsigned gs = g4.x + g4.y + g4.z + g4.w;
+  const unsigned inc = wave_scan(gs);
+  if (lane == 63) sh.red[0][w] = inc;
+  __syncthreads();
+  unsigned before = inc - gs;
+#pragma unroll
+  for (int w2 = 0; w2 < kWaves; ++w2) before += unsigned(w2) < w ? sh.red[0][w2] : 0u;
+  const unsigned gq[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (before < p.W && before + gq[q] >= p.W) sh.digit = 4u * t + unsigned(q);
+    before += gq[q];
+  }
+  __syncthreads();
+  return (static_cast<unsigned long long>(sh.digit + 1u) << 32) | B;
+}
+
+// LDS of the one-pass kernel.
+struct OnePassShared {
+  SelShared sh;
+  unsigned start[kSelectMaxGatherSlots + 1];      // slot s holds positions [start[s], start[s+1])
+  alignas(16) unsigned long long all[kRankCap];   // survivors' composites, when they fit
+  alignas(16) unsigned long long buck[kRankCap];  // the same, grouped by key bin
+  alignas(16) unsigned long long top[kOnePassRankMax];  // the exact top W
+  unsigned bstart[2048];                          // first position of each key bin in buck
+  unsigned ntop;
+};
+
+// Composite of a candidate: its key above its complemented flat index, so
+// that one 64-bit comparison orders by score, then by lower index.
+__device__ inline unsigned long long composite(uint2 e) {
+  return (static_cast<unsigned long long>(e.x) << 32) | unsigned(~e.y);
+}
+
+// Writes out each of the m (<= kRankCap) composites in `c` (LDS) whose
+// place among them -- the number of larger ones -- is below W.  The
+// composites are grouped by a 2048-bin histogram of key - lo (bins in
+// descending key order, so a bin's first position is the number of
+// composites in the bins above it); a composite's place is then its bin's
+// first position plus the larger composites of its own bin, which is
+// usually a handful (all of them only when the keys are nearly equal).
+template <bool BEAM>
+__device__ inline void bucket_rank_emit(const SelectParams& p, OnePassShared& u, unsigned r,
+                                        const unsigned long long* c, unsigned m,
+                                        unsigned part = 0u, unsigned nparts = 1u) {
+  SelShared& sh = u.sh;
+  const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
+  unsigned lo = ~0u, hi = 0u;
+  for (unsigned q = t; q < m; q += kThreads) {
+    const unsigned k = unsigned(c[q] >> 32);
+    lo = min(lo, k);
+    hi = max(hi, k);
+  }
+  const Red3 rr = block_reduce(sh, 0u, lo, hi);
+  if (m == 0u) return;
+  const int width = bit_width(rr.hi - rr.lo);
+  const int shift = width > 11 ? width - 11 : 0;
+  auto bin_of = [&](unsigned long long x) { return (unsigned(x >> 32) - rr.lo) >> shift; };
+  reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  for (unsigned q = t; q < m; q += kThreads) atomicAdd(&sh.hist[bin_of(c[q])], 1u);
+  __syncthreads();
+  {  // bstart[b] = composites in bins above b; thread t holds bins 2047 - 4t .. 2044 - 4t
+    const uint4 h = reinterpret_cast<const uint4*>(sh.hist)[kThreads - 1 - t];
+    const unsigned sum = h.x + h.y + h.z + h.w;
+    const unsigned inc = wave_scan(sum);
+    if (lane == 63) sh.red[0][w] = inc;
+    __syncthreads();
+    unsigned above = inc - sum;
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2) above += unsigned(w2) < w ? sh.red[0][w2] : 0u;
+    const unsigned b0 = 2047u - 4u * t;
+    u.bstart[b0] = above;
+    u.bstart[b0 - 1u] = above + h.w;
+    u.bstart[b0 - 2u] = above + h.w + h.z;
+    u.bstart[b0 - 3u] = above + h.w + h.z + h.y;
+  }
+  __syncthreads();
+  reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);  // now per-bin cursors
+  __syncthreads();
+  for (unsigned q = t; q < m; q += kThreads) {
+    const unsigned long long x = c[q];
+    const unsigned b = bin_of(x);
+    u.buck[u.bstart[b] + atomicAdd(&sh.hist[b], 1u)] = x;
+  }
+  __syncthreads();
+  // this workgroup's share: composites part, part + nparts, ... of c (the
+  // order within a bin of `buck` differs between workgroups, the order of c
+  // does not), 16 lanes each (they split the bin's comparisons)
+  const unsigned sub = t & 15u;
+  for (unsigned k = t >> 4;; k += kThreads / 16u) {
+    const unsigned q = part + nparts * k;
+    if (part + nparts * (k - (t >> 4)) >= m) break;  // workgroup-uniform: no group has work
+    const unsigned long long x = c[q < m ? q : 0u];
+    const unsigned b = bin_of(x);
+    const unsigned s0 = u.bstart[b], e0 = b > 0u ? u.bstart[b - 1u] : m;
+    unsigned cnt = 0u;
+    if (q < m)
+      for (unsigned i = s0 + sub; i < e0; i += 16u) cnt += unsigned(u.buck[i] > x);
+    cnt += dppu<0xB1>(cnt);   // quad_perm [1,0,3,2]
+    cnt += dppu<0x4E>(cnt);   // quad_perm [2,3,0,1]
+    cnt += dppu<0x141>(cnt);  // row_half_mirror
+    cnt += dppu<0x140>(cnt);  // row_mirror
+    if (sub == 0u && q < m && s0 + cnt < p.W) emit_pick<BEAM>(p, r, s0 + cnt, x);
+  }
+}
+
+// The exact top W (W <= kOnePassRankMax <= n) of the n survivors of request
+// r, read through get(q) in position (= index) order: radix passes of up to
+// 11 bits over key - lo find the cut (every key above tau is in, and of the
+// keys equal to tau the first `take` by position, or all keys >= tau when
+// take = 0), the kept composites are collected in LDS, and each is placed by
+// the number of larger ones.
+template <bool BEAM, typename Get>
+__device__ inline void onepass_topw(const SelectParams& p, OnePassShared& u, unsigned r,
+                                    unsigned n, Get&& get) {
+  const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
+  SelShared& sh = u.sh;
+  const unsigned W = p.W;
+  unsigned tau = 0u, take = 0u;
+  bool all_in = n <= W;
+  if (!all_in) {
+    unsigned lo = ~0u, hi = 0u;
+    for (unsigned q = t; q < n; q += kThreads) {
+      const unsigned k = unsigned(get(q) >> 32);
+      lo = min(lo, k);
+      hi = max(hi, k);
+    }
+    const Red3 rr = block_reduce(sh, 0u, lo, hi);
+    if (rr.lo == rr.hi) {  // all equal: the first W by position
+      tau = rr.lo;
+      take = W;
+    } else {
+      int shift = bit_width(rr.hi - rr.lo);
+      unsigned prefix = 0u, need = W;  // of key - lo
+#pragma nounroll
+      for (;;) {
+        const int bits = shift < 11 ? shift : 11;
+        shift -= bits;
+        reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
+        __syncthreads();
+        const unsigned mask = (1u << bits) - 1u;
+        for (unsigned q = t; q < n; q += kThreads) {
+          const unsigned rel = unsigned(get(q) >> 32) - rr.lo;
+          if (shr(rel, shift + bits) == prefix) atomicAdd(&sh.hist[(rel >> shift) & mask], 1u);
+        }
+        __syncthreads();
+        find_bin(sh, need);
+        prefix = (prefix << bits) | sh.digit;
+        need = sh.need;
+        const unsigned cnt = sh.cnt;
+        if (cnt == need) {  // the boundary bin is taken whole
+          tau = rr.lo + (prefix << shift);
+          take = 0u;
+          break;
+        }
+        if (shift == 0) {
+          tau = rr.lo + prefix;
+          take = need;
+          break;
+        }
+      }
+    }
+  }
+  if (t == 0) u.ntop = 0u;
+  __syncthreads();
+  unsigned eq_before = 0u;  // keys equal to tau at earlier positions
+  for (unsigned base = 0u; base < n; base += kThreads) {
+    const unsigned q = base + t;
+    const bool valid = q < n;
+    const unsigned long long c = valid ? get(q) : 0ull;
+    const unsigned k = unsigned(c >> 32);
+    bool sel = valid && (all_in || (take == 0u ? k >= tau : k > tau));
+    if (take > 0u) {  // workgroup-uniform
+      const bool eq = valid && k == tau;
+      const unsigned long long be = __ballot(eq);
+      if (lane == 0) sh.red[0][w] = unsigned(__popcll(be));
+      __syncthreads();
+      unsigned before = eq_before, round = 0u;
+#pragma unroll
+      for (int w2 = 0; w2 < kWaves; ++w2) {
+        const unsigned x = sh.red[0][w2];
+        round += x;
+        before += unsigned(w2) < w ? x : 0u;
+      }
+      if (eq && before + mbcnt(be) < take) sel = true;
+      eq_before += round;
+      __syncthreads();  // sh.red is rewritten next round
+    }
+    if (sel) {
+      const unsigned at = atomicAdd(&u.ntop, 1u);
+      if (at < unsigned(kOnePassRankMax)) u.top[at] = c;
+    }
+  }
+  __syncthreads();
+  bucket_rank_emit<BEAM>(p, u, r, u.top, min(u.ntop, unsigned(kOnePassRankMax)));
+}
+
+// Final stage of request r in its last workgroup (every chunk's slot and
+// (count, largest key) pair are stored): survivors of up to kRankCap are
+// staged in LDS first, more are read from the slots on every pass.
+template <bool BEAM>
+__device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, unsigned r,
+                                     unsigned part, unsigned nparts) {
+  const unsigned ns = p.nwg, t = threadIdx.x;
+  const unsigned lane = lane_id(), w = t >> 6;
+  SelShared& sh = u.sh;
+  unsigned c4[4], sum = 0u;
+  {
+    const uint2* cm = reinterpret_cast<const uint2*>(p.cnt_out) + size_t(r) * ns;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const unsigned sl = 4u * t + unsigned(q);
+      c4[q] = sl < ns ? cm[sl].x : 0u;
+      sum += c4[q];
+    }
+  }
+  const unsigned inc = wave_scan(sum);
+  if (lane == 63) sh.red[0][w] = inc;
+  __syncthreads();
+  unsigned run = inc - sum, total = 0u;
+#pragma unroll
+  for (int w2 = 0; w2 < kWaves; ++w2) {
+    const unsigned x = sh.red[0][w2];
+    total += x;
+    run += unsigned(w2) < w ? x : 0u;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const unsigned sl = 4u * t + unsigned(q);
+    if (sl < ns) u.start[sl] = run;
+    run += c4[q];
+  }
+  if (t == 0) u.start[ns] = total;
+  __syncthreads();
+  const uint2* slots = p.cand_out + size_t(r) * ns * p.cap;
+  // position q lies in the last slot whose start is <= q
+  auto from_slots = [&](unsigned q) -> unsigned long long {
+    unsigned lo = 0u, hi = ns;  // start[lo] <= q < start[hi]
+    while (hi - lo > 1u) {
+      const unsigned mid = (lo + hi) >> 1;
+      if (u.start[mid] <= q) lo = mid;
+      else hi = mid;
+    }
+    return composite(slots[size_t(lo) * p.cap + (q - u.start[lo])]);
+  };
+  if (total > unsigned(kRankCap)) {  // rare (heavy ties, or a bound that came late)
+    if (part == 0u) onepass_topw<BEAM>(p, u, r, total, from_slots);
+    return;
+  }
+  constexpr int kNR = kRankCap / kThreads;
+  unsigned long long c[kNR];
+#pragma unroll
+  for (int i = 0; i < kNR; ++i) {
+    const unsigned q = unsigned(i) * kThreads + t;
+    c[i] = q < total ? from_slots(q) : 0ull;
+  }
+#pragma unroll
+  for (int i = 0; i < kNR; ++i) {
+    const unsigned q = unsigned(i) * kThreads + t;
+    if (q < total) u.all[q] = c[i];
+  }
+  __syncthreads();
+  bucket_rank_emit<BEAM>(p, u, r, u.all, total, part, nparts);
+}
+
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p) {
+  __shared__ SelShared sh;
+  __shared__ unsigned flag[2];
+  __shared__ unsigned wmax[kWaves];
+  const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
+  const unsigned base = c * unsigned(kSelectChunk);
+  const unsigned n = min(p.N - base, unsigned(kSelectChunk));
+  const unsigned t = threadIdx.x, w = t >> 6;
+  unsigned key[kNI];
+  const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
+  // 1. this wave's (M, m), published; the workgroup counts itself in
+  unsigned lmax = 0u;  // invalid slots hold key 0
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) lmax = max(lmax, key[i]);
+  const Red3 wr = wave_reduce(0u, (vm & 1u) ? lmax : ~0u, lmax);
+  const unsigned km = unsigned(__popcll(__ballot((vm & 1u) && lmax == wr.hi)));
+  if (lane_id() == 0) {
+    uint2* e = reinterpret_cast<uint2*>(p.ex + size_t(r) * p.nseg + c * kWaves + w);
+    st_agent(e, make_uint2(wr.hi, wr.lo));
+    st_agent(e + 1, make_uint2(km, 0u));
+    wmax[w] = wr.hi;
+  }
+  wait_stores();
+  __syncthreads();
+  if (t == 0) flag[0] = atomicAdd(&p.ctl->arrive[r], 1u) == p.nwg - 1u;
+  __syncthreads();
+  // 2. the bound: computed by the last arrival, waited for by the others
+  unsigned bound;  // keys below it are dropped
+  if (flag[0]) {
+    const unsigned long long bw = onepass_bound(p, sh, r);
+    if (t == 0)
+      __hip_atomic_store(&p.ctl->bound[r], bw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
+    bound = (c > cstar && B < ~0u) ? B + 1u : B;
+  } else {
+    if (t == 0) {
+      const unsigned long long bw = wait_bound(&p.ctl->bound[r], p.wait_ticks);
+      const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
+      // 0 after a timeout: no bound
+      flag[1] = bw == 0ull ? 0u : ((c > cstar && B < ~0u) ? B + 1u : B);
+    }
+    __syncthreads();
+    bound = flag[1];
+  }
+  // 3. survivors into the chunk's slot (as the filter kernel); the final
+  // kernel reads them after this launch has ended
+  unsigned keep = vm;
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < bound) << i);
+  Ordered o = ordered_plan(keep, sh);
+  if (o.total > p.cap) {  // a chunk's exact top W of its survivors
+    __syncthreads();
+    keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
+    o = ordered_plan(keep, sh);
+  }
+  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
+  ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
+    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + t);
+  });
+  if (t == 0) {
+    unsigned top = 0u;
+#pragma unroll
+    for (int w2 = 0; w2 < kWaves; ++w2) top = max(top, wmax[w2]);
+    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(o.total, top);
+  }
+}
+
+// 4. kOnePassFinalParts workgroups per request, after the pass: each stages
+// all survivors and places its share of them; the first also returns the
+// request's counters to zero for the next call.
+template <bool BEAM>
+__global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectParams p) {
+  __shared__ OnePassShared u;
+  const unsigned r = blockIdx.x / kOnePassFinalParts;
+  const unsigned part = blockIdx.x - r * kOnePassFinalParts;
+  if (threadIdx.x == 0 && part == 0u) {
+    p.ctl->arrive[r] = 0u;
+    p.ctl->bound[r] = 0ull;
+  }
+  onepass_final<BEAM>(p, u, r, part, kOnePassFinalParts);
+}
+
 unsigned pow2_ceil(unsigned x) {
   unsigned y = 1;
   while (y < x) y <<= 1;
   return y;
 }
+
+// Workgroups of the one-pass kernel that can be resident at once on the
+// current device (all of a call's workgroups must be, or they would wait on
+// ones that cannot start), and its wait for the bound in wall-clock ticks;
+// both queried once per device.
+struct OnePassDevice {
+  unsigned capacity;
+  unsigned long long wait_ticks;
+};
+OnePassDevice onepass_device() {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static OnePassDevice cache[kMaxDevices] = {};
+  static bool known[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return {0u, 0ull};
+  std::lock_guard<std::mutex> lock(mu);
+  if (!known[dev]) {
+    OnePassDevice d{0u, 0ull};
+    int cus = 0, per_cu_a = 0, per_cu_b = 0, khz = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu_a, reinterpret_cast<const void*>(select_onepass_kernel<true>), kThreads, 0) ==
+            hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu_b, reinterpret_cast<const void*>(select_onepass_kernel<false>), kThreads, 0) ==
+            hipSuccess &&
+        hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) == hipSuccess &&
+        cus > 0 && khz > 0) {
+      d.capacity = unsigned(cus) * unsigned(std::min(per_cu_a, per_cu_b));
+      d.wait_ticks = 20ull * unsigned(khz) / 1000ull;  // 20 us
+    }
+    cache[dev] = d;
+    known[dev] = true;
+  }
+  return cache[dev];
+}
+unsigned onepass_capacity() { return onepass_device().capacity; }
+unsigned long long onepass_wait_ticks() { return onepass_device().wait_ticks; }
 
 }  // namespace
 
@@ -1115,6 +1679,10 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
   plan->group = unsigned(kSelectChunk) / cap;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   const unsigned nchunks = (N + kSelectChunk - 1) / kSelectChunk;
+  // Every plan starts with the one-pass path's control block, which no other
+  // data overwrites, so that a workspace shared by calls of any shape keeps
+  // its counters at zero between calls.
+  const size_t ctl = kSelectCtlBytes;
   // Two-pass path: enough wave maxima (2048 candidates each) for a tight
   // bound, few enough chunks for the one-workgroup gather.
   if (N > unsigned(kSelectChunk) && uint64_t(N) >= uint64_t(2) * W * 2048u &&
@@ -1122,8 +1690,8 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
     plan->two_pass = true;
     plan->nchunks = nchunks;
     plan->nseg = nchunks * (kSelectThreads / 64);
-    plan->seg_off = 0;
-    plan->slot_off = up(size_t(R) * plan->nseg * sizeof(unsigned));
+    plan->seg_off = ctl;  // [R][nseg] wave summaries: uint4 (one-pass), uint32 (two-pass)
+    plan->slot_off = ctl + up(size_t(R) * plan->nseg * sizeof(uint4));
     plan->cnt_off = plan->slot_off + up(size_t(R) * nchunks * cap * sizeof(uint2));
     plan->total = plan->cnt_off + up(size_t(R) * nchunks * sizeof(uint2));
     return true;
@@ -1152,7 +1720,7 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
     plan->final_in = N;
   }
   plan->stages = s;
-  size_t off = 0;
+  size_t off = ctl;
   for (int b = 0; b < 2; ++b) {
     plan->pair_off[b] = off;
     off += up(pairs[b]);
@@ -1182,6 +1750,26 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
   p.inv_v = 1.0 / double(vocab);
   char* ws = static_cast<char*>(workspace);
   const bool has_beam = beam != nullptr;
+  if (plan.two_pass && R <= kSelectOnePassMaxRequests && width <= kOnePassRankMax &&
+      plan.nseg <= unsigned(kOnePassSegPer * kThreads) &&
+      unsigned(R) * plan.nchunks <= onepass_capacity()) {
+    p.ctl = reinterpret_cast<OnePassCtl*>(ws);
+    p.ex = reinterpret_cast<uint4*>(ws + plan.seg_off);
+    p.nseg = plan.nseg;
+    p.nwg = plan.nchunks;
+    p.cand_out = reinterpret_cast<uint2*>(ws + plan.slot_off);
+    p.cnt_out = reinterpret_cast<unsigned*>(ws + plan.cnt_off);
+    p.wait_ticks = onepass_wait_ticks();
+    const unsigned blocks = unsigned(R) * plan.nchunks;
+    if (has_beam) select_onepass_kernel<true><<<blocks, kThreads, 0, st>>>(p);
+    else select_onepass_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned fblocks = unsigned(R) * kOnePassFinalParts;
+    if (has_beam) select_onepass_final_kernel<true><<<fblocks, kThreads, 0, st>>>(p);
+    else select_onepass_final_kernel<false><<<fblocks, kThreads, 0, st>>>(p);
+    return hipGetLastError();
+  }
   if (plan.two_pass) {
     p.segmax = reinterpret_cast<unsigned*>(ws + plan.seg_off);
     p.nseg = plan.nseg;

@@ -186,8 +186,9 @@ class BeamSelector:
         torch = _torch()
         self.R, self.prev_width, self.vocab, self.width = R, prev_width, vocab, width
         self.ws_bytes = ab.onela_select_workspace_bytes(R, prev_width, vocab, width)
-        self.workspace = (torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
-                          if self.ws_bytes else None)
+        # zero-filled once: the selection keeps its cross-workgroup counters
+        # here and returns them to zero after every call
+        self.workspace = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
         self.parents = torch.empty((R, width), dtype=torch.int32, device=device)
         self.tokens = torch.empty((R, width), dtype=torch.int32, device=device)
         self.scores = torch.empty((R, width), dtype=torch.float32, device=device)

@@ -37,6 +37,14 @@ CASES = [
     # rising beam scores: many survivors, each gather round beats the last
     ("two_pass_rising_rounds", 1, 512, SELECT_CODEBOOK, 512, "rising", True),
     ("two_pass_rising_r2_w1024", 2, 1024, 4096, 1024, "rising", True),
+    # one launch with a cross-workgroup bound (all chunks resident at once):
+    # ragged last chunk, ties cut off after the chunk where W tied candidates
+    # are guaranteed, special values over two requests, rising scores at the
+    # widest result it takes
+    ("one_pass_ragged", 1, 500, 8000, 300, "logsoftmax", True),
+    ("one_pass_ties_w64", 1, 300, SELECT_CODEBOOK, 64, "ties", True),
+    ("one_pass_r2_special", 2, 100, SELECT_CODEBOOK, 200, "special", True),
+    ("one_pass_rising_w1024", 1, 1024, 4096, 1024, "rising", True),
 ]
 
 
@@ -85,3 +93,66 @@ def test_select_deterministic_and_feeds_resolve():
     for x, y in zip(a[2:], b[2:]):
         assert np.array_equal(x.view(np.int32), y.view(np.int32))
     assert a[2].min() >= 0 and a[2].max() < P
+
+
+def _check(logp, beam, W, par, tok, sc):
+    for r in range(logp.shape[0]):
+        op, ot, osc = orc.select_beams(logp[r], W, None if beam is None else beam[r])
+        assert np.array_equal(par[r], op), f"request {r}: parents differ"
+        assert np.array_equal(tok[r], ot), f"request {r}: tokens differ"
+        assert np.array_equal(sc[r].view(np.int32), osc.view(np.int32)), \
+            f"request {r}: scores differ"
+
+
+def test_select_shared_workspace_across_shapes():
+    """One zero-filled workspace serves a sequence of calls of different
+    shapes and paths (one launch with a cross-workgroup bound, reduction
+    tree, wave-maxima two-pass, the one-launch path again): each call leaves
+    the counters the next one relies on at zero."""
+    import torch
+    shapes = [(1, 512, SELECT_CODEBOOK, 512, "logsoftmax"), (3, 37, 1001, 300, "ties"),
+              (2, 600, 4096, 256, "logsoftmax"), (1, 64, SELECT_CODEBOOK, 64, "rising"),
+              (2, 256, SELECT_CODEBOOK, 128, "logsoftmax"), (1, 512, SELECT_CODEBOOK, 512, "ties")]
+    need = max(ab.onela_select_workspace_bytes(R, P, V, W) for R, P, V, W, _ in shapes)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (R, P, V, W, kind) in enumerate(shapes):
+        print(f"shared workspace call {i}: R={R} W_prev={P} V={V} W={W} {kind}", flush=True)
+        logp, beam = make_select_inputs(R, P, V, 60 + i, kind, True)
+        par = torch.empty((R, W), dtype=torch.int32, device="cuda")
+        tok = torch.empty((R, W), dtype=torch.int32, device="cuda")
+        sc = torch.empty((R, W), dtype=torch.float32, device="cuda")
+        ab.onela_select_beams(R, P, V, W, torch.from_numpy(logp).cuda(),
+                              torch.from_numpy(beam).cuda(), par, tok, sc, ws, need)
+        torch.cuda.synchronize()
+        _check(logp, beam, W, par.cpu().numpy(), tok.cpu().numpy(), sc.cpu().numpy())
+
+
+def test_select_graph_replays_with_new_scores():
+    """The headline selection captured once in a HIP graph and replayed with
+    new scores copied into its input buffers between replays (eager work
+    and synchronisation in between): every replay matches the oracle."""
+    import torch
+    from paper_2609_12399_amd.runner import BeamSelector
+    R, P, V, W = 1, 512, SELECT_CODEBOOK, 512
+    logp0, beam0 = make_select_inputs(R, P, V, 70, "logsoftmax", True)
+    dl = torch.from_numpy(logp0).cuda()
+    db = torch.from_numpy(beam0).cuda()
+    s = torch.cuda.Stream()
+    sel = BeamSelector(R, P, V, W, stream=s)
+    with torch.cuda.stream(s):
+        sel(dl, db)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        sel(dl, db)
+    torch.cuda.synchronize()
+    for rep, kind in enumerate(["logsoftmax", "rising", "logsoftmax", "ties"]):
+        logp, beam = make_select_inputs(R, P, V, 80 + rep, kind, True)
+        dl.copy_(torch.from_numpy(logp))
+        db.copy_(torch.from_numpy(beam))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        print(f"graph replay {rep} ({kind})", flush=True)
+        _check(logp, beam, W, sel.parents.cpu().numpy(), sel.tokens.cpu().numpy(),
+               sel.scores.cpu().numpy())
