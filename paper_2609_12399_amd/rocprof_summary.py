@@ -3,6 +3,7 @@
     python -m paper_2609_12399_amd.rocprof_summary trace <dir-or-file>
     python -m paper_2609_12399_amd.rocprof_summary pmc <FETCH_SIZE dir> <WRITE_SIZE dir>
     python -m paper_2609_12399_amd.rocprof_summary mfma <counter dir> [<trace dir>]
+    python -m paper_2609_12399_amd.rocprof_summary counters <kernel-substring> <dir> [<dir> ...]
 
 ``trace`` reads a ``--kernel-trace`` result (``*_kernel_trace.csv`` or a
 ``*_results.db``) and prints one markdown row per kernel instance (calls,
@@ -16,7 +17,9 @@ GRBM_GUI_ACTIVE`` run and prints, per kernel, the bf16 MFMA flops per dispatch
 (MOPS x 512), the matrix-core busy fraction (busy cycles over active cycles
 times the 1024 SIMDs, rocprofv3's MfmaUtil; the CSV sums GRBM_GUI_ACTIVE over
 the 8 XCDs, so one XCD's active cycles are taken as that sum / 8) and, given a
-kernel trace of the same command, the achieved bf16 MFMA rate.
+kernel trace of the same command, the achieved bf16 MFMA rate.  ``counters``
+reads any number of ``--pmc`` runs and prints, for every kernel whose short
+name contains the substring, the average per dispatch of each counter found.
 """
 from __future__ import annotations
 
@@ -184,11 +187,32 @@ def summarize_mfma(counter_dir: str, trace_dir: str | None = None) -> str:
     return "\n".join(out)
 
 
+def summarize_counters(sub: str, dirs) -> str:
+    acc = defaultdict(lambda: defaultdict(list))
+    names = []
+    for d in dirs:
+        for name, grid, wg, cname, val in pmc_rows(d):
+            k = short_name(name)
+            if sub not in k:
+                continue
+            acc[(k, grid // max(wg, 1))][cname].append(val)
+            if cname not in names:
+                names.append(cname)
+    out = ["| kernel | workgroups | " + " | ".join(names) + " |",
+           "|---|---|" + "---|" * len(names)]
+    for (k, g), c in sorted(acc.items()):
+        vals = [f"{sum(c[n]) / len(c[n]):.4g}" if c.get(n) else "-" for n in names]
+        out.append(f"| {k} | {g} | " + " | ".join(vals) + " |")
+    return "\n".join(out)
+
+
 if __name__ == "__main__":
     if len(sys.argv) >= 3 and sys.argv[1] == "trace":
         print(summarize_trace(sys.argv[2]))
     elif len(sys.argv) >= 4 and sys.argv[1] == "pmc":
         print(summarize_pmc(sys.argv[2], sys.argv[3]))
+    elif len(sys.argv) >= 4 and sys.argv[1] == "counters":
+        print(summarize_counters(sys.argv[2], sys.argv[3:]))
     elif len(sys.argv) >= 3 and sys.argv[1] == "mfma":
         print(summarize_mfma(sys.argv[2], sys.argv[3] if len(sys.argv) > 3 else None))
     else:
