@@ -75,6 +75,24 @@ def measured_traffic(workload: str, variant: str):
     return None
 
 
+SELECT_SRC = os.path.join(ROOT, "paper_2609_12399_amd", "csrc", "kernels_select.hip")
+SELECT_PROFILE = os.path.join(ROOT, "profiles", "select_beams_r1_wprev512_v8192_w512_kernel_trace.md")
+
+
+def measured_select_traffic(workload: str):
+    """HBM bytes per selection call from the committed selection profile, or
+    None when it is missing, for another shape, or taken on another source."""
+    if not os.path.exists(SELECT_PROFILE):
+        return None
+    want = hashlib.sha256(open(SELECT_SRC, "rb").read()).hexdigest()
+    for line in open(SELECT_PROFILE):
+        if line.startswith("bench-select-traffic: "):
+            rec = json.loads(line[len("bench-select-traffic: "):])
+            if rec.get("select_source_sha256") == want and rec.get("workload") == workload:
+                return rec["bytes_per_call"]
+    return None
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -673,6 +691,8 @@ def main():
             "achieved_GBs": sel_bytes / (sel_us * 1e-6) / 1e9,
             "frac_of_hbm_peak": sel_bytes / (sel_us * 1e-6) / 8.0e12,
             "torch_topk_us": topk_us,
+            "traffic_bytes_per_call": measured_select_traffic(f"R{spec.R}_wprev{wp}_v{vocab}_w{wp}"),
+            "traffic_source": os.path.relpath(SELECT_PROFILE, ROOT),
             "note": "onela_select_beams (fused beam-score add, total order); torch.topk is "
                     "timed on precomputed scores as a reference only"}
         log(f"[bench] beam selection {sel_us:.1f} us/call ({wp}x{vocab} -> {wp}), "
