@@ -64,7 +64,9 @@ typedef enum { ONELA_F32 = 0, ONELA_BF16 = 1 } onela_dtype_t;
  *   Sec. 3.2 (Eq. 2), delta_t = beta_t (v_t - alpha_t S_{t-1} k_t), computed
  *   and appended by the decode step, which replays the ancestral records on
  *   the two projections S_ctx q_t and S_ctx k_t (Eqs. 3-4).  delta is stored
- *   in fp16 for bf16 io (fp32 for fp32 io). */
+ *   in fp16 for bf16 io, scaled per row slice by a power of two that puts
+ *   the row's largest magnitude at 2^14 (so neither fp16 overflow nor its
+ *   subnormal range limits the inputs' magnitude), and in fp32 for fp32 io. */
 typedef enum { ONELA_RECORD_INPUTS = 0, ONELA_RECORD_DELTA = 1 } onela_record_kind_t;
 
 /* Where ONELA_RECORD_INPUTS records live (Sec. 3.3: a step's records are
@@ -112,7 +114,8 @@ onela_status_t onela_check_config(const onela_config_t* cfg);
  * are borrowed, the record arena: k [R][T_max][H_K][W_max][d_k],
  * v [R][T_max][H_V][W_max][d_v] in the io dtype, (alpha, beta)
  * [R][T_max][H_V][W_max] fp32 pairs and, for ONELA_RECORD_DELTA,
- * delta [R][T_max][H_V][W_max][d_v] (fp16 / fp32). */
+ * delta [R][T_max][H_V][W_max][d_v] (fp16 / fp32) and, per delta row, a
+ * 32-bit word of int8 scale exponents [R][T_max][H_V][W_max]. */
 size_t onela_workspace_bytes(const onela_config_t* cfg);
 
 /* Creates a decode context and binds the shared post-prefill state

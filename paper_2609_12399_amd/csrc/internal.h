@@ -43,6 +43,7 @@ struct Arena {
   void* v;           // [R][tmax][HV][wmax][dv] io dtype
   float2* ab;        // [R][tmax][HV][wmax] (alpha, beta)
   void* d;           // delta records [R][tmax][HV][wmax][dv], fp16 (bf16 io) / fp32; or null
+  unsigned* dsc;     // per delta row: one int8 scale exponent per row slice [R][tmax][HV][wmax]
   // borrowed records (Shape::borrow): the caller's buffers of step j,
   // k [R][w[j]][HK][dk], v [R][w[j]][HV][dv], alpha / beta [R][w[j]][HV]
   const void* bk[kMaxSteps];
@@ -54,7 +55,7 @@ struct Arena {
 
 // Bytes of each region, in workspace order, each rounded up to 256.
 struct Layout {
-  size_t status, anc, s_frag, k, v, ab, d, total;
+  size_t status, anc, s_frag, k, v, ab, d, ds, total;
 };
 Layout layout_of(const Shape& s);
 

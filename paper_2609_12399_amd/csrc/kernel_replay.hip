@@ -28,7 +28,11 @@
 //
 // delta is stored in fp16 for bf16 inputs (fp32 for fp32 inputs): the paper's
 // record is a 32-bit decay with 16-bit delta and key vectors; bf16 would cost
-// ~8x more error.  MODE: DECODE reads the step-t record from the arena (after
+// ~8x more error.  fp16 alone would bound the magnitudes the inputs may have
+// (values above 65504 overflow, values below 2^-14 lose bits), so each row
+// slice of delta_t is stored divided by 2^e, with e chosen from the slice's
+// largest magnitude (which then lies in [2^14, 2^15)); e is kept as an int8
+// per slice, four to a 32-bit word per row.  MODE: DECODE reads the step-t record from the arena (after
 // onela_append_records); FUSED reads it from the caller and performs the
 // ancestry update and the append in the same launch.
 #include "device_common.h"
@@ -53,6 +57,7 @@ struct ReplayParams {
   void* av;    // arena step inputs v (DECODE mode reads step t from here)
   float2* ab;  // arena (alpha, beta)
   void* ad;    // arena delta [R][tmax][HV][wmax][dv], fp16 (bf16 io) or fp32
+  unsigned* adsc;  // arena delta scale exponents [R][tmax][HV][wmax], int8 per slice
   const int* anc_rd;
   int* anc_wr;
   int R, HK, HV, G, W, W_prev, wmax, tmax;
@@ -178,6 +183,7 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
     return static_cast<char*>(p.ad) + ((long(r) * tmax + j) * p.HV + hv) * wmax * long(vslot);
   };
   auto ab_slab = [&](int j) { return p.ab + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
+  auto ds_slab = [&](int j) { return p.adsc + ((long(r) * tmax + j) * p.HV + hv) * wmax; };
 
   // ---- round 1: indices, then query and the beam's step-t inputs.  Every
   // load is made by the fold lanes of the beam, as whole lines (see the
@@ -216,6 +222,7 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   K8 qr[C8], kt[C8];
   K8 kr[NAX][C8];
   float alr[NAX];
+  unsigned esc[NAX];  // scale exponents of the ancestral delta rows (bf16 io)
   float2 abt;
   VL vt;
   VL dr[NAX];
@@ -260,6 +267,7 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
 #pragma unroll
     for (int c = 0; c < C8; ++c) kr[j][c].load(ks, slot * kslot + li * EPL * IOB + c * K8::kBytes);
     alr[j] = ab_slab(j)[slot].x;
+    if constexpr (BF16) esc[j] = ds_slab(j)[slot];
     dr[j].load(d_slab(j), slot * vslot + voff);
   };
   if constexpr (FUSED && NA > 0) {
@@ -416,6 +424,11 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       const float wq = fok[j] ? decay * cq[j] : 0.f, wk = fok[j] ? decay * ck[j] : 0.f;
       float dj[VPL];
       delta_to_float<BF16>(dr[j].w, dj, VPL);
+      if constexpr (BF16) {
+        const int e = int(static_cast<signed char>((esc[j] >> (8 * slice)) & 0xffu));
+#pragma unroll
+        for (int x = 0; x < VPL; ++x) dj[x] = ldexpf(dj[x], e);
+      }
 #pragma unroll
       for (int e = 0; e < VPL; ++e) {
         rq[e] = fmaf(wq, dj[e], rq[e]);
@@ -468,6 +481,8 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
   __syncthreads();
 
   // ---- phase 4: Eq. 4 per output row; append delta_t
+  __shared__ float mx_lds[NW][BEAMS];  // per wave and beam: largest |delta_t| of its rows
+  float dts[NBLK][RPL];
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb) {
     const int bl = nb * 16 + (lane & 15);
@@ -493,9 +508,44 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       for (int i = 0; i < MB; ++i)  // o is not read again: streaming stores
         __builtin_nontemporal_store(f32x4{ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]},
                                     reinterpret_cast<f32x4*>(dst + i));
+    }
+    float mx = 0.f;
+#pragma unroll
+    for (int e = 0; e < RPL; ++e) {
+      dts[nb][e] = dt[e];
+      mx = fmaxf(mx, fabsf(dt[e]));
+    }
+    if constexpr (BF16) {  // the beam's 4 lane groups of this wave, then the waves
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (g4 == 0) mx_lds[w][bl] = mx;
+    }
+  }
+  if constexpr (BF16) __syncthreads();
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) {
+    const int bl = nb * 16 + (lane & 15);
+    const int sb = b0 + bl;
+    int e = 0;  // the slice's largest |delta_t| becomes 2^14 .. 2^15 (bf16 io)
+    if constexpr (BF16) {
+      float mx = 0.f;
+#pragma unroll
+      for (int w2 = 0; w2 < NW; ++w2) mx = fmaxf(mx, mx_lds[w2][bl]);
+      int ex = 0;
+      frexpf(mx, &ex);  // mx = f 2^ex, f in [0.5, 1)
+      e = mx > 0.f ? ex - 15 : 0;
+      e = e < -128 ? -128 : (e > 127 ? 127 : e);
+    }
+    if (sb < W) {
+      float ds[RPL];
+#pragma unroll
+      for (int x = 0; x < RPL; ++x) ds[x] = BF16 ? ldexpf(dts[nb][x], -e) : dts[nb][x];
       VR dw;
-      float_to_delta<BF16>(dt, dw.w, RPL);
+      float_to_delta<BF16>(ds, dw.w, RPL);
       dw.store(d_slab(NA), sb * vslot + row0 * IOB);
+      if constexpr (BF16)
+        if (w == 0 && g4 == 0)
+          reinterpret_cast<signed char*>(ds_slab(NA) + sb)[slice] = static_cast<signed char>(e);
     }
   }
 }
@@ -563,6 +613,7 @@ ReplayParams base_params(const Shape& s, int width, const void* q, float* o, con
   prm.av = a.v;
   prm.ab = a.ab;
   prm.ad = a.d;
+  prm.adsc = a.dsc;
   prm.status = a.status;
   prm.R = s.R;
   prm.HK = s.HK;

@@ -88,7 +88,8 @@ Layout layout_of(const Shape& s) {
   l.v = arena * round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
   l.ab = arena * round256(sizeof(float2) * R * T * s.HV * W);
   l.d = s.delta ? l.v : 0;  // delta rows take the size of input v rows (fp16 / fp32)
-  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab + l.d;
+  l.ds = s.delta ? round256(sizeof(unsigned) * R * T * s.HV * W) : 0;  // delta row scales
+  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab + l.d + l.ds;
   return l;
 }
 
@@ -172,6 +173,8 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   c->arena.ab = s.borrow ? nullptr : reinterpret_cast<float2*>(p);
   p += l.ab;
   c->arena.d = s.delta ? p : nullptr;
+  p += l.d;
+  c->arena.dsc = s.delta ? reinterpret_cast<unsigned*>(p) : nullptr;
 
   c->status_live = false;
   c->search_zeroed = false;

@@ -75,8 +75,9 @@ def test_workspace_bytes_layout(lib):
     assert n == expect
     assert n % 256 == 0
     # transition records add a delta arena the size of the v arena (fp16 rows)
+    # and one 32-bit word of slice scale exponents per delta row
     nd = ab.onela_workspace_bytes(cfg(record_kind=ab.ONELA_RECORD_DELTA))
-    assert nd == n + T * H * W * d * 2
+    assert nd == n + T * H * W * d * 2 + T * H * W * 4
     # borrowed records: no arena at all
     nb = ab.onela_workspace_bytes(cfg(record_storage=ab.ONELA_RECORDS_BORROW))
     assert nb == 256 + 2 * (W * T * 4) + 2 * 2 * H * d * d

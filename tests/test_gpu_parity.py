@@ -366,6 +366,28 @@ def test_delta_records_match_oracle(name):
         assert np.array_equal(results[False][t], results[True][t])
 
 
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("scale", [3e5, 1e-7, 1e-30])
+def test_delta_records_extreme_magnitudes(scale, fused):
+    """delta magnitudes beyond fp16's range (|v| ~ 3e5, so |delta| reaches
+    ~1e6) and inside or below its subnormal range (|v| ~ 1e-7, 1e-30), with
+    decays near 1: v of the prompt and of every step scaled, so S_ctx,
+    delta and o scale with it.  The per-slice power-of-two scale of the 16-bit
+    delta rows keeps the outputs within the bound."""
+    spec = W.WorkloadSpec("delta_mag", 1, 2, 4, 128, 128, 48, (32, 32, 32, 32), "bf16", "zipf",
+                          1.1, -5.0, seed=31)
+    wl = W.make_workload(spec)
+    for x in [wl.prompt_v] + [st.v for st in wl.steps]:
+        _set(x, x.f64 * scale)
+    s0 = oracle_s0(wl)
+    ref, _ = oracle_outputs(wl, s0)
+    o, g = run_gpu(wl, s0, fused=fused, records="delta")
+    errs = [rel_err(o[t], ref[t]) for t in range(spec.T)]
+    log(f"[delta magnitude {scale:g}] max rel err per step {['%.2e' % e for e in errs]}")
+    assert np.all(np.isfinite(np.concatenate([x.ravel() for x in o])))
+    assert max(errs) <= REL_TOL
+
+
 @pytest.mark.parametrize("spec", WIDE[:4], ids=[s.name for s in WIDE[:4]])
 def test_delta_records_wide_geometries(spec):
     log(f"[delta-wide] {spec.name}")
