@@ -695,12 +695,6 @@ DecodeParams base_params(const Shape& s, int width, const void* q, float* o, con
 
 }  // namespace
 
-bool decode_supported(const Shape& s) {
-  const int dk = s.dk, dv = s.dv;
-  if ((dk == 32 && dv == 32) || (dk == 64 && dv == 64) || (dk == 128 && dv == 128)) return true;
-  if (!s.bf16) return false;
-  return (dk == 128 && (dv == 256 || dv == 512)) || (dk == 256 && (dv == 256 || dv == 512));
-}
 
 hipError_t launch_decode(const Shape& s, int step, int width, const void* q, float* o,
                          const Arena& a, hipStream_t st) {

@@ -488,13 +488,6 @@ hipError_t launch_t(const Shape& s, const PrefillParams& prm, hipStream_t st) {
 
 }  // namespace
 
-size_t prefill_chunked_workspace_bytes(const Shape& s, int prompt_len) {
-  const size_t nch = size_t(prompt_len + kC - 1) / kC;
-  const size_t per = size_t(kC) * (2 * s.dk + s.dv) * sizeof(float);
-  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t units = size_t(s.R) * s.HV;
-  return up(units * nch * per) + up(units * nch * sizeof(float));
-}
 
 hipError_t launch_prefill_chunked(const Shape& s, int prompt_len, const void* k, const void* v,
                                   const float* alpha, const float* beta, float* s0_out,

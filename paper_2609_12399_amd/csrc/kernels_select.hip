@@ -1618,11 +1618,6 @@ __global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectPa
   onepass_final<BEAM>(p, u, r, part, kOnePassFinalParts);
 }
 
-unsigned pow2_ceil(unsigned x) {
-  unsigned y = 1;
-  while (y < x) y <<= 1;
-  return y;
-}
 
 // Workgroups of the one-pass kernel that can be resident at once on the
 // current device (all of a call's workgroups must be, or they would wait on
@@ -1664,72 +1659,6 @@ unsigned onepass_capacity() { return onepass_device().capacity; }
 unsigned long long onepass_wait_ticks() { return onepass_device().wait_ticks; }
 
 }  // namespace
-
-bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
-  *plan = SelectPlan{};
-  if (R < 1 || N < 1 || W < 1 || W > N || W > unsigned(kSelectMaxWidth) ||
-      N > kSelectMaxCandidates)
-    return false;
-  // Slot capacity: room for about twice the kept count, at least 64, at most
-  // a quarter of a workgroup's candidates (never below W).
-  unsigned cap = pow2_ceil(2 * W);
-  if (cap < 64) cap = 64;
-  if (cap > unsigned(kSelectChunk) / 4) cap = std::max(unsigned(kSelectChunk) / 4, pow2_ceil(W));
-  plan->cap = cap;
-  plan->group = unsigned(kSelectChunk) / cap;
-  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const unsigned nchunks = (N + kSelectChunk - 1) / kSelectChunk;
-  // Every plan starts with the one-pass path's control block, which no other
-  // data overwrites, so that a workspace shared by calls of any shape keeps
-  // its counters at zero between calls.
-  const size_t ctl = kSelectCtlBytes;
-  // Two-pass path: enough wave maxima (2048 candidates each) for a tight
-  // bound, few enough chunks for the one-workgroup gather.
-  if (N > unsigned(kSelectChunk) && uint64_t(N) >= uint64_t(2) * W * 2048u &&
-      nchunks <= unsigned(kSelectMaxGatherSlots)) {
-    plan->two_pass = true;
-    plan->nchunks = nchunks;
-    plan->nseg = nchunks * (kSelectThreads / 64);
-    plan->seg_off = ctl;  // [R][nseg] wave summaries: uint4 (one-pass), uint32 (two-pass)
-    plan->slot_off = ctl + up(size_t(R) * plan->nseg * sizeof(uint4));
-    plan->cnt_off = plan->slot_off + up(size_t(R) * nchunks * cap * sizeof(uint2));
-    plan->total = plan->cnt_off + up(size_t(R) * nchunks * sizeof(uint2));
-    return true;
-  }
-  size_t pairs[2] = {0, 0}, counts[2] = {0, 0};
-  int s = 0;
-  if (N > unsigned(kSelectChunk)) {
-    unsigned slots = nchunks;  // stage 0: raw chunks
-    plan->nwg[0] = slots;
-    plan->nin[0] = N;
-    pairs[0] = size_t(R) * slots * cap * sizeof(uint2);
-    counts[0] = size_t(R) * slots * sizeof(unsigned);
-    s = 1;
-    while (slots > plan->group) {
-      if (s == kSelectMaxStages) return false;
-      const unsigned nwg = (slots + plan->group - 1) / plan->group;
-      plan->nin[s] = slots;
-      plan->nwg[s] = nwg;
-      pairs[s & 1] = std::max(pairs[s & 1], size_t(R) * nwg * cap * sizeof(uint2));
-      counts[s & 1] = std::max(counts[s & 1], size_t(R) * nwg * sizeof(unsigned));
-      slots = nwg;
-      ++s;
-    }
-    plan->final_in = slots;
-  } else {
-    plan->final_in = N;
-  }
-  plan->stages = s;
-  size_t off = ctl;
-  for (int b = 0; b < 2; ++b) {
-    plan->pair_off[b] = off;
-    off += up(pairs[b]);
-    plan->count_off[b] = off;
-    off += up(counts[b]);
-  }
-  plan->total = off;
-  return true;
-}
 
 hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int vocab, int width,
                          const float* logp, const float* beam, int* parents, int* tokens,

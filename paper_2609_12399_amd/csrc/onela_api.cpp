@@ -10,56 +10,22 @@
 #include "../../include/onela.h"
 #include "internal.h"
 
+using onela::aligned16;
+using onela::aligned4;
 using onela::Arena;
 using onela::Layout;
+using onela::Protocol;
 using onela::Shape;
+using onela::shape_of;
 
 struct onela_ctx_s {
   Shape shape;
   Arena arena;
   hipStream_t stream;
-  int resolved;  // last step whose ancestry was resolved (-1: none)
-  bool status_live;  // a launch that zeroes the status word was enqueued (ever)
-  bool search_zeroed;  // ... in the current beam search (since init / reset)
-  int appended;  // last step whose records were appended (-1: none)
-  int widths[onela::kMaxSteps];
+  Protocol pr;  // steps resolved / appended, widths, status-word state
 };
 
 namespace {
-
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
-
-size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
-
-onela_status_t shape_of(const onela_config_t* c, Shape* s) {
-  if (!c) return ONELA_EINVAL;
-  if (c->num_requests < 1 || c->num_qk_heads < 1 || c->num_v_heads < 1)
-    return ONELA_EINVAL;
-  if (c->num_v_heads % c->num_qk_heads) return ONELA_EINVAL;
-  if (c->max_beams < 1 || c->max_beams > 65536) return ONELA_EINVAL;
-  if (c->max_steps < 1 || c->max_steps > onela::kMaxSteps) return ONELA_EINVAL;
-  if (c->io_dtype != ONELA_F32 && c->io_dtype != ONELA_BF16) return ONELA_EINVAL;
-  if (c->record_kind != ONELA_RECORD_INPUTS && c->record_kind != ONELA_RECORD_DELTA)
-    return ONELA_EINVAL;
-  if (c->record_storage != ONELA_RECORDS_COPY && c->record_storage != ONELA_RECORDS_BORROW)
-    return ONELA_EINVAL;
-  if (c->record_storage == ONELA_RECORDS_BORROW && c->record_kind == ONELA_RECORD_DELTA)
-    return ONELA_EINVAL;
-  Shape t{c->num_requests, c->num_qk_heads, c->num_v_heads,
-          c->d_k,          c->d_v,          c->max_beams,
-          c->max_steps,    c->io_dtype == ONELA_BF16, c->record_kind == ONELA_RECORD_DELTA,
-          c->record_storage == ONELA_RECORDS_BORROW};
-  if (!onela::decode_supported(t)) return ONELA_EINVAL;
-  // the kernels form 32-bit byte offsets: every region must stay below 2 GiB
-  const double big = double(t.R) * t.tmax * (t.HV > t.HK ? t.HV : t.HK) * t.wmax *
-                     (t.dv > t.dk ? t.dv : t.dk) * t.io_bytes();
-  const double outb = double(t.R) * t.wmax * t.HV * t.dv * 4.0;
-  const double s0b = double(t.R) * t.HV * t.dv * t.dk * 4.0;
-  if (big >= 2147483648.0 || outb >= 2147483648.0 || s0b >= 2147483648.0) return ONELA_EINVAL;
-  *s = t;
-  return ONELA_OK;
-}
 
 bool launch_ok(hipError_t e) { return e == hipSuccess; }
 
@@ -70,30 +36,11 @@ void borrow_step(onela_ctx_s* c, int t, const void* k, const void* v, const floa
   c->arena.bv[t] = v;
   c->arena.balpha[t] = alpha;
   c->arena.bbeta[t] = beta;
-  c->arena.bw[t] = c->widths[t];
+  c->arena.bw[t] = c->pr.widths[t];
 }
 
 }  // namespace
 
-namespace onela {
-
-Layout layout_of(const Shape& s) {
-  Layout l{};
-  const size_t R = s.R, T = s.tmax, W = s.wmax;
-  l.status = 256;
-  l.anc = round256(sizeof(int) * R * W * T);
-  l.s_frag = round256(sizeof(uint16_t) * 2 * R * s.HV * size_t(s.dv) * s.dk);
-  const size_t arena = s.borrow ? 0 : 1;  // borrowed records need no arena
-  l.k = arena * round256(size_t(s.io_bytes()) * R * T * s.HK * W * s.dk);
-  l.v = arena * round256(size_t(s.io_bytes()) * R * T * s.HV * W * s.dv);
-  l.ab = arena * round256(sizeof(float2) * R * T * s.HV * W);
-  l.d = s.delta ? l.v : 0;  // delta rows take the size of input v rows (fp16 / fp32)
-  l.ds = s.delta ? round256(sizeof(unsigned) * R * T * s.HV * W) : 0;  // delta row scales
-  l.total = l.status + 2 * l.anc + l.s_frag + l.k + l.v + l.ab + l.d + l.ds;
-  return l;
-}
-
-}  // namespace onela
 
 extern "C" {
 
@@ -154,8 +101,7 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   if (!c) return ONELA_ENOMEM;
   c->shape = s;
   c->stream = static_cast<hipStream_t>(stream);
-  c->resolved = -1;
-  c->appended = -1;
+  c->pr = Protocol{};
   char* p = static_cast<char*>(workspace);
   c->arena.status = reinterpret_cast<int*>(p);
   p += l.status;
@@ -176,17 +122,15 @@ onela_status_t onela_init(const onela_config_t* cfg, const float* s0,
   p += l.d;
   c->arena.dsc = s.delta ? reinterpret_cast<unsigned*>(p) : nullptr;
 
-  c->status_live = false;
-  c->search_zeroed = false;
   *out = c;
   return ONELA_OK;
 }
 
 onela_status_t onela_reset(onela_ctx_t c) {
   if (!c) return ONELA_EINVAL;
-  c->resolved = -1;
-  c->appended = -1;
-  c->search_zeroed = false;
+  c->pr.resolved = -1;
+  c->pr.appended = -1;
+  c->pr.search_zeroed = false;
   return ONELA_OK;
 }
 
@@ -194,30 +138,27 @@ onela_status_t onela_resolve_ancestry(onela_ctx_t c, int32_t step, int32_t width
                                       const int32_t* parents, int32_t* gather_out) {
   if (!c) return ONELA_EINVAL;
   const Shape& s = c->shape;
-  if (step != c->resolved + 1 || c->appended != c->resolved) return ONELA_ESTEP;
-  if (step >= s.tmax) return ONELA_ECAPACITY;
-  if (width < 1 || width > s.wmax) return ONELA_ECAPACITY;
-  if (step == 0 && parents) return ONELA_EINVAL;
-  if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
-  if (gather_out && !aligned4(gather_out)) return ONELA_EINVAL;
+  Protocol& pr = c->pr;
+  const onela_status_t rc = onela::check_resolve(s, pr, step, width, parents, gather_out);
+  if (rc != ONELA_OK) return rc;
   if (step > 0) {
     // The step-0 decode launch zeroes the status word of a new search.  When
     // the caller resolves step 1 without having decoded step 0, zero it here
     // first, so that what the resolve kernel flags is not mixed with a word
     // that was never cleared (or still holds an earlier search's error).
-    if (!c->search_zeroed) {
+    if (!pr.search_zeroed) {
       if (!launch_ok(onela::launch_clear_status(c->arena.status, c->stream))) return ONELA_EHIP;
-      c->search_zeroed = true;
-      c->status_live = true;
+      pr.search_zeroed = true;
+      pr.status_live = true;
     }
-    hipError_t e = onela::launch_resolve(s, step, width, c->widths[step - 1], parents,
+    hipError_t e = onela::launch_resolve(s, step, width, pr.widths[step - 1], parents,
                                          c->arena.anc[(step - 1) & 1],
                                          c->arena.anc[step & 1], gather_out,
                                          c->arena.status, c->stream);
     if (!launch_ok(e)) return ONELA_EHIP;
   }
-  c->widths[step] = width;
-  c->resolved = step;
+  pr.widths[step] = width;
+  pr.resolved = step;
   return ONELA_OK;
 }
 
@@ -225,32 +166,30 @@ onela_status_t onela_append_records(onela_ctx_t c, int32_t step, const void* k,
                                     const void* v, const float* alpha,
                                     const float* beta) {
   if (!c) return ONELA_EINVAL;
-  if (step != c->resolved || step != c->appended + 1) return ONELA_ESTEP;
-  if (!k || !v || !alpha || !beta) return ONELA_EINVAL;
-  if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta))
-    return ONELA_EINVAL;
+  const onela_status_t rc = onela::check_append(c->pr, step, k, v, alpha, beta);
+  if (rc != ONELA_OK) return rc;
   if (c->shape.borrow) {
     borrow_step(c, step, k, v, alpha, beta);
   } else {
-    hipError_t e = onela::launch_append(c->shape, step, c->widths[step], k, v, alpha,
+    hipError_t e = onela::launch_append(c->shape, step, c->pr.widths[step], k, v, alpha,
                                         beta, c->arena, c->stream);
     if (!launch_ok(e)) return ONELA_EHIP;
   }
-  c->appended = step;
+  c->pr.appended = step;
   return ONELA_OK;
 }
 
 onela_status_t onela_decode_step(onela_ctx_t c, int32_t step, const void* q, float* o) {
   if (!c) return ONELA_EINVAL;
-  if (step < 0 || step != c->resolved || step != c->appended) return ONELA_ESTEP;
-  if (!q || !o || !aligned16(q) || !aligned16(o)) return ONELA_EINVAL;
+  const onela_status_t rc = onela::check_decode(c->pr, step, q, o);
+  if (rc != ONELA_OK) return rc;
+  const int width = c->pr.widths[step];
   hipError_t e = c->shape.delta
-                     ? onela::launch_replay_decode(c->shape, step, c->widths[step], q, o,
-                                                   c->arena, c->stream)
-                     : onela::launch_decode(c->shape, step, c->widths[step], q, o, c->arena,
-                                            c->stream);
+                     ? onela::launch_replay_decode(c->shape, step, width, q, o, c->arena,
+                                                   c->stream)
+                     : onela::launch_decode(c->shape, step, width, q, o, c->arena, c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
-  if (step == 0) c->status_live = c->search_zeroed = true;
+  if (step == 0) c->pr.status_live = c->pr.search_zeroed = true;
   return ONELA_OK;
 }
 
@@ -260,34 +199,28 @@ onela_status_t onela_decode_step_fused(onela_ctx_t c, int32_t step, int32_t widt
                                        float* o, int32_t* gather_out) {
   if (!c) return ONELA_EINVAL;
   const Shape& s = c->shape;
-  if (step != c->resolved + 1 || c->appended != c->resolved) return ONELA_ESTEP;
-  if (step >= s.tmax) return ONELA_ECAPACITY;
-  if (width < 1 || width > s.wmax) return ONELA_ECAPACITY;
-  if (step == 0 && parents) return ONELA_EINVAL;
-  if (step > 0 && (!parents || !aligned4(parents))) return ONELA_EINVAL;
-  if (gather_out && !aligned4(gather_out)) return ONELA_EINVAL;
-  if (!k || !v || !alpha || !beta || !q || !o) return ONELA_EINVAL;
-  if (!aligned16(k) || !aligned16(v) || !aligned4(alpha) || !aligned4(beta) || !aligned16(q) ||
-      !aligned16(o))
-    return ONELA_EINVAL;
-  const int prev = step > 0 ? c->widths[step - 1] : 0;
+  Protocol& pr = c->pr;
+  const onela_status_t rc =
+      onela::check_fused(s, pr, step, width, parents, k, v, alpha, beta, q, o, gather_out);
+  if (rc != ONELA_OK) return rc;
+  const int prev = step > 0 ? pr.widths[step - 1] : 0;
   hipError_t e = s.delta ? onela::launch_replay_fused(s, step, width, prev, parents, k, v, alpha,
                                                       beta, q, o, gather_out, c->arena, c->stream)
                          : onela::launch_fused_step(s, step, width, prev, parents, k, v, alpha,
                                                     beta, q, o, gather_out, c->arena, c->stream);
   if (!launch_ok(e)) return ONELA_EHIP;
-  c->widths[step] = width;
+  pr.widths[step] = width;
   if (s.borrow) borrow_step(c, step, k, v, alpha, beta);
-  c->resolved = step;
-  c->appended = step;
-  if (step == 0) c->status_live = c->search_zeroed = true;
+  pr.resolved = step;
+  pr.appended = step;
+  if (step == 0) pr.status_live = pr.search_zeroed = true;
   return ONELA_OK;
 }
 
 onela_status_t onela_get_device_status(onela_ctx_t c) {
   if (!c) return ONELA_EINVAL;
   if (hipStreamSynchronize(c->stream) != hipSuccess) return ONELA_EHIP;
-  if (!c->status_live) return ONELA_OK;  // no step has run: nothing was flagged
+  if (!c->pr.status_live) return ONELA_OK;  // no step has run: nothing was flagged
   int word = 0;
   if (hipMemcpy(&word, c->arena.status, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
     return ONELA_EHIP;
@@ -398,12 +331,8 @@ onela_status_t onela_select_workspace_bytes(int32_t num_requests, int32_t prev_w
   if (!bytes) return ONELA_EINVAL;
   *bytes = 0;
   onela::SelectPlan plan;
-  if (num_requests < 1 || num_requests > 65536 || prev_width < 1 || vocab < 1 || width < 1)
-    return ONELA_EINVAL;
-  const uint64_t n = uint64_t(prev_width) * uint64_t(vocab);
-  if (n > onela::kSelectMaxCandidates ||
-      !onela::select_plan(num_requests, unsigned(n), unsigned(width), &plan))
-    return ONELA_EINVAL;
+  const onela_status_t rc = onela::check_select(num_requests, prev_width, vocab, width, &plan);
+  if (rc != ONELA_OK) return rc;
   *bytes = plan.total;
   return ONELA_OK;
 }
