@@ -234,7 +234,8 @@ onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len
  * Workspace: onela_prefill_workspace_bytes(cfg, prompt_len) bytes (0 for an
  * empty prompt, or for an invalid cfg), 256-byte aligned, owned by the caller
  * and used only by the enqueued work: per (request, value head, chunk) the
- * fp32 matrices W [64][d_k], Kt^T [d_k][64], U^T [d_v][64] and one decay.
+ * fp32 matrices W [64][d_k], Kt^T [d_k][64], U^T [d_v][64] (in the order the
+ * scan loads them) and the chunk's decay (16 copies).
  * Errors: ONELA_EINVAL, ONELA_ECAPACITY (workspace too small), ONELA_EHIP. */
 size_t onela_prefill_workspace_bytes(const onela_config_t* cfg, int32_t prompt_len);
 onela_status_t onela_prefill_state_chunked(const onela_config_t* cfg, int32_t prompt_len,

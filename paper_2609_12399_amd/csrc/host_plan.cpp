@@ -78,7 +78,7 @@ size_t prefill_chunked_workspace_bytes(const Shape& s, int prompt_len) {
   const size_t per = size_t(kPrefillChunk) * (2 * s.dk + s.dv) * sizeof(float);
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t units = size_t(s.R) * s.HV;
-  return up(units * nch * per) + up(units * nch * sizeof(float));
+  return up(units * nch * per) + up(units * nch * 16 * sizeof(float));
 }
 
 bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {

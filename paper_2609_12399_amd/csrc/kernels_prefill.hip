@@ -22,10 +22,13 @@
 //   phase 1 (prefill_chunk_kernel): one workgroup per (request, value head,
 //     chunk) forms the decay products Gamma from a doubling table (lane
 //     shuffles), M from K K^T, T by forward substitution (each column held in
-//     registers by a quad of lanes), then W and U, and stores W' [C][d_k],
-//     K^T [d_k][C] (io dtype), U'^T [d_v][C] and g to the workspace.  The
+//     registers by a quad of lanes), then W and U, and stores W', K^T (io
+//     dtype), U'^T and g to the workspace.  The
 //     three products run on v_mfma_f32_16x16x4f32.  No division: products of
-//     alpha are formed directly, so alpha = 0 is exact.
+//     alpha are formed directly, so alpha = 0 is exact.  Each operand of
+//     phase 2 is stored in the order phase 2's lanes load it (16 bytes per
+//     lane, whole 1 KB blocks per wave); W' is formed transposed so that a
+//     lane holds 4 consecutive keys of one token.
 //   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
 //     state rows; the row blocks of a head share one XCD) walks the chunks in
 //     order: X^T = W' S^T, D'^T = U'^T - X^T, S^T <- g S^T + K^T D'^T, on
@@ -33,8 +36,9 @@
 //     (a 16 x 16 fp32 accumulator tile that never leaves registers); the
 //     contraction orders are chosen so that the tile is directly the B
 //     operand of the next chunk's X and X's output is directly the B operand
-//     of the update.  The partial X of the waves are summed through LDS by the
-//     wave that forms the D' tile, so each U' tile is read by one wave only.
+//     of the update.  The partial X of the d_k / 16 waves are summed through
+//     LDS, each token tile by d_k / 64 waves that take a share of its
+//     accumulator components.
 // A ragged last chunk is padded with alpha = 1, beta = 0, k = v = 0, which
 // leaves the state unchanged.
 #include <type_traits>
@@ -54,10 +58,11 @@ struct PrefillParams {
   const float* alpha; // [R][P][HV]
   const float* beta;
   float* s_out;       // [R][HV][DV][DK]
-  float* wb;          // [R*HV][nch][C][DK]   W' = diag(sigma) W
-  void* ktb;          // [R*HV][nch][DK][C]   K^T, io dtype
-  float* utb;         // [R*HV][nch][DV][C]   U'^T = (diag(sigma) U)^T
-  float* gb;          // [R*HV][nch]
+  // per (request, value head, chunk), in phase 2's fragment order:
+  float* wb;          // [R*HV][nch][DK/16][4][64] f32x4   W' = diag(sigma) W
+  void* ktb;          // [R*HV][nch] x DK*C keys, io dtype   K^T
+  float* utb;         // [R*HV][nch][DV/16][4][64] f32x4   U'^T = (diag(sigma) U)^T
+  float* gb;          // [R*HV][nch][16]  g, repeated (phase 2 loads it per lane)
   int HK, HV, P, nch;
   int xcd_map;  // phase 2: all row blocks of a unit on one XCD (units % 8 == 0)
 };
@@ -269,16 +274,36 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   __syncthreads();
 
   const long cu = long(unit) * p.nch + c;
-  // W' = diag(sigma) T diag(beta gamma) K -> wb [C][DK];  K^T -> ktb [DK][C] in the io
-  // dtype (the keys' own bits: bf16 keys stay exact)
-  float* wdst = p.wb + cu * kC * DK;
-  for (int i = tid; i < kC * DK; i += kP1Threads) {
-    const int kk = i / kC, t = i - kk * kC;
-    if constexpr (BF16)
-      static_cast<uint16_t*>(p.ktb)[cu * DK * kC + i] = sh.K[t][kk];
-    else
-      static_cast<float*>(p.ktb)[cu * DK * kC + i] = sh.K[t][kk];
+  // The three operands of phase 2 are stored in the order its lanes load them
+  // (16 bytes per lane, 1 KB per wave and fragment).  K^T in the io dtype (the
+  // keys' own bits: bf16 keys stay exact): fragment (column block b, token tile
+  // a) of lane l holds K(t = 16 a + 4 (l / 16) + j, k = 16 b + l % 16), j =
+  // 0..3; bf16 fragments of the tiles 2 h and 2 h + 1 are interleaved per lane.
+  if constexpr (BF16) {
+    uint4* kdst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.ktb) + cu * DK * kC);
+    for (int e = tid; e < DK / 16 * 2 * 64; e += kP1Threads) {
+      const int l = e & 63, h = (e >> 6) & 1, b = e >> 7;
+      const int kk = 16 * b + (l & 15), tt = 32 * h + 4 * (l >> 4);
+      unsigned x[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int t = tt + 16 * (q >> 1) + 2 * (q & 1);
+        x[q] = unsigned(sh.K[t][kk]) | (unsigned(sh.K[t + 1][kk]) << 16);
+      }
+      kdst[e] = make_uint4(x[0], x[1], x[2], x[3]);
+    }
+  } else {
+    f32x4* kdst = reinterpret_cast<f32x4*>(static_cast<float*>(p.ktb) + cu * DK * kC);
+    for (int e = tid; e < DK / 16 * 4 * 64; e += kP1Threads) {
+      const int l = e & 63, a = (e >> 6) & 3, b = e >> 8;
+      const int kk = 16 * b + (l & 15), t = 16 * a + 4 * (l >> 4);
+      kdst[e] = f32x4{sh.K[t][kk], sh.K[t + 1][kk], sh.K[t + 2][kk], sh.K[t + 3][kk]};
+    }
   }
+  // W' = diag(sigma) T diag(beta gamma) K, formed transposed so that a lane
+  // holds 4 consecutive keys of one token: fragment (b, a) of lane l holds
+  // W'(t = 16 a + l % 16, k = 16 b + 4 (l / 16) + i), i = 0..3
+  f32x4* wdst = reinterpret_cast<f32x4*>(p.wb + cu * kC * DK);
   // (T is lower triangular: row block a needs k < 16 (a + 1))
   constexpr int NBW = DK / 16;
   for (int x = w; x < 4 * NBW; x += 4) {
@@ -288,20 +313,17 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int kk = 4 * (ks + u) + l4;
-        acc4[u] = mfma4(sh.T[16 * a + l16][kk], sh.be[kk] * sh.gam[kk] * sh.key(kk, 16 * b + l16),
+        acc4[u] = mfma4(sh.be[kk] * sh.gam[kk] * sh.key(kk, 16 * b + l16), sh.T[16 * a + l16][kk],
                         acc4[u]);
       }
     }
     const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int t = 16 * a + 4 * l4 + q;
-      wdst[t * DK + 16 * b + l16] = sh.sig[t] * acc[q];
-    }
+    wdst[(b * 4 + a) * 64 + lane] = sh.sig[16 * a + l16] * acc;
   }
-  // U' = diag(sigma) T diag(beta) V -> utb [DV][C] (4 consecutive tokens per lane and
-  // tile)
-  float* udst = p.utb + cu * DV * kC;
+  // U' = diag(sigma) T diag(beta) V, as U'^T fragments: fragment (row block rb,
+  // token tile a) of lane l holds U'^T(16 rb + l % 16, t = 16 a + 4 (l / 16) + j),
+  // j = 0..3
+  f32x4* udst = reinterpret_cast<f32x4*>(p.utb + cu * DV * kC);
   constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
   constexpr int NBU = VC / 16;
   for (int cb = 0; cb < DV; cb += VC) {
@@ -321,27 +343,28 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
       }
       const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
       const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
-      *reinterpret_cast<f32x4*>(udst + (cb + 16 * b + l16) * kC + 16 * a + 4 * l4) = sg * acc;
+      udst[((cb / 16 + b) * 4 + a) * 64 + lane] = sg * acc;
     }
     __syncthreads();
   }
-  if (tid == 0) p.gb[cu] = sh.gam[kC - 1];
+  if (tid < 16) p.gb[cu * 16 + tid] = sh.gam[kC - 1];
 }
 
 // ---- phase 2 ----------------------------------------------------------------
 
-// Operands of one chunk for one lane (see prefill_scan_kernel).
-// Operands of one chunk for one lane (see prefill_scan_kernel).  The keys
-// stay in their io encoding until they are used, so that a load issued for a
-// later chunk is not waited for early.
+// Operands of one chunk for one lane (see prefill_scan_kernel), loaded from
+// the workspace's fragment order.  The keys stay in their io encoding until
+// they are used, so that a load issued for a later chunk is not waited for
+// early; bf16 keys of two token tiles share one 16-byte load.
 template <bool BF16, int NU>
 struct ScanOps {
   f32x4 w[4], u[NU];
-  typename std::conditional<BF16, uint2, f32x4>::type k[4];
+  typename std::conditional<BF16, uint4, f32x4>::type k[BF16 ? 2 : 4];
   float g;
   __device__ float key(int mt, int j) const {
     if constexpr (BF16) {
-      const unsigned h = j < 2 ? k[mt].x : k[mt].y;
+      const uint4 q = k[mt >> 1];
+      const unsigned h = (mt & 1) ? (j < 2 ? q.z : q.w) : (j < 2 ? q.x : q.y);
       return __uint_as_float((j & 1) ? (h & 0xffff0000u) : (h << 16));
     } else {
       return k[mt][j];
@@ -349,12 +372,42 @@ struct ScanOps {
   }
 };
 
+template <int N>
+struct Vec {
+  typedef float type __attribute__((ext_vector_type(N)));
+};
+template <>
+struct Vec<1> {
+  typedef float type;
+};
+
+// Components N g .. N g + N - 1 of v.
+template <int N>
+__device__ inline typename Vec<N>::type slice(const f32x4& v, int g) {
+  if constexpr (N == 4) {
+    return v;
+  } else if constexpr (N == 2) {
+    return g == 0 ? v.xy : v.zw;
+  } else {
+    return v[g];
+  }
+}
+
 template <int DK, int DV, bool BF16>
 __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
   constexpr int NW = DK / 16;  // waves: state columns 16 w .. 16 w + 15
-  constexpr int NU = (4 + NW - 1) / NW;  // D tiles a wave forms (tiles w, w + NW, ..)
-  __shared__ f32x4 xp[NW][4][64];  // partial X^T tiles of every wave
-  __shared__ f32x4 ds[4][64];      // D'^T tiles: U'^T minus the sums of the partials
+  // The NW partial X^T of a token tile are summed by NW / 4 waves, each taking
+  // NCP of the 4 accumulator components a lane holds (with fewer than 4 waves
+  // a wave sums TPW whole tiles).
+  constexpr int TPW = NW >= 4 ? 1 : 4 / NW;
+  constexpr int NCP = NW >= 4 ? 16 / NW : 4;
+  constexpr int NG = 4 / NCP;
+  using VN = typename Vec<NCP>::type;
+  // operand sets in flight: three, two where three do not fit in the registers
+  // of a 1024-thread workgroup
+  constexpr int NS = (DK == 256 && !BF16) ? 2 : 3;
+  __shared__ VN xp[NW][4][NG][64];  // partial X^T tiles of every wave, by component group
+  __shared__ f32x4 ds[4][64];       // D'^T tiles: U'^T minus the sums of the partials
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   // The DV / 16 row blocks of a (request, value head) read the same W and
   // Kt of every chunk.  Workgroups are dispatched round-robin over the 8
@@ -379,92 +432,116 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
     *reinterpret_cast<f32x4*>(dst) = st;
     return;
   }
+  // the token tiles whose D' this wave forms, and its component group
+  const int g0 = NW >= 4 ? w >> 2 : 0;
+  auto tile = [&](int i) { return NW >= 4 ? (w & 3) : w + NW * i; };
   // Loads are unconditional (past the end they re-read the last chunk) so
   // the compiler can count them and wait only for the set about to be used.
-  auto load = [&](int c, ScanOps<BF16, NU>& o) {
+  // Every load is one lane's 16 bytes of a fragment stored contiguously by
+  // phase 1, so a wave reads whole 1 KB blocks.
+  auto load = [&](int c, ScanOps<BF16, TPW>& o) {
     const long cu = long(unit) * p.nch + (c < p.nch ? c : p.nch - 1);
-    const float* wc = p.wb + cu * kC * DK;
-    const void* kt = static_cast<const char*>(p.ktb) + cu * DK * kC * (BF16 ? 2 : 4);
-    const float* ut = p.utb + cu * DV * kC;
-    o.g = p.gb[cu];
+    const f32x4* wc = reinterpret_cast<const f32x4*>(p.wb + cu * kC * DK);
+    const f32x4* ut = reinterpret_cast<const f32x4*>(p.utb + cu * DV * kC);
+    // g through the vector memory path (16 copies, one per lane of a row):
+    // a scalar load would be waited for by the step's first LDS wait
+    o.g = p.gb[cu * 16 + lr];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      // A of X: W(t = 16 mt + lr, k = 16 w + 4 lq + i), i = 0..3
-      o.w[mt] = *reinterpret_cast<const f32x4*>(wc + (16 * mt + lr) * DK + 16 * w + 4 * lq);
-      // A of the update: K^T(k = 16 w + lr, t = 16 mt + 4 lq + j), j = 0..3
-      const long ko = (16 * w + lr) * kC + 16 * mt + 4 * lq;
-      if constexpr (BF16)
-        o.k[mt] = *reinterpret_cast<const uint2*>(static_cast<const __bf16*>(kt) + ko);
-      else
-        o.k[mt] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(kt) + ko);
-    }
-    // U'^T(row0 + lr, t = 16 mt + 4 lq + j) of the tiles this wave forms (a wave
-    // without one re-reads tile 3)
+    for (int mt = 0; mt < 4; ++mt) o.w[mt] = wc[(w * 4 + mt) * 64 + lane];
+    if constexpr (BF16) {
+      const uint4* kt = reinterpret_cast<const uint4*>(static_cast<const __bf16*>(p.ktb) +
+                                                       cu * DK * kC);
 #pragma unroll
-    for (int i = 0; i < NU; ++i) {
-      const int mt = w + NW * i < 4 ? w + NW * i : 3;
-      o.u[i] = *reinterpret_cast<const f32x4*>(ut + (row0 + lr) * kC + 16 * mt + 4 * lq);
+      for (int h = 0; h < 2; ++h) o.k[h] = kt[(w * 2 + h) * 64 + lane];
+    } else {
+      const f32x4* kt = reinterpret_cast<const f32x4*>(static_cast<const float*>(p.ktb) +
+                                                       cu * DK * kC);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) o.k[mt] = kt[(w * 4 + mt) * 64 + lane];
     }
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) o.u[i] = ut[(rb * 4 + tile(i)) * 64 + lane];
   };
-  auto step = [&](int c, const ScanOps<BF16, NU>& o) {
+  auto step = [&](int c, const ScanOps<BF16, TPW>& o) {
     if (c >= p.nch) return;
-    // partial X^T(t, n) over this wave's 16 state columns
+    // partial X^T(t, n) over this wave's 16 state columns: four independent
+    // accumulator chains, one per token tile
+    f32x4 xa[4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < 4; ++mt) xa[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(o.w[mt][i], st[i], acc, 0, 0, 0);
-      xp[w][mt][lane] = acc;
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+        xa[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.w[mt][i], st[i], xa[mt], 0, 0, 0);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int g = 0; g < NG; ++g) xp[w][mt][g][lane] = slice<NCP>(xa[mt], g);
+    __syncthreads();
+    // D'^T(t = 16 mt + 4 lq + j, n = lr) = U'^T - sum over the waves of X^T,
+    // components NCP g0 .. of the tiles this wave forms
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int mt = tile(i);
+      VN x = xp[0][mt][g0][lane];
+#pragma unroll
+      for (int v = 1; v < NW; ++v) x += xp[v][mt][g0][lane];
+      *reinterpret_cast<VN*>(reinterpret_cast<float*>(&ds[mt][lane]) + NCP * g0) =
+          slice<NCP>(o.u[i], g0) - x;
     }
     __syncthreads();
-    // wave w forms the tiles w, w + NW, .. of
-    // D'^T(t = 16 mt + 4 lq + j, n = lr) = U'^T - sum over the waves of X^T
-#pragma unroll
-    for (int i = 0; i < NU; ++i) {
-      const int mt = w + NW * i;
-      if (mt < 4) {
-        f32x4 x = xp[0][mt][lane];
-#pragma unroll
-        for (int v = 1; v < NW; ++v) x += xp[v][mt][lane];
-        ds[mt][lane] = o.u[i] - x;
-      }
-    }
-    __syncthreads();
-    // S^T <- g S^T + K^T D'^T: one independent chain per token block, summed
-    f32x4 up[4];
+    // S^T <- g S^T + K^T D'^T: one independent chain per token tile, summed
+    f32x4 up[4], dd[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      const f32x4 d = ds[mt][lane];
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(o.key(mt, j), d[j], acc, 0, 0, 0);
-      up[mt] = acc;
+      dd[mt] = ds[mt][lane];
+      up[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+        up[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.key(mt, j), dd[mt][j], up[mt], 0, 0, 0);
     st = o.g * st + ((up[0] + up[1]) + (up[2] + up[3]));
   };
-  // Three operand sets in flight: chunk c + 2 is requested before chunk c is
-  // processed.  (xp and ds are rewritten only after the next chunk's first
-  // barrier, which every wave reaches after reading them.)
-  // The scheduling barriers keep every load group in program order, so the
-  // wait before a step covers only its own (oldest) group.
-  ScanOps<BF16, NU> a, b, c3;
-  load(0, a);
-  load(1, b);
-  for (int c = 0; c < p.nch; c += 3) {
+  // NS operand sets in flight: chunk c + NS - 1 is requested before chunk c
+  // is processed.  (xp and ds are rewritten only after the next chunk's first
+  // barrier, which every wave reaches after reading them.)  The scheduling
+  // barriers keep every load group in program order, so the wait before a
+  // step covers only its own (oldest) group.
+  ScanOps<BF16, TPW> a, b;
+  if constexpr (NS == 3) {
+    ScanOps<BF16, TPW> c3;
+    load(0, a);
     __builtin_amdgcn_sched_barrier(0);
-    load(c + 2, c3);
-    __builtin_amdgcn_sched_barrier(0);
-    step(c, a);
-    __builtin_amdgcn_sched_barrier(0);
-    load(c + 3, a);
-    __builtin_amdgcn_sched_barrier(0);
-    step(c + 1, b);
-    __builtin_amdgcn_sched_barrier(0);
-    load(c + 4, b);
-    __builtin_amdgcn_sched_barrier(0);
-    step(c + 2, c3);
+    load(1, b);
+    for (int c = 0; c < p.nch; c += 3) {
+      __builtin_amdgcn_sched_barrier(0);
+      load(c + 2, c3);
+      __builtin_amdgcn_sched_barrier(0);
+      step(c, a);
+      __builtin_amdgcn_sched_barrier(0);
+      load(c + 3, a);
+      __builtin_amdgcn_sched_barrier(0);
+      step(c + 1, b);
+      __builtin_amdgcn_sched_barrier(0);
+      load(c + 4, b);
+      __builtin_amdgcn_sched_barrier(0);
+      step(c + 2, c3);
+    }
+  } else {
+    load(0, a);
+    for (int c = 0; c < p.nch; c += 2) {
+      __builtin_amdgcn_sched_barrier(0);
+      load(c + 1, b);
+      __builtin_amdgcn_sched_barrier(0);
+      step(c, a);
+      __builtin_amdgcn_sched_barrier(0);
+      load(c + 2, a);
+      __builtin_amdgcn_sched_barrier(0);
+      step(c + 1, b);
+    }
   }
   *reinterpret_cast<f32x4*>(dst) = st;
 }

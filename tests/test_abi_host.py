@@ -220,14 +220,14 @@ def test_select_host_errors(lib):
 @pytest.mark.parametrize("P,dk,dv", [(4096, 128, 128), (1, 128, 128), (65, 256, 512), (200, 32, 32)])
 def test_prefill_workspace_bytes(lib, P, dk, dv):
     """Per (request, value head, 64-token chunk): fp32 W [64][d_k], Kt^T
-    [d_k][64], U^T [d_v][64], then one fp32 decay per chunk; two 256-byte
-    aligned regions."""
+    [d_k][64], U^T [d_v][64], then the chunk's fp32 decay repeated 16 times;
+    two 256-byte aligned regions."""
     c = cfg(d_k=dk, d_v=dv, num_requests=2, num_v_heads=32)
     nch = -(-P // 64)
     up = lambda x: -(-x // 256) * 256
     units = 2 * 32
     assert ab.onela_prefill_workspace_bytes(c, P) == up(units * nch * 64 * (2 * dk + dv) * 4) + \
-        up(units * nch * 4)
+        up(units * nch * 16 * 4)
     assert ab.onela_prefill_workspace_bytes(c, 0) == 0
     assert ab.onela_prefill_workspace_bytes(cfg(d_k=96, d_v=96), P) == 0
     assert ab.onela_prefill_workspace_bytes(c, -1) == 0
