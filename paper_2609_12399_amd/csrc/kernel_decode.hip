@@ -531,32 +531,41 @@ __global__ __launch_bounds__(decode_threads(DK, DVW)) void decode_kernel(DecodeP
           for (int hl = 0; hl < 2; ++hl) frag[((ks * MB + mb) * 2 + hl) * 64] = A[ks][mb][hl];
       }
   }
-  // Two accumulator chains per output block (hi*hi, and the two cross
-  // terms) and the beam blocks interleaved keep several independent MFMAs
-  // in flight.
-  f32x4 acc[NBLK][MB], acx[NBLK][MB];
+  // Three accumulator chains per output block (hi*hi and the two cross
+  // terms), the beam blocks interleaved: consecutive MFMAs are independent,
+  // and the B fragments of the next k-step are read while this one's run.
+  f32x4 acc[NBLK][MB], acx[NBLK][MB], acy[NBLK][MB];
 #pragma unroll
   for (int nb = 0; nb < NBLK; ++nb)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
       acx[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acy[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+  uint4 bh[2][NBLK], bl[2][NBLK];
+#pragma unroll
+  for (int nb = 0; nb < NBLK; ++nb) {
+    bh[0][nb] = p_lds[0][nb][0][g4][lane & 15];
+    bl[0][nb] = p_lds[1][nb][0][g4][lane & 15];
+  }
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    uint4 bh[NBLK], bl[NBLK];
+    const int cb = ks & 1;
+    if (ks + 1 < KS) {
 #pragma unroll
-    for (int nb = 0; nb < NBLK; ++nb) {
-      bh[nb] = p_lds[0][nb][ks][g4][lane & 15];
-      bl[nb] = p_lds[1][nb][ks][g4][lane & 15];
+      for (int nb = 0; nb < NBLK; ++nb) {
+        bh[cb ^ 1][nb] = p_lds[0][nb][ks + 1][g4][lane & 15];
+        bl[cb ^ 1][nb] = p_lds[1][nb][ks + 1][g4][lane & 15];
+      }
     }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int nb = 0; nb < NBLK; ++nb) {
-        acx[nb][mb] = mfma_bf16(A[ks][mb][1], bh[nb], acx[nb][mb]);
-        acc[nb][mb] = mfma_bf16(A[ks][mb][0], bh[nb], acc[nb][mb]);
-        acx[nb][mb] = mfma_bf16(A[ks][mb][0], bl[nb], acx[nb][mb]);
+        acc[nb][mb] = mfma_bf16(A[ks][mb][0], bh[cb][nb], acc[nb][mb]);
+        acx[nb][mb] = mfma_bf16(A[ks][mb][0], bl[cb][nb], acx[nb][mb]);
+        acy[nb][mb] = mfma_bf16(A[ks][mb][1], bh[cb][nb], acy[nb][mb]);
       }
   }
 
@@ -569,10 +578,11 @@ __global__ __launch_bounds__(decode_threads(DK, DVW)) void decode_kernel(DecodeP
 #pragma unroll
     for (int e = 0; e < RPL; e += 4) {
       const float4 v4 = *reinterpret_cast<const float4*>(&v_lds[bl][rloc + e]);
-      ov[e] = acx[nb][e >> 2][0] + acc[nb][e >> 2][0] + v4.x;
-      ov[e + 1] = acx[nb][e >> 2][1] + acc[nb][e >> 2][1] + v4.y;
-      ov[e + 2] = acx[nb][e >> 2][2] + acc[nb][e >> 2][2] + v4.z;
-      ov[e + 3] = acx[nb][e >> 2][3] + acc[nb][e >> 2][3] + v4.w;
+      const f32x4 x = acx[nb][e >> 2] + acy[nb][e >> 2];
+      ov[e] = x[0] + acc[nb][e >> 2][0] + v4.x;
+      ov[e + 1] = x[1] + acc[nb][e >> 2][1] + v4.y;
+      ov[e + 2] = x[2] + acc[nb][e >> 2][2] + v4.z;
+      ov[e + 3] = x[3] + acc[nb][e >> 2][3] + v4.w;
     }
     // o is written once and not read again by the step: non-temporal
     // (streaming) stores, about 0.5 us per launch faster than plain ones.

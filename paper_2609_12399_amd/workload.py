@@ -86,6 +86,10 @@ SPECS = {
     # beams, 16 heads, d = 128, 6 decode steps (7 output tokens), 1024-token prompts.
     "r4_h16_d128_w512_t6": _spec("r4_h16_d128_w512_t6", 4, 16, 16, 128, 1024, 512, 6,
                                  "bf16", "zipf", 1.1, seed=1007),
+    # The paper's largest operator geometry: 16 requests x 512 beams, 16 heads,
+    # d = 128, 1024-token prompts, 4 steps.
+    "r16_h16_d128_w512": _spec("r16_h16_d128_w512", 16, 16, 16, 128, 1024, 512, 4, "bf16",
+                               "zipf", 1.1, seed=1009),
     # The widest value-head count of the paper's operator suite (H_V = 64):
     # 64 value heads over 16 query/key heads, d = 128, 256 beams, 4 steps.
     "gqa_h16x64_d128_w256": _spec("gqa_h16x64_d128_w256", 1, 16, 64, 128, 2048, 256, 4,
