@@ -43,6 +43,7 @@
 // leaves the state unchanged.
 #include <type_traits>
 
+#include "device_common.h"
 #include "internal.h"
 
 namespace onela {
@@ -50,7 +51,6 @@ namespace {
 
 constexpr int kC = kPrefillChunk;  // tokens per chunk
 constexpr int kP1Threads = 256;
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct PrefillParams {
   const void* k;      // [R][P][HK][DK] io dtype
@@ -131,10 +131,11 @@ struct P1Shared {
   float T[kC][kC + 4];    // (I + M)^{-1}
   union {
     float M[kC][kC + 4];  // until T is formed
-    float X[kC][128 + 4]; // then a 128-column block of beta V
+    float X[kC][128 + 4]; // then a 128-column block of beta V (fp32 keys)
+    uint16_t V[kC][128 + 8];  // or of V, raw (bf16)
   };
   float P[7][kC];         // P[k][t]: product of the 2^k decays ending at token t
-  float al[kC], be[kC], gam[kC], sig[kC];
+  alignas(16) float al[kC], be[kC], gam[kC], sig[kC], bg[kC];  // bg = beta gamma
   __device__ float key(int t, int c) const {
     if constexpr (BF16) return __uint_as_float(unsigned(K[t][c]) << 16);
     else return K[t][c];
@@ -168,6 +169,51 @@ __device__ inline float quad_sum(float x) {
 
 __device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// bf16 inputs: the products of phase 1 run on v_mfma_f32_16x16x32_bf16 (lane l
+// supplies A(l % 16, 8 (l / 16) + j) and B(8 (l / 16) + j, l % 16), j = 0..7,
+// of each 32-deep step).  The keys and values are exact in bf16; the fp32
+// factor built from T is split into three bf16 parts whose sum is exactly
+// that factor, so every product is exact and only the fp32 accumulation
+// rounds, as on the fp32 matrix instruction.
+
+// Rows s0 .. s0 + 7 of column c of a row-major bf16 array (row stride ld), as
+// one operand.
+__device__ inline uint4 gather8(const uint16_t* a, int ld, int s0, int c) {
+  unsigned u[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    u[j] = unsigned(a[(s0 + 2 * j) * ld + c]) | (unsigned(a[(s0 + 2 * j + 1) * ld + c]) << 16);
+  return make_uint4(u[0], u[1], u[2], u[3]);
+}
+
+// x = hi + mid + lo (8 floats, three bf16 vectors; exact for normal x).
+__device__ inline void split3(const float* x, uint4& hi, uint4& mid, uint4& lo) {
+  unsigned h[4], m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
+    const float r0 = x[2 * i] - bf16_lo_to_float(h[i]);
+    const float r1 = x[2 * i + 1] - bf16_hi_to_float(h[i]);
+    m[i] = pack_bf16x2(r0, r1);
+    l[i] = pack_bf16x2(r0 - bf16_lo_to_float(m[i]), r1 - bf16_hi_to_float(m[i]));
+  }
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  mid = make_uint4(m[0], m[1], m[2], m[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// Row t, columns s0 .. s0 + 7 of T scaled per column by f, split in three.
+__device__ inline void t_row_split(const float (&T)[kC][kC + 4], const float* f, int t, int s0,
+                                   uint4& hi, uint4& mid, uint4& lo) {
+  const f32x4 t0 = *reinterpret_cast<const f32x4*>(&T[t][s0]);
+  const f32x4 t1 = *reinterpret_cast<const f32x4*>(&T[t][s0 + 4]);
+  const f32x4 f0 = *reinterpret_cast<const f32x4*>(f + s0);
+  const f32x4 f1 = *reinterpret_cast<const f32x4*>(f + s0 + 4);
+  const f32x4 p0 = t0 * f0, p1 = t1 * f1;
+  const float x[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+  split3(x, hi, mid, lo);
 }
 
 // The products of phase 1 run on v_mfma_f32_16x16x4f32 in 16 x 16 tiles: for
@@ -225,6 +271,7 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
     // gamma_t = alpha_0 ... alpha_t; sigma_t = alpha_{t+1} ... alpha_{C-1}
     sh.gam[tid] = decay(sh.P, tid, -1);
     sh.sig[tid] = decay(sh.P, kC - 1, tid);
+    sh.bg[tid] = sh.be[tid] * sh.gam[tid];
   }
   // M is zero above its diagonal 16 x 16 tiles (the product below fills the
   // rest)
@@ -237,12 +284,23 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   // tiles on or below the diagonal of K K^T
   for (int x = w; x < 10; x += 4) {
     const int a = (x >= 1) + (x >= 3) + (x >= 6), b = x - a * (a + 1) / 2;
-    f32x4 acc4[4] = {};  // four independent chains over the key dimension
+    f32x4 acc;
+    if constexpr (BF16) {  // two chains of 16 x 16 x 32 steps over the keys
+      f32x4 acc2[2] = {};
+#pragma unroll
+      for (int ks = 0; ks < DK / 32; ++ks)
+        acc2[ks & 1] = mfma_bf16(*reinterpret_cast<const uint4*>(&sh.K[16 * a + l16][32 * ks + 8 * l4]),
+                                 *reinterpret_cast<const uint4*>(&sh.K[16 * b + l16][32 * ks + 8 * l4]),
+                                 acc2[ks & 1]);
+      acc = acc2[0] + acc2[1];
+    } else {
+      f32x4 acc4[4] = {};  // four independent chains over the key dimension
 #pragma unroll 8
-    for (int ks = 0; ks < DK / 4; ++ks)
-      acc4[ks & 3] = mfma4(sh.key(16 * a + l16, 4 * ks + l4), sh.key(16 * b + l16, 4 * ks + l4),
-                           acc4[ks & 3]);
-    const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+      for (int ks = 0; ks < DK / 4; ++ks)
+        acc4[ks & 3] = mfma4(sh.key(16 * a + l16, 4 * ks + l4), sh.key(16 * b + l16, 4 * ks + l4),
+                             acc4[ks & 3]);
+      acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int t = 16 * a + 4 * l4 + q, i = 16 * b + l16;
@@ -306,19 +364,45 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   f32x4* wdst = reinterpret_cast<f32x4*>(p.wb + cu * kC * DK);
   // (T is lower triangular: row block a needs k < 16 (a + 1))
   constexpr int NBW = DK / 16;
-  for (int x = w; x < 4 * NBW; x += 4) {
-    const int a = x / NBW, b = x - a * NBW;
-    f32x4 acc4[4] = {};
-    for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+  if constexpr (BF16) {
+    // W^T(k, t) = sum_s K(s, k) (T diag(beta gamma))(t, s): 32-token steps
+    // (the first covering rows a = 0, 1, the second a = 2, 3); the factor
+    // is split once per row block and used for all of the wave's key blocks
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int kk = 4 * (ks + u) + l4;
-        acc4[u] = mfma4(sh.be[kk] * sh.gam[kk] * sh.key(kk, 16 * b + l16), sh.T[16 * a + l16][kk],
-                        acc4[u]);
+    for (int a = 0; a < 4; ++a) {
+      const int nks = (a + 2) / 2;
+      uint4 fh[2], fm[2], fl[2];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        if (ks < nks) t_row_split(sh.T, sh.bg, 16 * a + l16, 32 * ks + 8 * l4, fh[ks], fm[ks], fl[ks]);
+      for (int b = w; b < NBW; b += 4) {
+        f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          if (ks < nks) {
+            const uint4 kf = gather8(&sh.K[0][0], Sh::KLD, 32 * ks + 8 * l4, 16 * b + l16);
+            c2 = mfma_bf16(kf, fl[ks], c2);
+            c1 = mfma_bf16(kf, fm[ks], c1);
+            c0 = mfma_bf16(kf, fh[ks], c0);
+          }
+        wdst[(b * 4 + a) * 64 + lane] = sh.sig[16 * a + l16] * ((c2 + c1) + c0);
       }
     }
-    const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
-    wdst[(b * 4 + a) * 64 + lane] = sh.sig[16 * a + l16] * acc;
+  } else {
+    for (int x = w; x < 4 * NBW; x += 4) {
+      const int a = x / NBW, b = x - a * NBW;
+      f32x4 acc4[4] = {};
+      for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kk = 4 * (ks + u) + l4;
+          acc4[u] = mfma4(sh.be[kk] * sh.gam[kk] * sh.key(kk, 16 * b + l16), sh.T[16 * a + l16][kk],
+                          acc4[u]);
+        }
+      }
+      const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+      wdst[(b * 4 + a) * 64 + lane] = sh.sig[16 * a + l16] * acc;
+    }
   }
   // U' = diag(sigma) T diag(beta) V, as U'^T fragments: fragment (row block rb,
   // token tile a) of lane l holds U'^T(16 rb + l % 16, t = 16 a + 4 (l / 16) + j),
@@ -327,23 +411,66 @@ __global__ __launch_bounds__(kP1Threads) void prefill_chunk_kernel(PrefillParams
   constexpr int VC = DV < 128 ? DV : 128;  // V columns per block
   constexpr int NBU = VC / 16;
   for (int cb = 0; cb < DV; cb += VC) {
-    fill_rows<VC, 128 + 4, BF16>(&sh.X[0][0], p.v, n, cb,
-                             [&](int t) { return ((tok0 + t) * p.HV + hv) * DV; },
-                             [&](int t) { return sh.be[t]; });
-    __syncthreads();
-    for (int x = w; x < 4 * NBU; x += 4) {
-      const int a = x / NBU, b = x - a * NBU;
-      f32x4 acc4[4] = {};
-      for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+    if constexpr (BF16) {
+      // raw 16-byte copies of the value rows (zero past the prompt)
+      constexpr int NV = kC * VC / 8, PER = (NV + kP1Threads - 1) / kP1Threads;
+      uint4 buf[PER];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int kk = 4 * (ks + u) + l4;
-          acc4[u] = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc4[u]);
+      for (int q = 0; q < PER; ++q) {
+        const int vi = tid + q * kP1Threads, t = vi / (VC / 8), cc = (vi - t * (VC / 8)) * 8;
+        buf[q] = make_uint4(0u, 0u, 0u, 0u);
+        if (vi < NV && t < n)
+          buf[q] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.v) +
+                                                   ((tok0 + t) * p.HV + hv) * DV + cb + cc);
+      }
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int vi = tid + q * kP1Threads, t = vi / (VC / 8), cc = (vi - t * (VC / 8)) * 8;
+        if (vi < NV) *reinterpret_cast<uint4*>(&sh.V[t][cc]) = buf[q];
+      }
+      __syncthreads();
+      // U(t, d) = sum_s (T diag(beta))(t, s) V(s, d), the factor split once
+      // per row block
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int nks = (a + 2) / 2;
+        uint4 fh[2], fm[2], fl[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          if (ks < nks) t_row_split(sh.T, sh.be, 16 * a + l16, 32 * ks + 8 * l4, fh[ks], fm[ks], fl[ks]);
+        const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
+        for (int b = w; b < NBU; b += 4) {
+          f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0;
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks)
+            if (ks < nks) {
+              const uint4 vf = gather8(&sh.V[0][0], 128 + 8, 32 * ks + 8 * l4, 16 * b + l16);
+              c2 = mfma_bf16(fl[ks], vf, c2);
+              c1 = mfma_bf16(fm[ks], vf, c1);
+              c0 = mfma_bf16(fh[ks], vf, c0);
+            }
+          udst[((cb / 16 + b) * 4 + a) * 64 + lane] = sg * ((c2 + c1) + c0);
         }
       }
-      const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
-      const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
-      udst[((cb / 16 + b) * 4 + a) * 64 + lane] = sg * acc;
+    } else {
+      fill_rows<VC, 128 + 4, BF16>(&sh.X[0][0], p.v, n, cb,
+                               [&](int t) { return ((tok0 + t) * p.HV + hv) * DV; },
+                               [&](int t) { return sh.be[t]; });
+      __syncthreads();
+      for (int x = w; x < 4 * NBU; x += 4) {
+        const int a = x / NBU, b = x - a * NBU;
+        f32x4 acc4[4] = {};
+        for (int ks = 0; ks < 4 * (a + 1); ks += 4) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int kk = 4 * (ks + u) + l4;
+            acc4[u] = mfma4(sh.T[16 * a + l16][kk], sh.X[kk][16 * b + l16], acc4[u]);
+          }
+        }
+        const f32x4 acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+        const f32x4 sg = *reinterpret_cast<const f32x4*>(&sh.sig[16 * a + 4 * l4]);
+        udst[((cb / 16 + b) * 4 + a) * 64 + lane] = sg * acc;
+      }
     }
     __syncthreads();
   }
