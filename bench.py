@@ -470,43 +470,53 @@ def main():
         return g
 
     def fused_kernel_us(kind):
-        """Average fused-launch duration per decode step t (events around
-        NB back-to-back launches held in one graph per t)."""
+        """Average fused-launch duration per decode step t: graphs of the step-t
+        launches of G batches (a group of the whole-step protocol, so that
+        the caches hold what they hold there) and of the first G / 2,
+        replayed in turn; the difference of their event times over the
+        G - G / 2 extra launches leaves out the fixed cost of a graph replay."""
         def init_all():
             for i, b in enumerate(batches):
                 ctxs[i] = ab.onela_init(cfgs[kind], b["s0"], b["ws"], ws_bytes, rs)
 
-        def fused_all(t):
-            for i, b in enumerate(batches):
+        def fused_all(t, nb):
+            for i, b in enumerate(batches[:nb]):
                 st = b["steps"][t]
                 ab.onela_decode_step_fused(ctxs[i], t, st.width, st.parents, st.k, st.v,
                                            st.alpha, st.beta, st.q, b["outs"][t])
 
         # Graphs hold kernel arguments by value, so each one is captured with
         # the host-side contexts already advanced to the step it replays;
-        # replaying step_graphs[0..T-1] redoes the whole sequence on the
-        # device (onela_init enqueues nothing).
-        step_graphs = []
-        for t in range(T):
-            with torch.cuda.stream(rs):
-                init_all()
-                for tt in range(t):
-                    fused_all(tt)
-            step_graphs.append(capture_on_rs(lambda t=t: fused_all(t)))
-            for c in ctxs:
-                ab.onela_destroy(c)
+        # replaying graphs[0..T-1] redoes the whole sequence on the device
+        # (onela_init enqueues nothing).
+        full, half = G, max(1, G // 2)
+        graphs = {}
+        for nb in (full, half):
+            for t in range(T):
+                with torch.cuda.stream(rs):
+                    init_all()
+                    for tt in range(t):
+                        fused_all(tt, full)
+                graphs[nb, t] = capture_on_rs(lambda t=t, nb=nb: fused_all(t, nb))
+                for c in ctxs:
+                    ab.onela_destroy(c)
         torch.cuda.synchronize()
         n_roof = max(4, args.steps // 20)
-        dec_ms = np.zeros((n_roof, T))
+        ms = {nb: np.zeros((n_roof, T)) for nb in (full, half)}
         for i in range(n_roof):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
-            ev[0].record()
-            for t in range(T):
-                step_graphs[t].replay()
-                ev[t + 1].record()
-            torch.cuda.synchronize()
-            dec_ms[i] = [ev[t].elapsed_time(ev[t + 1]) / NB for t in range(T)]
-        return dec_ms[1:].mean(axis=0) * 1e3
+            for nb in (full, half):
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(T + 1)]
+                ev[0].record()
+                for t in range(T):
+                    graphs[nb, t].replay()
+                    ev[t + 1].record()
+                torch.cuda.synchronize()
+                ms[nb][i] = [ev[t].elapsed_time(ev[t + 1]) for t in range(T)]
+        if full > half:
+            diff = (ms[full][1:] - ms[half][1:]).mean(axis=0) / (full - half)
+        else:  # a group of one batch: the replay cost stays in
+            diff = ms[full][1:].mean(axis=0) / full
+        return diff * 1e3
 
     dec_us = fused_kernel_us(kind)
     bytes_t = [kernel_alg_bytes(wl, t, kind) for t in range(T)]
@@ -558,7 +568,9 @@ def main():
                                 else "decode_kernel<FUSED>"),
                      "alg_bytes_per_t": bytes_t,
                      "us_per_t": [round(float(x), 3) for x in dec_us],
-                     "timing": f"HIP events around {NB} back-to-back launches per t"},
+                     "timing": f"HIP events around graphs of the step-t launches of {G} "
+                               f"and of {max(1, G // 2)} batches (one whole-step group and "
+                               f"half of it); their difference per extra launch"},
     }
 
     # ---- A/B: the other record variants (borrowed or copied input records
