@@ -503,11 +503,10 @@ __global__ __launch_bounds__(4 * DK) void replay_kernel(ReplayParams p) {
       ov[e] = fmaf(dt[e], cqt, at_ * uq[e]);
     }
     if (sb < W) {
-      float4* dst = at<float4>(p.o, (((unsigned(r) * W + sb) * p.HV + hv) * DV + row0) * 4u);
+      const unsigned ooff = (((unsigned(r) * W + sb) * p.HV + hv) * DV + row0) * 4u;
 #pragma unroll
       for (int i = 0; i < MB; ++i)  // o is not read again: streaming stores
-        __builtin_nontemporal_store(f32x4{ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]},
-                                    reinterpret_cast<f32x4*>(dst + i));
+        store_out(p.o, ooff + 16u * i, f32x4{ov[4 * i], ov[4 * i + 1], ov[4 * i + 2], ov[4 * i + 3]});
     }
     float mx = 0.f;
 #pragma unroll
