@@ -331,6 +331,10 @@ def main():
     ap.add_argument("--skip-loop", action="store_true",
                     help="skip the closed-loop leg (fused decode + beam selection per step)")
     ap.add_argument("--skip-prefill", action="store_true")
+    ap.add_argument("--layers", type=int, default=18,
+                    help="GDN layers of the multi-layer leg (the paper's model has 18)")
+    ap.add_argument("--skip-layers", action="store_true",
+                    help="skip the multi-layer leg (one decode step over L layers' contexts)")
     ap.add_argument("--select-vocab", type=int, default=None,
                     help="codebook size of the beam-selection measurement")
     args = ap.parse_args()
@@ -785,6 +789,38 @@ def main():
         log(f"[bench] closed loop: {loop_ms * 1e3:.1f} us per {T}-step search "
             f"({loop_ms * 1e3 / T:.1f} us per decode + select)")
         del lb, lgraphs
+
+    # ---- a model with L GDN layers (supplementary, not part of `value`): L
+    # contexts, each with its own S_ctx, record slabs and workspace, advanced
+    # through the T decode steps; every step launches the fused kernel of each
+    # layer in turn (the layers of one token step are independent here: the
+    # model's other layers, which would feed one GDN layer's q, k, v from the
+    # previous one's output, are outside the path).  One graph per search.
+    if not args.skip_layers and args.layers > 0:
+        L = min(args.layers, NB)
+        lay = batches[:L]
+        lgraph = capture(lambda: group_steps(lay, True, kind))
+        lgraph.replay()
+        torch.cuda.synchronize()
+        nrep = 10
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(nrep):
+            lgraph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        search_us = e0.elapsed_time(e1) * 1e3 / nrep
+        result["layers"] = {
+            "layers": L, "decode_steps": T,
+            "us_per_search": search_us,
+            "us_per_token_step_all_layers": search_us / T,
+            "us_per_layer_launch": search_us / (T * L),
+            "beam_tokens_per_s": beam_tokens_per_step / (search_us * 1e-6),
+            "note": f"{L} GDN layers per token step, each its own context; T steps x L "
+                    f"fused launches (onela_init per layer) in one HIP graph, {nrep} replays"}
+        log(f"[bench] {L} layers: {search_us:.1f} us per {T}-step search "
+            f"({search_us / (T * L):.2f} us per layer launch)")
+        del lgraph
 
     # ---- practical HBM ceiling: a plain device copy (torch copy_, 16-byte
     # vector blit) of the same size as the dominant kernel's traffic, and of

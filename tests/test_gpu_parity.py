@@ -274,7 +274,7 @@ def test_protocol_order_enforced():
     dec.close()
 
 
-@pytest.mark.parametrize("name", ["tiny_h2_d32_w8", "h16_d128_w128"])
+@pytest.mark.parametrize("name", ["tiny_h2_d32_w8", "h16_d128_w128", "h16_d128_w512"])
 def test_fullstate_baseline_matches_oracle(name):
     log(f"[fullstate] {name}")
     wl, s0, ref = cached_case(name)
