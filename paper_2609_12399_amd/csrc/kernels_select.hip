@@ -1162,23 +1162,29 @@ __device__ inline unsigned long long wait_bound(unsigned long long* word,
 }
 
 // Data that crosses workgroups of one pass launch (the XCDs' L2 caches are
-// not coherent with each other) is written and read with agent-scope atomic
-// accesses: such stores write through to memory and such
-// loads bypass the compute unit's and the XCD's caches, so no cache-wide
-// write-back or invalidation (an agent-scope fence, several microseconds
-// with 256 workgroups issuing them) is needed.  A writer waits for its
-// stores to complete (vmcnt(0), the vector memory counter also covers
-// stores on this architecture) before it updates a counter.
-__device__ inline void st_agent(uint2* at, uint2 v) {
-  __hip_atomic_store(reinterpret_cast<unsigned long long*>(at),
-                     (static_cast<unsigned long long>(v.y) << 32) | v.x, __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
+// not coherent with each other) is written and read at agent scope (cache
+// policy sc1, as the compiler emits for agent-scope atomics): such stores
+// write through to memory and such loads bypass the compute unit's and the
+// XCD's caches, so no cache-wide write-back or invalidation (an agent-scope
+// fence, several microseconds with 256 workgroups issuing them) is needed.
+// A writer waits for its stores to complete (vmcnt(0), the vector memory
+// counter also covers stores on this architecture) before it updates a
+// counter.  Buffer accesses from a workgroup-uniform base; byte offsets stay
+// below 2^31.
+// A buffer access at or beyond `bytes` touches no memory (a load returns
+// zeros), which lets a variable number of loads issue without a branch.
+__device__ inline __amdgpu_buffer_rsrc_t agent_rsrc(const void* base, int bytes = 0x7fffffff) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), bytes,
+                                           0x00020000);
 }
-__device__ inline uint2 ld_agent(const uint2* at) {
-  const unsigned long long v =
-      __hip_atomic_load(const_cast<unsigned long long*>(reinterpret_cast<const unsigned long long*>(at)),
-                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_uint2(unsigned(v), unsigned(v >> 32));
+constexpr int kAgentScope = 16;  // cache policy bit sc1
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+__device__ inline void st_agent4(void* base, unsigned off, uint4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), agent_rsrc(base), off, 0,
+                                         kAgentScope);
+}
+__device__ inline uint4 ld_agent4(__amdgpu_buffer_rsrc_t rs, unsigned off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kAgentScope));
 }
 __device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
@@ -1189,23 +1195,43 @@ __device__ inline unsigned wave_live_lanes(const SelectParams& p, unsigned c, un
   return nc > first ? min(nc - first, 64u) : 0u;
 }
 
+// LDS of the bound (the last arrival only).
+constexpr int kBoundList = 512;  // events of one histogram bin resolved by brute force
+struct BoundShared {
+  uint2 ev[kBoundList];          // (key, weight) of the events in the chosen bin
+  unsigned nev;
+  unsigned red[2][kWaves];
+  unsigned part[kOnePassSegPer][kWaves];  // guaranteed counts at B per (summary row, wave)
+};
+
 // Bound word of request r from every wave's summary (see step 2 above):
 // ((c* + 1) << 32) | B.  All of a thread's summaries are loaded in one round
 // (nseg <= kOnePassSegPer * kThreads).
+//
+// Each live summary (M, m, kM) of a wave with nl live lanes is two weighted
+// events: (M, kM) and (m, nl - kM).  The guaranteed count at a key x is the
+// total weight of the events at keys >= x (for m >= x: kM + nl - kM = nl;
+// for M >= x > m: kM), so B, the largest key whose guaranteed count reaches
+// W, is the key of the event at which the weight counted from the top
+// reaches W.  A 2048-bin weight histogram over key - lo finds the bin that
+// holds it; the events of that bin (usually a few) are then compared with
+// each other directly.  A bin with more than kBoundList events is split by a
+// second histogram pass over the next 11 bits; should that one hold too many
+// as well, B is its smallest event key (its count still reaches W).
 __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
-                                                   unsigned r) {
+                                                   BoundShared& bs, unsigned r) {
   const unsigned nseg = p.nwg * unsigned(kWaves);
-  const uint2* ex = reinterpret_cast<const uint2*>(p.ex + size_t(r) * nseg);
   const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
-  uint2 e[kOnePassSegPer], f[kOnePassSegPer];  // (M, m), (kM, -)
+  const unsigned W = p.W;
+  // all rows are issued at once: the ones beyond nseg read nothing (a load
+  // under a branch would be waited for where the branch joins)
+  uint4 e[kOnePassSegPer];  // (M, m, kM, 0)
+  const __amdgpu_buffer_rsrc_t rs = agent_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
 #pragma unroll
-  for (int i = 0; i < kOnePassSegPer; ++i)
-    if (unsigned(i) * kThreads < nseg) {  // workgroup-uniform
-      const unsigned s = unsigned(i) * kThreads + t;
-      const unsigned sc = s < nseg ? s : 0u;
-      e[i] = ld_agent(ex + 2u * sc);
-      f[i] = ld_agent(ex + 2u * sc + 1u);
-    }
+  for (int i = 0; i < kOnePassSegPer; ++i) e[i] = ld_agent4(rs, (unsigned(i) * kThreads + t) * 16u);
+  // while the summaries are in flight: clear the histogram and the list
+  reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
+  if (t == 0) bs.nev = 0u;
   unsigned nl[kOnePassSegPer], lo = ~0u, hi = 0u;
 #pragma unroll
   for (int i = 0; i < kOnePassSegPer; ++i) {
@@ -1219,69 +1245,140 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       }
     }
   }
-  const Red3 rr = block_reduce(sh, 0u, lo, hi);
-  unsigned B = rr.lo;
-  if (rr.lo < rr.hi) {
-    // radix passes over key - lo, each within the bin the previous one chose
-    int shift = bit_width(rr.hi - rr.lo);
-    unsigned prefix = 0u, need = p.W;
-    for (int pass = 0; pass < 2 && shift > 0; ++pass) {
+  {
+    const Red3 wr = wave_reduce(0u, lo, hi);
+    if (lane == 0) {
+      bs.red[0][w] = wr.lo;
+      bs.red[1][w] = wr.hi;
+    }
+  }
+  __syncthreads();
+  lo = ~0u;
+  hi = 0u;
+#pragma unroll
+  for (int w2 = 0; w2 < kWaves; ++w2) {
+    lo = min(lo, bs.red[0][w2]);
+    hi = max(hi, bs.red[1][w2]);
+  }
+  unsigned B = lo;
+  if (lo < hi) {
+    int shift = bit_width(hi - lo);
+    unsigned prefix = 0u, need = W;
+    bool done = false;
+    for (int pass = 0; pass < 2 && !done; ++pass) {  // workgroup-uniform
       const int bits = shift < 11 ? shift : 11;
       shift -= bits;
       const unsigned mask = (1u << bits) - 1u;
-      reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
-      __syncthreads();
+      if (pass > 0) {
+        reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
+        if (t == 0) bs.nev = 0u;
+        __syncthreads();
+      }
+      // weights by bin, among the events inside the bin chosen so far
 #pragma unroll
       for (int i = 0; i < kOnePassSegPer; ++i)
         if (nl[i] > 0u) {
-          const unsigned rm = e[i].x - rr.lo, rl = e[i].y - rr.lo;
-          if (shr(rm, shift + bits) == prefix) atomicAdd(&sh.hist[(rm >> shift) & mask], f[i].x);
-          if (nl[i] > f[i].x && shr(rl, shift + bits) == prefix)
-            atomicAdd(&sh.hist[(rl >> shift) & mask], nl[i] - f[i].x);
+          const unsigned rm = e[i].x - lo, rl = e[i].y - lo;
+          if (shr(rm, shift + bits) == prefix) atomicAdd(&sh.hist[(rm >> shift) & mask], e[i].z);
+          if (nl[i] > e[i].z && shr(rl, shift + bits) == prefix)
+            atomicAdd(&sh.hist[(rl >> shift) & mask], nl[i] - e[i].z);
         }
       __syncthreads();
       find_bin(sh, need);  // the live lanes (>= N / 32 >= W) always reach W
       prefix = (prefix << bits) | sh.digit;
       need = sh.need;
-    }
-    B = rr.lo + (prefix << shift);
-    // raise B to the smallest summary key at or above it: no guarantee
-    // changes in between, and a tie at the top then sits exactly at B
-    unsigned nb = ~0u;
+      // the events of the chosen bin
 #pragma unroll
-    for (int i = 0; i < kOnePassSegPer; ++i)
-      if (nl[i] > 0u) {
-        if (e[i].x >= B) nb = min(nb, e[i].x);
-        if (e[i].y >= B) nb = min(nb, e[i].y);
+      for (int i = 0; i < kOnePassSegPer; ++i)
+        if (nl[i] > 0u) {
+          const unsigned rm = e[i].x - lo, rl = e[i].y - lo;
+          if (shr(rm, shift) == prefix) {
+            const unsigned q = atomicAdd(&bs.nev, 1u);
+            if (q < unsigned(kBoundList)) bs.ev[q] = make_uint2(e[i].x, e[i].z);
+          }
+          if (nl[i] > e[i].z && shr(rl, shift) == prefix) {
+            const unsigned q = atomicAdd(&bs.nev, 1u);
+            if (q < unsigned(kBoundList)) bs.ev[q] = make_uint2(e[i].y, nl[i] - e[i].z);
+          }
+        }
+      __syncthreads();
+      const unsigned n = bs.nev;
+      if (n <= unsigned(kBoundList)) {
+        // B = the largest event key x of the bin whose weight at keys >= x,
+        // within the bin, reaches need (the bin's smallest key always does)
+        unsigned cand = 0u;
+        if (t < n) {
+          const unsigned x = bs.ev[t].x;
+          unsigned g = 0u;
+          for (unsigned u = 0; u < n; ++u) {
+            const uint2 o = bs.ev[u];
+            g += o.x >= x ? o.y : 0u;
+          }
+          cand = g >= need ? x : 0u;
+        }
+        const Red3 wr = wave_reduce(0u, 0u, cand);
+        if (lane == 0) bs.red[1][w] = wr.hi;
+        __syncthreads();
+        B = 0u;
+#pragma unroll
+        for (int w2 = 0; w2 < kWaves; ++w2) B = max(B, bs.red[1][w2]);
+        done = true;
       }
-    B = block_reduce(sh, 0u, nb, 0u).lo;
+    }
+    if (!done) {
+      // still too many events in the bin: its smallest event key
+      const unsigned floor = lo + (prefix << shift);
+      unsigned nb = ~0u;
+#pragma unroll
+      for (int i = 0; i < kOnePassSegPer; ++i)
+        if (nl[i] > 0u) {
+          if (e[i].x >= floor) nb = min(nb, e[i].x);
+          if (nl[i] > e[i].z && e[i].y >= floor) nb = min(nb, e[i].y);
+        }
+      const Red3 wr = wave_reduce(0u, nb, 0u);
+      if (lane == 0) bs.red[0][w] = wr.lo;
+      __syncthreads();
+      B = ~0u;
+#pragma unroll
+      for (int w2 = 0; w2 < kWaves; ++w2) B = min(B, bs.red[0][w2]);
+    }
   }
-  // c*: guaranteed count of each chunk at B, summed in chunk order (chunk
-  // 4t + q in thread t, nchunks <= 4 * kThreads)
-  unsigned* gc = sh.hist;
-  reinterpret_cast<uint4*>(gc)[t] = make_uint4(0u, 0u, 0u, 0u);
+  // c*: the chunks' guaranteed counts at B, summed in chunk order.  Thread t
+  // holds summary i * kThreads + t, i.e. wave t % 8 of chunk i * 64 + t / 8:
+  // a chunk's count is a sum over 8 adjacent lanes, and chunk order is (i,
+  // wave, lane) order.
+  unsigned gch[kOnePassSegPer], excl[kOnePassSegPer];
+#pragma unroll
+  for (int i = 0; i < kOnePassSegPer; ++i) {
+    gch[i] = 0u;
+    excl[i] = 0u;
+    if (unsigned(i) * kThreads < nseg) {
+      unsigned g = nl[i] > 0u ? (e[i].y >= B ? nl[i] : (e[i].x >= B ? e[i].z : 0u)) : 0u;
+      g += dppu<0xB1>(g);   // quad_perm [1,0,3,2]
+      g += dppu<0x4E>(g);   // quad_perm [2,3,0,1]
+      g += dppu<0x141>(g);  // row_half_mirror: the other quad of the 8 lanes
+      gch[i] = g;
+      const unsigned x = (lane & 7u) == 0u ? g : 0u;
+      const unsigned inc = wave_scan(x);
+      excl[i] = inc - x;
+      if (lane == 63) bs.part[i][w] = inc;
+    }
+  }
+  if (t == 0) sh.digit = ~0u;  // (c* always exists: the counts at B reach W)
   __syncthreads();
+  unsigned before = 0u;
 #pragma unroll
   for (int i = 0; i < kOnePassSegPer; ++i)
-    if (nl[i] > 0u) {
-      const unsigned g = e[i].y >= B ? nl[i] : (e[i].x >= B ? f[i].x : 0u);
-      if (g > 0u) atomicAdd(&gc[(unsigned(i) * kThreads + t) / kWaves], g);
+    if (unsigned(i) * kThreads < nseg) {
+      unsigned b = before + excl[i];
+#pragma unroll
+      for (int w2 = 0; w2 < kWaves; ++w2) {
+        const unsigned x = bs.part[i][w2];
+        b += unsigned(w2) < w ? x : 0u;
+        before += x;
+      }
+      if ((lane & 7u) == 0u && b < W && b + gch[i] >= W) sh.digit = unsigned(i) * 64u + t / 8u;
     }
-  __syncthreads();
-  const uint4 g4 = reinterpret_cast<const uint4*>(gc)[t];
-  const unsigned gs = g4.x + g4.y + g4.z + g4.w;
-  const unsigned inc = wave_scan(gs);
-  if (lane == 63) sh.red[0][w] = inc;
-  __syncthreads();
-  unsigned before = inc - gs;
-#pragma unroll
-  for (int w2 = 0; w2 < kWaves; ++w2) before += unsigned(w2) < w ? sh.red[0][w2] : 0u;
-  const unsigned gq[4] = {g4.x, g4.y, g4.z, g4.w};
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if (before < p.W && before + gq[q] >= p.W) sh.digit = 4u * t + unsigned(q);
-    before += gq[q];
-  }
   __syncthreads();
   return (static_cast<unsigned long long>(sh.digit + 1u) << 32) | B;
 }
@@ -1295,6 +1392,8 @@ struct OnePassShared {
   alignas(16) unsigned long long top[kOnePassRankMax];  // the exact top W
   unsigned bstart[2048];                          // first position of each key bin in buck
   unsigned ntop;
+  unsigned over[kThreads];                        // chunks with more than kSpecEntries survivors
+  unsigned nover;
 };
 
 // Composite of a candidate: its key above its complemented flat index, so
@@ -1467,77 +1566,125 @@ __device__ inline void onepass_topw(const SelectParams& p, OnePassShared& u, uns
   bucket_rank_emit<BEAM>(p, u, r, u.top, min(u.ntop, unsigned(kOnePassRankMax)));
 }
 
-// Final stage of request r in its last workgroup (every chunk's slot and
-// (count, largest key) pair are stored): survivors of up to kRankCap are
-// staged in LDS first, more are read from the slots on every pass.
+// Final stage of request r in one of its nparts workgroups (every chunk's
+// slot and (count, largest key) pair are stored).  One round of loads brings
+// every chunk's count (thread t: chunk t, nchunks <= kThreads) and the first
+// kSpecEntries entries of every slot (coalesced: a wave instruction covers 4
+// slots, 16 lanes x 16 bytes each), which holds every survivor of most chunks;
+// the survivors beyond them (a chunk holding many) are loaded by whole
+// waves, one such chunk per wave at a time.  Up to kRankCap survivors are
+// staged in LDS in position order; more are read from the slots on every
+// pass of the exact top-W cut.
+constexpr int kSpecEntries = 32;     // slot entries loaded with the counts
+constexpr int kSpecRows = kThreads / 32;  // 32 slots per row of loads (8 waves x 4 slots)
+constexpr int kBruteRankMax = 2048;  // survivors ranked by direct comparison
 template <bool BEAM>
 __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, unsigned r,
                                      unsigned part, unsigned nparts) {
   const unsigned ns = p.nwg, t = threadIdx.x;
   const unsigned lane = lane_id(), w = t >> 6;
   SelShared& sh = u.sh;
-  unsigned c4[4], sum = 0u;
-  {
-    const uint2* cm = reinterpret_cast<const uint2*>(p.cnt_out) + size_t(r) * ns;
+  const uint2* slots = p.cand_out + size_t(r) * ns * p.cap;
+  const unsigned cnt = t < ns ? reinterpret_cast<const uint2*>(p.cnt_out)[size_t(r) * ns + t].x : 0u;
+  uint4 ent[kSpecRows];  // entries 2 (lane % 16), + 1 of slot 32 i + 4 w + lane / 16
+  // every row is loaded, from clamped addresses: a load under a branch is
+  // waited for where the branch joins, which would serialise the rows
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const unsigned sl = 4u * t + unsigned(q);
-      c4[q] = sl < ns ? cm[sl].x : 0u;
-      sum += c4[q];
-    }
+  for (int i = 0; i < kSpecRows; ++i) {
+    const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
+    ent[i] = reinterpret_cast<const uint4*>(slots + size_t(c < ns ? c : 0u) * p.cap)[lane & 15u];
   }
-  const unsigned inc = wave_scan(sum);
+  if (t == 0) u.nover = 0u;
+  const unsigned inc = wave_scan(cnt);
   if (lane == 63) sh.red[0][w] = inc;
   __syncthreads();
-  unsigned run = inc - sum, total = 0u;
+  unsigned start = inc - cnt, total = 0u;
 #pragma unroll
   for (int w2 = 0; w2 < kWaves; ++w2) {
     const unsigned x = sh.red[0][w2];
     total += x;
-    run += unsigned(w2) < w ? x : 0u;
+    start += unsigned(w2) < w ? x : 0u;
   }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const unsigned sl = 4u * t + unsigned(q);
-    if (sl < ns) u.start[sl] = run;
-    run += c4[q];
-  }
+  if (t < ns) u.start[t] = start;
   if (t == 0) u.start[ns] = total;
+  if (cnt > unsigned(kSpecEntries)) u.over[atomicAdd(&u.nover, 1u)] = t;
   __syncthreads();
-  const uint2* slots = p.cand_out + size_t(r) * ns * p.cap;
-  // position q lies in the last slot whose start is <= q
-  auto from_slots = [&](unsigned q) -> unsigned long long {
-    unsigned lo = 0u, hi = ns;  // start[lo] <= q < start[hi]
-    while (hi - lo > 1u) {
-      const unsigned mid = (lo + hi) >> 1;
-      if (u.start[mid] <= q) lo = mid;
-      else hi = mid;
-    }
-    return composite(slots[size_t(lo) * p.cap + (q - u.start[lo])]);
-  };
   if (total > unsigned(kRankCap)) {  // rare (heavy ties, or a bound that came late)
+    // position q lies in the last slot whose start is <= q
+    auto from_slots = [&](unsigned q) -> unsigned long long {
+      unsigned lo = 0u, hi = ns;  // start[lo] <= q < start[hi]
+      while (hi - lo > 1u) {
+        const unsigned mid = (lo + hi) >> 1;
+        if (u.start[mid] <= q) lo = mid;
+        else hi = mid;
+      }
+      return composite(slots[size_t(lo) * p.cap + (q - u.start[lo])]);
+    };
     if (part == 0u) onepass_topw<BEAM>(p, u, r, total, from_slots);
     return;
   }
-  constexpr int kNR = kRankCap / kThreads;
-  unsigned long long c[kNR];
 #pragma unroll
-  for (int i = 0; i < kNR; ++i) {
-    const unsigned q = unsigned(i) * kThreads + t;
-    c[i] = q < total ? from_slots(q) : 0ull;
-  }
-#pragma unroll
-  for (int i = 0; i < kNR; ++i) {
-    const unsigned q = unsigned(i) * kThreads + t;
-    if (q < total) u.all[q] = c[i];
+  for (int i = 0; i < kSpecRows; ++i)
+    if (unsigned(i) * 32u < ns) {
+      const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
+      if (c < ns) {
+        const unsigned s0 = u.start[c], n = u.start[c + 1] - s0, j = 2u * (lane & 15u);
+        if (j < n) u.all[s0 + j] = composite(make_uint2(ent[i].x, ent[i].y));
+        if (j + 1u < n) u.all[s0 + j + 1u] = composite(make_uint2(ent[i].z, ent[i].w));
+      }
+    }
+  for (unsigned i = w; i < u.nover; i += kWaves) {  // wave-uniform
+    const unsigned c = u.over[i], s0 = u.start[c], n = u.start[c + 1] - s0;
+    const uint2* sl = slots + size_t(c) * p.cap;
+    for (unsigned j = kSpecEntries + lane; j < n; j += 64u) u.all[s0 + j] = composite(sl[j]);
   }
   __syncthreads();
-  bucket_rank_emit<BEAM>(p, u, r, u.all, total, part, nparts);
+  if (total > unsigned(kBruteRankMax)) {
+    bucket_rank_emit<BEAM>(p, u, r, u.all, total, part, nparts);
+    return;
+  }
+  // this workgroup's share: survivors part, part + nparts, ...; a survivor's
+  // place is the number of larger composites.  A group of 16 lanes counts
+  // for two survivors at once over interleaved pairs of positions, four pairs
+  // per lane in flight (positions up to total + 127 < kRankCap are read; the
+  // ones at or beyond total are not counted).
+  const unsigned sub = t & 15u, g = t >> 4;
+  constexpr unsigned kGroups = kThreads / 16u;
+  for (unsigned k = 0;; k += 2u * kGroups) {
+    if (part + nparts * k >= total) break;  // workgroup-uniform
+    const unsigned q0 = part + nparts * (k + g), q1 = part + nparts * (k + kGroups + g);
+    const unsigned long long x0 = u.all[q0 < total ? q0 : 0u], x1 = u.all[q1 < total ? q1 : 0u];
+    unsigned c0 = 0u, c1 = 0u;
+    for (unsigned j0 = 0; j0 < total; j0 += 128u) {
+      ulonglong2 y[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        y[i] = *reinterpret_cast<const ulonglong2*>(&u.all[j0 + 32u * unsigned(i) + 2u * sub]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const unsigned j = j0 + 32u * unsigned(i) + 2u * sub;
+        const bool v0 = j < total, v1 = j + 1u < total;
+        c0 += unsigned(v0 && y[i].x > x0) + unsigned(v1 && y[i].y > x0);
+        c1 += unsigned(v0 && y[i].x > x1) + unsigned(v1 && y[i].y > x1);
+      }
+    }
+    c0 += dppu<0xB1>(c0);   // quad_perm [1,0,3,2]
+    c1 += dppu<0xB1>(c1);
+    c0 += dppu<0x4E>(c0);   // quad_perm [2,3,0,1]
+    c1 += dppu<0x4E>(c1);
+    c0 += dppu<0x141>(c0);  // row_half_mirror
+    c1 += dppu<0x141>(c1);
+    c0 += dppu<0x140>(c0);  // row_mirror
+    c1 += dppu<0x140>(c1);
+    if (sub == 0u && q0 < total && c0 < p.W) emit_pick<BEAM>(p, r, c0, x0);
+    if (sub == 0u && q1 < total && c1 < p.W) emit_pick<BEAM>(p, r, c1, x1);
+  }
 }
 
 template <bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p) {
   __shared__ SelShared sh;
+  __shared__ BoundShared bs;
   __shared__ unsigned flag[2];
   __shared__ unsigned wmax[kWaves];
   const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
@@ -1553,9 +1700,7 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   const Red3 wr = wave_reduce(0u, (vm & 1u) ? lmax : ~0u, lmax);
   const unsigned km = unsigned(__popcll(__ballot((vm & 1u) && lmax == wr.hi)));
   if (lane_id() == 0) {
-    uint2* e = reinterpret_cast<uint2*>(p.ex + size_t(r) * p.nseg + c * kWaves + w);
-    st_agent(e, make_uint2(wr.hi, wr.lo));
-    st_agent(e + 1, make_uint2(km, 0u));
+    st_agent4(p.ex, (r * p.nseg + c * kWaves + w) * 16u, make_uint4(wr.hi, wr.lo, km, 0u));
     wmax[w] = wr.hi;
   }
   wait_stores();
@@ -1565,7 +1710,7 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   // 2. the bound: computed by the last arrival, waited for by the others
   unsigned bound;  // keys below it are dropped
   if (flag[0]) {
-    const unsigned long long bw = onepass_bound(p, sh, r);
+    const unsigned long long bw = onepass_bound(p, sh, bs, r);
     if (t == 0)
       __hip_atomic_store(&p.ctl->bound[r], bw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
