@@ -54,7 +54,7 @@ constexpr int kRankCap = 4096;                // survivors the rank kernel order
 constexpr int kRankPer = kThreads / 16;       // survivors ranked per workgroup (16 lanes each)
 constexpr int kRankBlocks = kRankCap / kRankPer;
 constexpr int kOnePassRankMax = 1024;         // widest result of the one-pass path
-constexpr int kOnePassFinalParts = 16;       // workgroups per request placing survivors
+constexpr int kOnePassFinalParts = 64;       // workgroups per request placing survivors (at most)
 constexpr int kOnePassSegPer = 8;             // wave summaries per thread of the bound:
                                               // chunks <= kOnePassSegPer * kThreads / 8
 static_assert(kNI == 32, "validity masks are 32-bit");
@@ -81,6 +81,7 @@ struct SelectParams {
   struct OnePassCtl* ctl;   // per-request counters and bound word
   uint4* ex;                // [R][nseg] per wave: (M, m, kM, 0), see the one-pass path
   unsigned long long wait_ticks;  // how long a workgroup waits for the bound (wall clock)
+  unsigned fparts;          // workgroups per request of the final kernel
 };
 
 // Per-request cross-workgroup state of the one-pass path, at the start of the
@@ -258,6 +259,42 @@ __device__ inline void ordered_apply(unsigned f, const Ordered& o, SelShared& sh
     if ((f >> i) & 1u) fn(i, sh.tab[i * kWaves + w] + ((o.pre[i / 4] >> (8 * (i % 4))) & 0xffu));
 }
 
+// Ordered compaction for a filter that keeps few elements: only the slots
+// that some lane of the wave flags are visited (wave-uniform loops over the
+// set bits of the wave's OR).  sh.tab must be zero on entry (the counts of
+// the slots no wave visits).  Returns the flagged count; apply_sparse() calls
+// fn(i, rank) as ordered_apply() does.
+__device__ inline unsigned ordered_plan_sparse(unsigned f, SelShared& sh) {
+  const unsigned lane = lane_id(), w = threadIdx.x >> 6;
+  for (unsigned any = wave_or(f); any != 0u; any &= any - 1u) {
+    const int i = __builtin_ctz(any);
+    const unsigned long long b = __ballot((f >> i) & 1u);
+    if (lane == 0) sh.tab[i * kWaves + w] = unsigned(__popcll(b));
+  }
+  __syncthreads();
+  if (w == 0) {
+    const uint4 v = reinterpret_cast<const uint4*>(sh.tab)[lane];
+    const unsigned s = v.x + v.y + v.z + v.w;
+    const unsigned inc = wave_scan(s);
+    const unsigned ex = inc - s;
+    reinterpret_cast<uint4*>(sh.tab)[lane] =
+        make_uint4(ex, ex + v.x, ex + v.x + v.y, ex + v.x + v.y + v.z);
+    if (lane == 63) sh.tab[kNI * kWaves] = inc;
+  }
+  __syncthreads();
+  return sh.tab[kNI * kWaves];
+}
+
+template <typename F>
+__device__ inline void ordered_apply_sparse(unsigned f, SelShared& sh, F&& fn) {
+  const unsigned w = threadIdx.x >> 6;
+  for (unsigned any = wave_or(f); any != 0u; any &= any - 1u) {
+    const int i = __builtin_ctz(any);
+    const unsigned long long b = __ballot((f >> i) & 1u);
+    if ((f >> i) & 1u) fn(i, sh.tab[i * kWaves + w] + mbcnt(b));
+  }
+}
+
 // ---- histograms ------------------------------------------------------------
 
 // hist[bin] += 1 for every lane with act.  The most frequent bin of the wave
@@ -288,7 +325,8 @@ __device__ inline void find_bin(SelShared& sh, unsigned need) {
   if (lane == 63) sh.red[0][w] = inc;
   __syncthreads();
   unsigned above = inc - s;
-  for (unsigned w2 = 0; w2 < w; ++w2) above += sh.red[0][w2];
+#pragma unroll
+  for (unsigned w2 = 0; w2 < unsigned(kWaves); ++w2) above += w2 < w ? sh.red[0][w2] : 0u;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     if (above < need && need <= above + hb[j]) {
@@ -1138,9 +1176,10 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
 //      exact top W when they overflow it), with the count and the chunk's
 //      largest key;
 //   4. the final kernel places the survivors: each one's place is the number
-//      of larger (key, ~index) composites, counted through a key histogram
-//      (up to kRankCap survivors, staged in LDS by each of the request's
-//      kOnePassFinalParts workgroups, which place a share each); with more,
+//      of larger (key, ~index) composites, counted directly (up to
+//      kBruteRankMax survivors) or through a key histogram (up to kRankCap;
+//      staged in LDS by each of the request's fparts workgroups, which place
+//      a share each); with more,
 //      one workgroup finds their exact top W first (radix cut, ties in index
 //      order, re-reading the slots on every pass).  It also returns the
 //      request's counters to zero.
@@ -1201,7 +1240,7 @@ struct BoundShared {
   uint2 ev[kBoundList];          // (key, weight) of the events in the chosen bin
   unsigned nev;
   unsigned red[2][kWaves];
-  unsigned part[kOnePassSegPer][kWaves];  // guaranteed counts at B per (summary row, wave)
+  alignas(16) unsigned gc[kOnePassSegPer * kThreads / kWaves];  // guaranteed count at B per chunk
 };
 
 // Bound word of request r from every wave's summary (see step 2 above):
@@ -1345,40 +1384,31 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
   }
   // c*: the chunks' guaranteed counts at B, summed in chunk order.  Thread t
   // holds summary i * kThreads + t, i.e. wave t % 8 of chunk i * 64 + t / 8:
-  // a chunk's count is a sum over 8 adjacent lanes, and chunk order is (i,
-  // wave, lane) order.
-  unsigned gch[kOnePassSegPer], excl[kOnePassSegPer];
+  // a chunk's count is a sum over 8 adjacent lanes, stored by the first of
+  // them (rows beyond nseg have no live lanes and store zeros); one wave
+  // then scans the chunks in order.
 #pragma unroll
   for (int i = 0; i < kOnePassSegPer; ++i) {
-    gch[i] = 0u;
-    excl[i] = 0u;
-    if (unsigned(i) * kThreads < nseg) {
-      unsigned g = nl[i] > 0u ? (e[i].y >= B ? nl[i] : (e[i].x >= B ? e[i].z : 0u)) : 0u;
-      g += dppu<0xB1>(g);   // quad_perm [1,0,3,2]
-      g += dppu<0x4E>(g);   // quad_perm [2,3,0,1]
-      g += dppu<0x141>(g);  // row_half_mirror: the other quad of the 8 lanes
-      gch[i] = g;
-      const unsigned x = (lane & 7u) == 0u ? g : 0u;
-      const unsigned inc = wave_scan(x);
-      excl[i] = inc - x;
-      if (lane == 63) bs.part[i][w] = inc;
-    }
+    unsigned g = nl[i] > 0u ? (e[i].y >= B ? nl[i] : (e[i].x >= B ? e[i].z : 0u)) : 0u;
+    g += dppu<0xB1>(g);   // quad_perm [1,0,3,2]
+    g += dppu<0x4E>(g);   // quad_perm [2,3,0,1]
+    g += dppu<0x141>(g);  // row_half_mirror: the other quad of the 8 lanes
+    if ((lane & 7u) == 0u) bs.gc[unsigned(i) * 64u + t / 8u] = g;
   }
   if (t == 0) sh.digit = ~0u;  // (c* always exists: the counts at B reach W)
   __syncthreads();
-  unsigned before = 0u;
+  if (w == 0) {  // lane l: chunks 8 l .. 8 l + 7
+    const uint4 a = reinterpret_cast<const uint4*>(bs.gc)[2u * lane];
+    const uint4 b = reinterpret_cast<const uint4*>(bs.gc)[2u * lane + 1u];
+    const unsigned v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    const unsigned sum = a.x + a.y + a.z + a.w + b.x + b.y + b.z + b.w;
+    unsigned before = wave_scan(sum) - sum;
 #pragma unroll
-  for (int i = 0; i < kOnePassSegPer; ++i)
-    if (unsigned(i) * kThreads < nseg) {
-      unsigned b = before + excl[i];
-#pragma unroll
-      for (int w2 = 0; w2 < kWaves; ++w2) {
-        const unsigned x = bs.part[i][w2];
-        b += unsigned(w2) < w ? x : 0u;
-        before += x;
-      }
-      if ((lane & 7u) == 0u && b < W && b + gch[i] >= W) sh.digit = unsigned(i) * 64u + t / 8u;
+    for (int q = 0; q < 8; ++q) {
+      if (before < W && before + v[q] >= W) sh.digit = 8u * lane + unsigned(q);
+      before += v[q];
     }
+  }
   __syncthreads();
   return (static_cast<unsigned long long>(sh.digit + 1u) << 32) | B;
 }
@@ -1623,16 +1653,21 @@ __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, un
     if (part == 0u) onepass_topw<BEAM>(p, u, r, total, from_slots);
     return;
   }
+  // starts of every row's slots first (in bounds for every row: c < kThreads),
+  // then the writes
+  unsigned s0[kSpecRows], nn[kSpecRows];
 #pragma unroll
-  for (int i = 0; i < kSpecRows; ++i)
-    if (unsigned(i) * 32u < ns) {
-      const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
-      if (c < ns) {
-        const unsigned s0 = u.start[c], n = u.start[c + 1] - s0, j = 2u * (lane & 15u);
-        if (j < n) u.all[s0 + j] = composite(make_uint2(ent[i].x, ent[i].y));
-        if (j + 1u < n) u.all[s0 + j + 1u] = composite(make_uint2(ent[i].z, ent[i].w));
-      }
-    }
+  for (int i = 0; i < kSpecRows; ++i) {
+    const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
+    s0[i] = u.start[c];
+    nn[i] = c < ns ? u.start[c + 1] - s0[i] : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < kSpecRows; ++i) {
+    const unsigned j = 2u * (lane & 15u);
+    if (j < nn[i]) u.all[s0[i] + j] = composite(make_uint2(ent[i].x, ent[i].y));
+    if (j + 1u < nn[i]) u.all[s0[i] + j + 1u] = composite(make_uint2(ent[i].z, ent[i].w));
+  }
   for (unsigned i = w; i < u.nover; i += kWaves) {  // wave-uniform
     const unsigned c = u.over[i], s0 = u.start[c], n = u.start[c + 1] - s0;
     const uint2* sl = slots + size_t(c) * p.cap;
@@ -1644,40 +1679,31 @@ __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, un
     return;
   }
   // this workgroup's share: survivors part, part + nparts, ...; a survivor's
-  // place is the number of larger composites.  A group of 16 lanes counts
-  // for two survivors at once over interleaved pairs of positions, four pairs
-  // per lane in flight (positions up to total + 127 < kRankCap are read; the
-  // ones at or beyond total are not counted).
-  const unsigned sub = t & 15u, g = t >> 4;
-  constexpr unsigned kGroups = kThreads / 16u;
-  for (unsigned k = 0;; k += 2u * kGroups) {
+  // place is the number of larger composites.  A wave counts for two
+  // survivors at once over interleaved pairs of positions, four pairs per
+  // lane in flight (positions up to total + 511 < kRankCap are read; the ones
+  // at or beyond total are not counted).
+  for (unsigned k = 0;; k += 2u * kWaves) {
     if (part + nparts * k >= total) break;  // workgroup-uniform
-    const unsigned q0 = part + nparts * (k + g), q1 = part + nparts * (k + kGroups + g);
+    const unsigned q0 = part + nparts * (k + w), q1 = part + nparts * (k + kWaves + w);
     const unsigned long long x0 = u.all[q0 < total ? q0 : 0u], x1 = u.all[q1 < total ? q1 : 0u];
     unsigned c0 = 0u, c1 = 0u;
-    for (unsigned j0 = 0; j0 < total; j0 += 128u) {
+    for (unsigned j0 = 0; j0 < total; j0 += 512u) {
       ulonglong2 y[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        y[i] = *reinterpret_cast<const ulonglong2*>(&u.all[j0 + 32u * unsigned(i) + 2u * sub]);
+        y[i] = *reinterpret_cast<const ulonglong2*>(&u.all[j0 + 128u * unsigned(i) + 2u * lane]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const unsigned j = j0 + 32u * unsigned(i) + 2u * sub;
+        const unsigned j = j0 + 128u * unsigned(i) + 2u * lane;
         const bool v0 = j < total, v1 = j + 1u < total;
         c0 += unsigned(v0 && y[i].x > x0) + unsigned(v1 && y[i].y > x0);
         c1 += unsigned(v0 && y[i].x > x1) + unsigned(v1 && y[i].y > x1);
       }
     }
-    c0 += dppu<0xB1>(c0);   // quad_perm [1,0,3,2]
-    c1 += dppu<0xB1>(c1);
-    c0 += dppu<0x4E>(c0);   // quad_perm [2,3,0,1]
-    c1 += dppu<0x4E>(c1);
-    c0 += dppu<0x141>(c0);  // row_half_mirror
-    c1 += dppu<0x141>(c1);
-    c0 += dppu<0x140>(c0);  // row_mirror
-    c1 += dppu<0x140>(c1);
-    if (sub == 0u && q0 < total && c0 < p.W) emit_pick<BEAM>(p, r, c0, x0);
-    if (sub == 0u && q1 < total && c1 < p.W) emit_pick<BEAM>(p, r, c1, x1);
+    const Red3 r0 = wave_reduce(c0, 0u, 0u), r1 = wave_reduce(c1, 0u, 0u);
+    if (lane == 0u && q0 < total && r0.sum < p.W) emit_pick<BEAM>(p, r, r0.sum, x0);
+    if (lane == 1u && q1 < total && r1.sum < p.W) emit_pick<BEAM>(p, r, r1.sum, x1);
   }
 }
 
@@ -1693,6 +1719,7 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   const unsigned t = threadIdx.x, w = t >> 6;
   unsigned key[kNI];
   const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
+  if (t < (kNI * kWaves + 4) / 4) reinterpret_cast<uint4*>(sh.tab)[t] = make_uint4(0u, 0u, 0u, 0u);
   // 1. this wave's (M, m), published; the workgroup counts itself in
   unsigned lmax = 0u;  // invalid slots hold key 0
 #pragma unroll
@@ -1730,37 +1757,41 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   unsigned keep = vm;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < bound) << i);
-  Ordered o = ordered_plan(keep, sh);
-  if (o.total > p.cap) {  // a chunk's exact top W of its survivors
+  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
+  auto put = [&](int i, unsigned rank) {
+    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + t);
+  };
+  unsigned total = ordered_plan_sparse(keep, sh);
+  if (total > p.cap) {  // a chunk's exact top W of its survivors
     __syncthreads();
     keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
-    o = ordered_plan(keep, sh);
+    const Ordered o = ordered_plan(keep, sh);
+    ordered_apply(keep, o, sh, put);
+    total = o.total;
+  } else {
+    ordered_apply_sparse(keep, sh, put);
   }
-  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
-  ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
-    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + t);
-  });
   if (t == 0) {
     unsigned top = 0u;
 #pragma unroll
     for (int w2 = 0; w2 < kWaves; ++w2) top = max(top, wmax[w2]);
-    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(o.total, top);
+    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(total, top);
   }
 }
 
-// 4. kOnePassFinalParts workgroups per request, after the pass: each stages
+// 4. fparts (<= kOnePassFinalParts) workgroups per request, after the pass: each stages
 // all survivors and places its share of them; the first also returns the
 // request's counters to zero for the next call.
 template <bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectParams p) {
   __shared__ OnePassShared u;
-  const unsigned r = blockIdx.x / kOnePassFinalParts;
-  const unsigned part = blockIdx.x - r * kOnePassFinalParts;
+  const unsigned r = blockIdx.x / p.fparts;
+  const unsigned part = blockIdx.x - r * p.fparts;
   if (threadIdx.x == 0 && part == 0u) {
     p.ctl->arrive[r] = 0u;
     p.ctl->bound[r] = 0ull;
   }
-  onepass_final<BEAM>(p, u, r, part, kOnePassFinalParts);
+  onepass_final<BEAM>(p, u, r, part, p.fparts);
 }
 
 
@@ -1839,7 +1870,10 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
     else select_onepass_kernel<false><<<blocks, kThreads, 0, st>>>(p);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const unsigned fblocks = unsigned(R) * kOnePassFinalParts;
+    // a share of survivors per workgroup, the whole call in about one round of
+    // workgroups (one per compute unit)
+    p.fparts = std::max(1u, std::min(unsigned(kOnePassFinalParts), 256u / unsigned(R)));
+    const unsigned fblocks = unsigned(R) * p.fparts;
     if (has_beam) select_onepass_final_kernel<true><<<fblocks, kThreads, 0, st>>>(p);
     else select_onepass_final_kernel<false><<<fblocks, kThreads, 0, st>>>(p);
     return hipGetLastError();
