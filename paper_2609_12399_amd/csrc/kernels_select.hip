@@ -189,6 +189,16 @@ __device__ inline unsigned shr(unsigned x, int s) {
   return unsigned(static_cast<unsigned long long>(x) >> s);
 }
 
+// Buffer resource of `bytes` bytes at `base` (a workgroup-uniform base; byte
+// offsets stay below 2^31).  An access at or beyond `bytes` touches no
+// memory (a load returns zeros), which lets a variable number of loads issue
+// without a branch: a load under a branch is waited for where the branch
+// joins, which serialises loads that should be in flight together.
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes = 0x7fffffff) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), bytes,
+                                           0x00020000);
+}
+
 // ---- keys ------------------------------------------------------------------
 
 // Monotone key of an fp32 score: larger score -> larger key, -0 < +0, every
@@ -851,20 +861,27 @@ __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p)
   unsigned keep = vm;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < bound) << i);
-  Ordered o = ordered_plan(keep, sh);
-  if (o.total > p.cap) {  // rare: keep the chunk's exact top W of the survivors
+  if (threadIdx.x < (kNI * kWaves + 4) / 4)  // the sparse compaction's zero counts
+    reinterpret_cast<uint4*>(sh.tab)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
+  auto put = [&](int i, unsigned rank) {
+    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + threadIdx.x);
+  };
+  unsigned total = ordered_plan_sparse(keep, sh);
+  if (total > p.cap) {  // rare: keep the chunk's exact top W of the survivors
     __syncthreads();
     keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
-    o = ordered_plan(keep, sh);
+    const Ordered o = ordered_plan(keep, sh);
+    ordered_apply(keep, o, sh, put);
+    total = o.total;
+  } else {
+    ordered_apply_sparse(keep, sh, put);
   }
-  uint2* out = p.cand_out + (size_t(r) * p.nwg + c) * p.cap;
-  ordered_apply(keep, o, sh, [&](int i, unsigned rank) {
-    out[rank] = make_uint2(key[i], base + unsigned(i) * kThreads + threadIdx.x);
-  });
   if (threadIdx.x == 0) {  // (count, largest key of the chunk: its waves' maxima)
     unsigned top = 0u;
     for (int w = 0; w < kWaves; ++w) top = max(top, seg[c * kWaves + unsigned(w)]);
-    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(o.total, top);
+    reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(total, top);
   }
 }
 
@@ -1066,8 +1083,8 @@ __device__ inline void gather_rounds(const SelectParams& p, FinalShared& fs, uns
 // LDS of the rank kernel's usual path.
 struct RankShared {
   unsigned start[kSelectMaxGatherSlots + 1];  // slot s holds positions [start[s], start[s+1])
-  alignas(16) unsigned long long all[kRankCap];  // every survivor's composite, by position
-  unsigned red[kWaves];
+  alignas(16) unsigned long long all[kRankCap + 128];  // every survivor's composite, by position
+  unsigned red[kWaves];                                 // (+ what the counting loop overreads)
 };
 
 template <bool BEAM>
@@ -1082,12 +1099,12 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
   const unsigned lane = lane_id(), w = t >> 6;
   // slot counts (thread t: slots 4t .. 4t + 3) and their exclusive prefix
   unsigned c4[4], sum = 0u;
-  {
-    const uint2* cm = reinterpret_cast<const uint2*>(p.cnt_in) + size_t(r) * ns;
+  {  // (slots beyond ns read as zero counts, without a branch)
+    const __amdgpu_buffer_rsrc_t rs =
+        buffer_rsrc(reinterpret_cast<const uint2*>(p.cnt_in) + size_t(r) * ns, int(ns * 8u));
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const unsigned sl = 4u * t + unsigned(q);
-      c4[q] = sl < ns ? cm[sl].x : 0u;
+      c4[q] = __builtin_amdgcn_raw_buffer_load_b32(rs, (4u * t + unsigned(q)) * 8u, 0, 0);
       sum += c4[q];
     }
   }
@@ -1132,14 +1149,22 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
   }
   __syncthreads();
   // survivor i = 32 b + t / 16: its rank is the number of larger composites,
-  // counted by 16 lanes over interleaved pairs of positions
+  // counted by 16 lanes over interleaved pairs of positions, four pairs per
+  // lane in flight (positions up to total + 127 < kRankCap + 128 are read;
+  // the ones at or beyond total are not counted)
   const unsigned i = b * unsigned(kRankPer) + (t >> 4), sub = t & 15u;
   const unsigned long long mine = u.rk.all[i < total ? i : 0u];
   unsigned cnt = 0u;
-  for (unsigned j = 2u * sub; j < total; j += 32u) {
-    const ulonglong2 x = *reinterpret_cast<const ulonglong2*>(&u.rk.all[j]);
-    cnt += unsigned(x.x > mine);
-    cnt += unsigned(j + 1u < total && x.y > mine);
+  for (unsigned j0 = 0; j0 < total; j0 += 128u) {
+    ulonglong2 x[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      x[k] = *reinterpret_cast<const ulonglong2*>(&u.rk.all[j0 + 32u * unsigned(k) + 2u * sub]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const unsigned j = j0 + 32u * unsigned(k) + 2u * sub;
+      cnt += unsigned(j < total && x[k].x > mine) + unsigned(j + 1u < total && x[k].y > mine);
+    }
   }
   cnt += dppu<0xB1>(cnt);   // quad_perm [1,0,3,2]
   cnt += dppu<0x4E>(cnt);   // quad_perm [2,3,0,1]
@@ -1208,18 +1233,11 @@ __device__ inline unsigned long long wait_bound(unsigned long long* word,
 // fence, several microseconds with 256 workgroups issuing them) is needed.
 // A writer waits for its stores to complete (vmcnt(0), the vector memory
 // counter also covers stores on this architecture) before it updates a
-// counter.  Buffer accesses from a workgroup-uniform base; byte offsets stay
-// below 2^31.
-// A buffer access at or beyond `bytes` touches no memory (a load returns
-// zeros), which lets a variable number of loads issue without a branch.
-__device__ inline __amdgpu_buffer_rsrc_t agent_rsrc(const void* base, int bytes = 0x7fffffff) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), bytes,
-                                           0x00020000);
-}
+// counter.
 constexpr int kAgentScope = 16;  // cache policy bit sc1
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 __device__ inline void st_agent4(void* base, unsigned off, uint4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), agent_rsrc(base), off, 0,
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), buffer_rsrc(base), off, 0,
                                          kAgentScope);
 }
 __device__ inline uint4 ld_agent4(__amdgpu_buffer_rsrc_t rs, unsigned off) {
@@ -1265,7 +1283,7 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
   // all rows are issued at once: the ones beyond nseg read nothing (a load
   // under a branch would be waited for where the branch joins)
   uint4 e[kOnePassSegPer];  // (M, m, kM, 0)
-  const __amdgpu_buffer_rsrc_t rs = agent_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
 #pragma unroll
   for (int i = 0; i < kOnePassSegPer; ++i) e[i] = ld_agent4(rs, (unsigned(i) * kThreads + t) * 16u);
   // while the summaries are in flight: clear the histogram and the list
@@ -1417,7 +1435,8 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
 struct OnePassShared {
   SelShared sh;
   unsigned start[kSelectMaxGatherSlots + 1];      // slot s holds positions [start[s], start[s+1])
-  alignas(16) unsigned long long all[kRankCap];   // survivors' composites, when they fit
+  alignas(16) unsigned long long all[kRankCap + 128];  // survivors' composites, when they fit
+                                                       // (+ a spare pair per lane)
   alignas(16) unsigned long long buck[kRankCap];  // the same, grouped by key bin
   alignas(16) unsigned long long top[kOnePassRankMax];  // the exact top W
   unsigned bstart[2048];                          // first position of each key bin in buck
@@ -1617,12 +1636,17 @@ __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, un
   const uint2* slots = p.cand_out + size_t(r) * ns * p.cap;
   const unsigned cnt = t < ns ? reinterpret_cast<const uint2*>(p.cnt_out)[size_t(r) * ns + t].x : 0u;
   uint4 ent[kSpecRows];  // entries 2 (lane % 16), + 1 of slot 32 i + 4 w + lane / 16
-  // every row is loaded, from clamped addresses: a load under a branch is
-  // waited for where the branch joins, which would serialise the rows
+  // every row is issued (a load under a branch is waited for where the
+  // branch joins, which would serialise the rows); rows beyond the request's
+  // slots fall outside the buffer and read nothing
+  {
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(slots, int(ns * p.cap * 8u));
 #pragma unroll
-  for (int i = 0; i < kSpecRows; ++i) {
-    const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
-    ent[i] = reinterpret_cast<const uint4*>(slots + size_t(c < ns ? c : 0u) * p.cap)[lane & 15u];
+    for (int i = 0; i < kSpecRows; ++i) {
+      const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
+      ent[i] = __builtin_bit_cast(
+          uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (c * p.cap + 2u * (lane & 15u)) * 8u, 0, 0));
+    }
   }
   if (t == 0) u.nover = 0u;
   const unsigned inc = wave_scan(cnt);
@@ -1635,8 +1659,10 @@ __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, un
     total += x;
     start += unsigned(w2) < w ? x : 0u;
   }
-  if (t < ns) u.start[t] = start;
-  if (t == 0) u.start[ns] = total;
+  // start[c] = total for every c >= ns (c <= kThreads), so that the slots
+  // beyond the request's chunks read as empty
+  u.start[t] = t < ns ? start : total;
+  if (t == 0) u.start[kThreads] = total;
   if (cnt > unsigned(kSpecEntries)) u.over[atomicAdd(&u.nover, 1u)] = t;
   __syncthreads();
   if (total > unsigned(kRankCap)) {  // rare (heavy ties, or a bound that came late)
@@ -1653,25 +1679,39 @@ __device__ inline void onepass_final(const SelectParams& p, OnePassShared& u, un
     if (part == 0u) onepass_topw<BEAM>(p, u, r, total, from_slots);
     return;
   }
-  // starts of every row's slots first (in bounds for every row: c < kThreads),
-  // then the writes
+  // starts of the rows' slots first (c < kThreads), then the writes of the
+  // rows that hold chunks, unconditional: an entry past its slot's count
+  // goes to a lane's own spare place after the staged range
   unsigned s0[kSpecRows], nn[kSpecRows];
 #pragma unroll
-  for (int i = 0; i < kSpecRows; ++i) {
+  for (int i = 0; i < kSpecRows; ++i) {  // (no branch around reads: see the loads above)
     const unsigned c = unsigned(i) * 32u + 4u * w + (lane >> 4);
     s0[i] = u.start[c];
-    nn[i] = c < ns ? u.start[c + 1] - s0[i] : 0u;
+    nn[i] = u.start[c + 1] - s0[i];  // 0 beyond the request's chunks
   }
+  const unsigned j = 2u * (lane & 15u), spare = unsigned(kRankCap) + 2u * lane;
 #pragma unroll
-  for (int i = 0; i < kSpecRows; ++i) {
-    const unsigned j = 2u * (lane & 15u);
-    if (j < nn[i]) u.all[s0[i] + j] = composite(make_uint2(ent[i].x, ent[i].y));
-    if (j + 1u < nn[i]) u.all[s0[i] + j + 1u] = composite(make_uint2(ent[i].z, ent[i].w));
-  }
+  for (int i = 0; i < kSpecRows; ++i)
+    if (unsigned(i) * 32u < ns) {
+      u.all[j < nn[i] ? s0[i] + j : spare] = composite(make_uint2(ent[i].x, ent[i].y));
+      u.all[j + 1u < nn[i] ? s0[i] + j + 1u : spare + 1u] = composite(make_uint2(ent[i].z, ent[i].w));
+    }
   for (unsigned i = w; i < u.nover; i += kWaves) {  // wave-uniform
     const unsigned c = u.over[i], s0 = u.start[c], n = u.start[c + 1] - s0;
     const uint2* sl = slots + size_t(c) * p.cap;
-    for (unsigned j = kSpecEntries + lane; j < n; j += 64u) u.all[s0 + j] = composite(sl[j]);
+    for (unsigned j0 = kSpecEntries; j0 < n; j0 += 512u) {  // 8 loads per lane in flight
+      uint2 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const unsigned jj = j0 + 64u * unsigned(k) + lane;
+        v[k] = sl[jj < n ? jj : n - 1u];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const unsigned jj = j0 + 64u * unsigned(k) + lane;
+        if (jj < n) u.all[s0 + jj] = composite(v[k]);
+      }
+    }
   }
   __syncthreads();
   if (total > unsigned(kBruteRankMax)) {
