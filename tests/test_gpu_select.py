@@ -72,6 +72,34 @@ def test_select_matches_oracle(name, R, P, V, W, kind, with_beam):
             f"request {r}: scores differ"
 
 
+@pytest.mark.parametrize("tied_slots", [6, 32], ids=["histogram_ranked", "exact_cut"])
+def test_select_one_pass_many_tied_survivors(tied_slots):
+    """Ties held by the first lane of every wave (a chunk's candidate at slot
+    i of lane t sits at position 512 i + t): each wave then guarantees one
+    candidate at the tied key, so all chunks up to c* (the 64th) keep every
+    tied candidate of theirs, 64 x 8 x tied_slots survivors -- more than the
+    final stage ranks by direct comparison (6 slots: 3072, ranked through the
+    key histogram) or more than it stages at all (32 slots: 16384, the exact
+    top-W cut over the slots).  The result is the W tied candidates with the
+    lowest flat indices."""
+    import torch
+    from paper_2609_12399_amd.runner import BeamSelector
+    R, P, V, W = 1, 512, SELECT_CODEBOOK, 512
+    rng = np.random.default_rng(7 + tied_slots)
+    logp = (-1.0 - rng.random(P * V, dtype=np.float32)).astype(np.float32)
+    q = np.arange(P * V)
+    logp[(q % 64 == 0) & ((q % 16384) // 512 < tied_slots)] = 0.0
+    logp = logp.reshape(R, P, V)
+    print(f"one-pass tied survivors: {64 * 8 * tied_slots}", flush=True)
+    sel = BeamSelector(R, P, V, W)
+    par, tok, sc = sel(torch.from_numpy(logp).cuda(), None)
+    torch.cuda.synchronize()
+    op, ot, osc = orc.select_beams(logp[0], W, None)
+    assert np.array_equal(par.cpu().numpy()[0], op)
+    assert np.array_equal(tok.cpu().numpy()[0], ot)
+    assert np.array_equal(sc.cpu().numpy()[0].view(np.int32), osc.view(np.int32))
+
+
 def test_select_all_equal_keeps_lowest_indices():
     import torch
     from paper_2609_12399_amd.runner import BeamSelector
