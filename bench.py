@@ -654,7 +654,10 @@ def main():
                          "flops": flops,
                          "count": "the fp32 products of the chunked method as computed: "
                                   "K K^T, T.(diag(beta gamma) K), T.(diag(beta) V) per "
-                                  "chunk, W' S^T and K^T D' per chunk and 16-row block"},
+                                  "chunk, W' S^T and K^T D' per chunk and 16-row block "
+                                  "(with bf16 keys the products with T and K^T D' run as "
+                                  "exact products of bf16 parts on the bf16 instruction; "
+                                  "counted once, as fp32 products)"},
             "note": "onela_prefill_state (token by token) vs onela_prefill_state_chunked "
                     "(64-token chunks); setup work, not part of `value`"}
         log(f"[bench] prefill {spec.P} tokens: sequential {seq_ms:.2f} ms, chunked {chk_ms:.3f} ms")

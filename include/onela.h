@@ -230,7 +230,8 @@ onela_status_t onela_prefill_state(const onela_config_t* cfg, int32_t prompt_len
  * delta_t of Eq. 2 solve a unit lower-triangular 64 x 64 system whose
  * matrices depend only on the chunk's own tokens (formed for all chunks in
  * parallel); a second launch then carries the state across the chunks in
- * order, on fp32 MFMA.  Inputs and output as for onela_prefill_state.
+ * order, on the matrix cores (fp32 products, and for bf16 keys exact products
+ * of bf16 parts).  Inputs and output as for onela_prefill_state.
  * Workspace: onela_prefill_workspace_bytes(cfg, prompt_len) bytes (0 for an
  * empty prompt, or for an invalid cfg), 256-byte aligned, owned by the caller
  * and used only by the enqueued work: per (request, value head, chunk) the

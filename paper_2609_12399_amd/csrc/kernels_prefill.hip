@@ -32,7 +32,9 @@
 //   phase 2 (prefill_scan_kernel): one workgroup per (request, value head, 16
 //     state rows; the row blocks of a head share one XCD) walks the chunks in
 //     order: X^T = W' S^T, D'^T = U'^T - X^T, S^T <- g S^T + K^T D'^T, on
-//     v_mfma_f32_16x16x4f32.  Wave w owns the state columns 16 w .. 16 w + 15
+//     v_mfma_f32_16x16x4f32 (the update with bf16 keys on
+//     v_mfma_f32_16x16x32_bf16, D' split exactly into three bf16 parts, so
+//     that its products too are exact).  Wave w owns the state columns 16 w .. 16 w + 15
 //     (a 16 x 16 fp32 accumulator tile that never leaves registers); the
 //     contraction orders are chosen so that the tile is directly the B
 //     operand of the next chunk's X and X's output is directly the B operand
@@ -618,19 +620,44 @@ __global__ __launch_bounds__(4 * DK) void prefill_scan_kernel(PrefillParams p) {
           slice<NCP>(o.u[i], g0) - x;
     }
     __syncthreads();
-    // S^T <- g S^T + K^T D'^T: one independent chain per token tile, summed
-    f32x4 up[4], dd[4];
+    // S^T <- g S^T + K^T D'^T
+    f32x4 sum;
+    if constexpr (BF16) {
+      // on v_mfma_f32_16x16x32_bf16, two token tiles per 32-deep step: the
+      // step's k = 8 lq + i stands for token 16 (2 h + i / 4) + 4 lq + i % 4,
+      // so that the lane's keys are its 16-byte load as it stands and its D'
+      // values are its own components of the two tiles.  The keys are exact
+      // in bf16 and D' is split exactly into three bf16 parts, so every
+      // product is exact and only the fp32 accumulation rounds.
+      f32x4 up[2], uq[2], ur[2];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      dd[mt] = ds[mt][lane];
-      up[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 d0 = ds[2 * h][lane], d1 = ds[2 * h + 1][lane];
+        const float x[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        uint4 dh, dm, dl;
+        split3(x, dh, dm, dl);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        up[h] = mfma_bf16(o.k[h], dh, z);
+        uq[h] = mfma_bf16(o.k[h], dm, z);
+        ur[h] = mfma_bf16(o.k[h], dl, z);
+      }
+      sum = (up[0] + up[1]) + ((uq[0] + uq[1]) + (ur[0] + ur[1]));
+    } else {
+      // one fp32 chain per token tile, summed
+      f32x4 up[4], dd[4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        dd[mt] = ds[mt][lane];
+        up[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+          up[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.key(mt, j), dd[mt][j], up[mt], 0, 0, 0);
+      sum = (up[0] + up[1]) + (up[2] + up[3]);
     }
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        up[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.key(mt, j), dd[mt][j], up[mt], 0, 0, 0);
-    st = o.g * st + ((up[0] + up[1]) + (up[2] + up[3]));
+    st = o.g * st + sum;
   };
   // NS operand sets in flight: chunk c + NS - 1 is requested before chunk c
   // is processed.  (xp and ds are rewritten only after the next chunk's first
