@@ -801,9 +801,12 @@ __global__ __launch_bounds__(kThreads) void select_final_kernel(SelectParams p) 
 //     index order, in its chunk's slot of `cap` (>= W) pairs, with the count
 //     and the chunk's largest key; a chunk with more survivors than the slot
 //     holds keeps their exact top W;
-//   rank: up to kRankCap survivors (the usual case), workgroups of the whole
-//     chip each load every survivor of the request into LDS and rank 32 of
-//     them: a survivor's place in the result is the number of survivors
+//   place (at most kThreads chunks and W <= kOnePassRankMax): the filter's
+//     slots and counts have the one-pass layout, and the one-pass path's
+//     placing kernel finishes the call exactly as it finishes that path;
+//   rank (more chunks): up to kRankCap survivors (the usual case), workgroups
+//     of the whole chip each load every survivor of the request into LDS and
+//     rank 32 of them: a survivor's place in the result is the number of survivors
 //     before it in the total order (composite (key, ~index) compared as one
 //     64-bit integer, unique per candidate), and those placed below W are
 //     written out directly: no sort and no single-workgroup pass;
@@ -1829,7 +1832,7 @@ __global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectPa
   __shared__ OnePassShared u;
   const unsigned r = blockIdx.x / p.fparts;
   const unsigned part = blockIdx.x - r * p.fparts;
-  if (threadIdx.x == 0 && part == 0u) {
+  if (threadIdx.x == 0 && part == 0u && p.ctl != nullptr) {
     p.ctl->arrive[r] = 0u;
     p.ctl->bound[r] = 0ull;
   }
@@ -1935,6 +1938,16 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
     else select_filter_kernel<false><<<blocks, kThreads, 0, st>>>(p);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (plan.nchunks <= unsigned(kThreads) && p.W <= unsigned(kOnePassRankMax)) {
+      // the filter's slots have the one-pass layout: the one-pass placing
+      // kernel ranks them (no control block: R may exceed its requests)
+      p.ctl = nullptr;
+      p.fparts = std::max(1u, std::min(unsigned(kOnePassFinalParts), 256u / unsigned(R)));
+      const unsigned fblocks = unsigned(R) * p.fparts;
+      if (has_beam) select_onepass_final_kernel<true><<<fblocks, kThreads, 0, st>>>(p);
+      else select_onepass_final_kernel<false><<<fblocks, kThreads, 0, st>>>(p);
+      return hipGetLastError();
+    }
     p.cand_in = p.cand_out;
     p.cnt_in = p.cnt_out;
     p.nslots_in = plan.nchunks;

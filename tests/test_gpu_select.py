@@ -45,6 +45,11 @@ CASES = [
     ("one_pass_ties_w64", 1, 300, SELECT_CODEBOOK, 64, "ties", True),
     ("one_pass_r2_special", 2, 100, SELECT_CODEBOOK, 200, "special", True),
     ("one_pass_rising_w1024", 1, 1024, 4096, 1024, "rising", True),
+    # two-pass path ranked by the placing kernel of the one-pass path: more
+    # chunks than fit at once, with heavy ties (more survivors than it
+    # stages), and more requests than the one-pass control block has
+    ("two_pass_placed_r8_ties", 8, 256, SELECT_CODEBOOK, 256, "ties", True),
+    ("two_pass_placed_r80", 80, 4, SELECT_CODEBOOK, 8, "ties", True),
 ]
 
 
