@@ -282,11 +282,12 @@ onela_status_t onela_fullstate_step(const onela_config_t* cfg, int32_t step,
  *   workspace    device, >= the size from onela_select_workspace_bytes,
  *                256-byte aligned; owned by the caller.  It must be
  *                zero-filled before its first use (e.g. one hipMemsetAsync
- *                when it is allocated): its first 1 KiB holds per-request
- *                counters that workgroups of one launch use to exchange a
- *                bound, and every call leaves them at zero again, so a
- *                workspace may serve any number of calls of any shape, one
- *                at a time
+ *                when it is allocated): its first 129 KiB hold what the
+ *                workgroups of one launch use to exchange a bound (a call
+ *                counter, per-request bound words, wave summaries tagged
+ *                with the call), and every call leaves them ready for the
+ *                next, so a workspace may serve any number of calls of any
+ *                shape, one at a time
  *   stream       hipStream_t (NULL: the default stream)
  * Limits: 1 <= R <= 65536, 1 <= W <= min(4096, W_prev * V),
  * W_prev * V <= 2^29.  All pointers 4-byte aligned.  Enqueued asynchronously;

@@ -95,10 +95,11 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
   plan->group = unsigned(kSelectChunk) / cap;
   auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
   const unsigned nchunks = (N + kSelectChunk - 1) / kSelectChunk;
-  // Every plan starts with the one-pass path's control block, which no other
-  // data overwrites, so that a workspace shared by calls of any shape keeps
-  // its counters at zero between calls.
-  const size_t ctl = kSelectCtlBytes;
+  // Every plan starts with the one-pass path's control block and summary
+  // region, which no other data overwrites, so that a workspace shared by
+  // calls of any shape keeps the state the one-pass path carries from call
+  // to call.
+  const size_t ctl = kSelectCtlBytes + kSelectSummaryBytes;
   // Two-pass path: enough wave maxima (2048 candidates each) for a tight
   // bound, few enough chunks for the one-workgroup gather.
   if (N > unsigned(kSelectChunk) && uint64_t(N) >= uint64_t(2) * W * 2048u &&
@@ -106,8 +107,8 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
     plan->two_pass = true;
     plan->nchunks = nchunks;
     plan->nseg = nchunks * (kSelectThreads / 64);
-    plan->seg_off = ctl;  // [R][nseg] wave summaries: uint4 (one-pass), uint32 (two-pass)
-    plan->slot_off = ctl + up(size_t(R) * plan->nseg * 16 /* (M, m, kM, 0) */);
+    plan->seg_off = ctl;  // [R][nseg] wave maxima (two-pass)
+    plan->slot_off = ctl + up(size_t(R) * plan->nseg * 4);
     plan->cnt_off = plan->slot_off + up(size_t(R) * nchunks * cap * 8 /* (key, index) */);
     plan->total = plan->cnt_off + up(size_t(R) * nchunks * 8 /* (count, largest key) */);
     return true;

@@ -59,6 +59,9 @@ constexpr unsigned kSelectMaxCandidates = 1u << 29;  // W_prev * V per request
 constexpr int kSelectMaxGatherSlots = 2048;          // chunks per request, two-pass path
 constexpr int kSelectOnePassMaxRequests = 64;        // requests of a one-pass call
 constexpr size_t kSelectCtlBytes = 1024;             // one-pass control block, workspace start
+// One-pass wave summaries (16 bytes each, at most 8192: R * nchunks <= 1024),
+// right after the control block; no other path writes this region.
+constexpr size_t kSelectSummaryBytes = size_t(8192) * 16;
 
 // Launch plan (tree path).  Stage 0 reads the raw scores in nwg[0] chunks of
 // kSelectChunk per request; stage s >= 1 reads the nin[s] output slots of
@@ -72,7 +75,8 @@ struct SelectPlan {
   unsigned final_in;
   unsigned cap, group;
   size_t pair_off[2], count_off[2], total;
-  // Two-pass path (see kernels_select.hip): per request nseg wave maxima,
+  // Two-pass and one-pass paths (see kernels_select.hip): per request nseg
+  // wave maxima (two-pass; the one-pass summaries have their own region),
   // then nchunks slots of `cap` pairs and their counts.
   bool two_pass;
   unsigned nchunks, nseg;

@@ -80,17 +80,19 @@ struct SelectParams {
   unsigned nwg;             // workgroups per request
   double inv_v;             // 1 / V
   // one-pass path
-  struct OnePassCtl* ctl;   // per-request counters and bound word
-  uint4* ex;                // [R][nseg] per wave: (M, m, kM, 0), see the one-pass path
+  struct OnePassCtl* ctl;   // call counter and per-request bound words
+  uint4* ex;                // [R][nseg] per wave: (M, m, kM, check), see the one-pass path
   unsigned long long wait_ticks;  // how long a workgroup waits for the bound (wall clock)
   unsigned fparts;          // workgroups per request of the final kernel
 };
 
-// Per-request cross-workgroup state of the one-pass path, at the start of the
-// workspace.  Zero when a call starts; the call's final kernel zeroes its
-// entries again.
+// Cross-workgroup state of the one-pass path, at the start of the workspace
+// (zero-filled before the first call).  The bound words are zero when a call
+// starts, and the call's final kernel zeroes its requests' words again; the
+// epoch counts the calls (see the summaries' tags).
 struct OnePassCtl {
-  unsigned arrive[kSelectOnePassMaxRequests];  // workgroups that published their summaries
+  unsigned epoch;     // this call's tag is epoch + 1
+  unsigned pad_[3];
   unsigned long long bound[kSelectOnePassMaxRequests];  // (1 << 32) | bound, once known
 };
 static_assert(sizeof(OnePassCtl) <= kSelectCtlBytes, "control block fits its region");
@@ -1188,9 +1190,10 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
 //      its live lanes' largest keys m, and the number kM of lanes whose
 //      largest key is M.  Each lane's largest key is a distinct candidate,
 //      so the wave guarantees kM candidates at keys <= M and all its nl live
-//      lanes' candidates at keys <= m.  The workgroup then counts itself in
-//      the request's arrival counter;
-//   2. the workgroup that arrives last reads every wave's summary and takes
+//      lanes' candidates at keys <= m.  The summary carries the call's tag;
+//   2. the request's first workgroup reads the wave summaries until all of
+//      them carry the tag (no counter: it sees the last one about one load
+//      round trip after it lands, with every summary already loaded) and takes
 //      as bound B a key at which the guaranteed count reaches W, so that no
 //      member of the top W lies below it: the floor of the bin where the
 //      count from the top reaches W after two 11-bit histogram passes (to
@@ -1212,7 +1215,7 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
 //      a share each); with more,
 //      one workgroup finds their exact top W first (radix cut, ties in index
 //      order, re-reading the slots on every pass).  It also returns the
-//      request's counters to zero.
+//      request's bound word to zero and advances the epoch.
 // The lane-level summaries make the bound tight also when the scores rise
 // with the beam (the top W all in the last rows): wave maxima alone then
 // guarantee only one candidate per wave.
@@ -1236,9 +1239,6 @@ __device__ inline unsigned long long wait_bound(unsigned long long* word,
 // write through to memory and such loads bypass the compute unit's and the
 // XCD's caches, so no cache-wide write-back or invalidation (an agent-scope
 // fence, several microseconds with 256 workgroups issuing them) is needed.
-// A writer waits for its stores to complete (vmcnt(0), the vector memory
-// counter also covers stores on this architecture) before it updates a
-// counter.
 constexpr int kAgentScope = 16;  // cache policy bit sc1
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 __device__ inline void st_agent4(void* base, unsigned off, uint4 v) {
@@ -1248,7 +1248,20 @@ __device__ inline void st_agent4(void* base, unsigned off, uint4 v) {
 __device__ inline uint4 ld_agent4(__amdgpu_buffer_rsrc_t rs, unsigned off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kAgentScope));
 }
-__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+// Tags of the one-pass wave summaries.  A summary (M, m, kM) is stored as one
+// 16-byte word whose last field is tag ^ mix(M, m, kM), tag = epoch + 1 of the
+// call that wrote it; a summary is current when its last field gives back the
+// current call's tag.  Every tag a summary in the region carries is at most
+// the current epoch (each one-pass call writes epoch + 1, and its final kernel
+// then advances the epoch to that value), so only this call's summaries match;
+// the region's zero fill reads as tag 0, which no call uses.  The mix (zero
+// at zero) makes a read that mixed fields of two different stores fail the
+// test as well, without relying on 16-byte stores being seen whole.
+__device__ inline unsigned summary_mix(unsigned M, unsigned m, unsigned km) {
+  return (M * 0x9E3779B1u) ^ __builtin_rotateleft32(m * 0x85EBCA77u, 13) ^ (km * 0xC2B2AE3Du);
+}
+__device__ inline unsigned summary_tag(uint4 e) { return e.w ^ summary_mix(e.x, e.y, e.z); }
 
 // Live lanes of wave w of chunk c (lanes holding at least one candidate).
 __device__ inline unsigned wave_live_lanes(const SelectParams& p, unsigned c, unsigned w) {
@@ -1257,7 +1270,7 @@ __device__ inline unsigned wave_live_lanes(const SelectParams& p, unsigned c, un
   return nc > first ? min(nc - first, 64u) : 0u;
 }
 
-// LDS of the bound (the last arrival only).
+// LDS of the bound (the request's first workgroup only).
 constexpr int kBoundList = 512;  // events of one histogram bin resolved by brute force
 struct BoundShared {
   uint2 ev[kBoundList];          // (key, weight) of the events in the chosen bin
@@ -1266,8 +1279,36 @@ struct BoundShared {
   alignas(16) unsigned gc[kOnePassSegPer * kThreads / kWaves];  // guaranteed count at B per chunk
 };
 
+// Reads request r's wave summaries until every one carries `tag` (thread t:
+// summaries i * kThreads + t, all rows loaded in each round, the ones beyond
+// nseg outside the buffer, reading zeros); false when the waiting time passed
+// first (in any thread).
+__device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned tag,
+                                    uint4 (&e)[kOnePassSegPer]) {
+  const unsigned nseg = p.nseg, t = threadIdx.x;
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
+  unsigned pending = 0u;
+#pragma unroll
+  for (int i = 0; i < kOnePassSegPer; ++i)
+    pending |= unsigned(unsigned(i) * kThreads + t < nseg) << i;
+  const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
+  int late = 0;
+  while (pending != 0u) {
+#pragma unroll
+    for (int i = 0; i < kOnePassSegPer; ++i) e[i] = ld_agent4(rs, (unsigned(i) * kThreads + t) * 16u);
+#pragma unroll
+    for (int i = 0; i < kOnePassSegPer; ++i)
+      if (summary_tag(e[i]) == tag) pending &= ~(1u << i);
+    if (static_cast<unsigned long long>(wall_clock64()) - t0 > p.wait_ticks) {
+      late = 1;
+      break;
+    }
+  }
+  return __syncthreads_or(late) == 0;
+}
+
 // Bound word of request r from every wave's summary (see step 2 above):
-// ((c* + 1) << 32) | B.  All of a thread's summaries are loaded in one round
+// ((c* + 1) << 32) | B.  Thread t holds summaries i * kThreads + t in e[i]
 // (nseg <= kOnePassSegPer * kThreads).
 //
 // Each live summary (M, m, kM) of a wave with nl live lanes is two weighted
@@ -1281,17 +1322,11 @@ struct BoundShared {
 // second histogram pass over the next 11 bits; should that one hold too many
 // as well, B is its smallest event key (its count still reaches W).
 __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
-                                                   BoundShared& bs, unsigned r) {
+                                                   BoundShared& bs,
+                                                   const uint4 (&e)[kOnePassSegPer]) {
   const unsigned nseg = p.nwg * unsigned(kWaves);
   const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
   const unsigned W = p.W;
-  // all rows are issued at once: the ones beyond nseg read nothing (a load
-  // under a branch would be waited for where the branch joins)
-  uint4 e[kOnePassSegPer];  // (M, m, kM, 0)
-  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
-#pragma unroll
-  for (int i = 0; i < kOnePassSegPer; ++i) e[i] = ld_agent4(rs, (unsigned(i) * kThreads + t) * 16u);
-  // while the summaries are in flight: clear the histogram and the list
   reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
   if (t == 0) bs.nev = 0u;
   unsigned nl[kOnePassSegPer], lo = ~0u, hi = 0u;
@@ -1756,33 +1791,35 @@ template <bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p) {
   __shared__ SelShared sh;
   __shared__ BoundShared bs;
-  __shared__ unsigned flag[2];
+  __shared__ unsigned flag[1];
   __shared__ unsigned wmax[kWaves];
   const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
   const unsigned base = c * unsigned(kSelectChunk);
   const unsigned n = min(p.N - base, unsigned(kSelectChunk));
   const unsigned t = threadIdx.x, w = t >> 6;
+  const unsigned tag = p.ctl->epoch + 1u;  // (the final kernel advances the epoch)
   unsigned key[kNI];
   const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
   if (t < (kNI * kWaves + 4) / 4) reinterpret_cast<uint4*>(sh.tab)[t] = make_uint4(0u, 0u, 0u, 0u);
-  // 1. this wave's (M, m), published; the workgroup counts itself in
+  // 1. this wave's (M, m), published with the call's tag
   unsigned lmax = 0u;  // invalid slots hold key 0
 #pragma unroll
   for (int i = 0; i < kNI; ++i) lmax = max(lmax, key[i]);
   const Red3 wr = wave_reduce(0u, (vm & 1u) ? lmax : ~0u, lmax);
   const unsigned km = unsigned(__popcll(__ballot((vm & 1u) && lmax == wr.hi)));
   if (lane_id() == 0) {
-    st_agent4(p.ex, (r * p.nseg + c * kWaves + w) * 16u, make_uint4(wr.hi, wr.lo, km, 0u));
+    st_agent4(p.ex, (r * p.nseg + c * kWaves + w) * 16u,
+              make_uint4(wr.hi, wr.lo, km, tag ^ summary_mix(wr.hi, wr.lo, km)));
     wmax[w] = wr.hi;
   }
-  wait_stores();
-  __syncthreads();
-  if (t == 0) flag[0] = atomicAdd(&p.ctl->arrive[r], 1u) == p.nwg - 1u;
-  __syncthreads();
-  // 2. the bound: computed by the last arrival, waited for by the others
+  // 2. the bound: computed by the request's first workgroup once every
+  // summary is in, waited for by the others
   unsigned bound;  // keys below it are dropped
-  if (flag[0]) {
-    const unsigned long long bw = onepass_bound(p, sh, bs, r);
+  if (c == 0u) {
+    uint4 e[kOnePassSegPer];
+    // (waited too long: B = 0 for every chunk, i.e. no bound)
+    const unsigned long long bw =
+        onepass_poll(p, r, tag, e) ? onepass_bound(p, sh, bs, e) : (~0ull << 32);
     if (t == 0)
       __hip_atomic_store(&p.ctl->bound[r], bw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
@@ -1792,10 +1829,10 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
       const unsigned long long bw = wait_bound(&p.ctl->bound[r], p.wait_ticks);
       const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
       // 0 after a timeout: no bound
-      flag[1] = bw == 0ull ? 0u : ((c > cstar && B < ~0u) ? B + 1u : B);
+      flag[0] = bw == 0ull ? 0u : ((c > cstar && B < ~0u) ? B + 1u : B);
     }
     __syncthreads();
-    bound = flag[1];
+    bound = flag[0];
   }
   // 3. survivors into the chunk's slot (as the filter kernel); the final
   // kernel reads them after this launch has ended
@@ -1824,17 +1861,32 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   }
 }
 
+// Advances the epoch past this call's tag (workgroup 0 of the final kernel).
+// After the largest tag it starts again at 0, and the summary region is
+// cleared first, so that no summary left there carries a later call's tag.
+__device__ inline void advance_epoch(const SelectParams& p) {
+  const unsigned tag = p.ctl->epoch + 1u;
+  __syncthreads();  // every thread has read it before thread 0 rewrites it
+  if (tag == ~0u) {
+    for (unsigned i = threadIdx.x; i < unsigned(kSelectSummaryBytes / 16); i += kThreads)
+      p.ex[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  if (threadIdx.x == 0) p.ctl->epoch = tag == ~0u ? 0u : tag;
+}
+
 // 4. fparts (<= kOnePassFinalParts) workgroups per request, after the pass: each stages
 // all survivors and places its share of them; the first also returns the
-// request's counters to zero for the next call.
+// request's bound word to zero for the next call, and workgroup 0 advances
+// the epoch.  (Without a control block, as after the two-pass filter, it
+// only places.)
 template <bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectParams p) {
   __shared__ OnePassShared u;
   const unsigned r = blockIdx.x / p.fparts;
   const unsigned part = blockIdx.x - r * p.fparts;
-  if (threadIdx.x == 0 && part == 0u && p.ctl != nullptr) {
-    p.ctl->arrive[r] = 0u;
-    p.ctl->bound[r] = 0ull;
+  if (p.ctl != nullptr) {
+    if (threadIdx.x == 0 && part == 0u) p.ctl->bound[r] = 0ull;
+    if (blockIdx.x == 0u) advance_epoch(p);
   }
   onepass_final<BEAM>(p, u, r, part, p.fparts);
 }
@@ -1902,9 +1954,10 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
   const bool has_beam = beam != nullptr;
   if (plan.two_pass && R <= kSelectOnePassMaxRequests && width <= kOnePassRankMax &&
       plan.nseg <= unsigned(kOnePassSegPer * kThreads) &&
+      size_t(R) * plan.nseg * 16u <= kSelectSummaryBytes &&
       unsigned(R) * plan.nchunks <= onepass_capacity()) {
     p.ctl = reinterpret_cast<OnePassCtl*>(ws);
-    p.ex = reinterpret_cast<uint4*>(ws + plan.seg_off);
+    p.ex = reinterpret_cast<uint4*>(ws + kSelectCtlBytes);
     p.nseg = plan.nseg;
     p.nwg = plan.nchunks;
     p.cand_out = reinterpret_cast<uint2*>(ws + plan.slot_off);

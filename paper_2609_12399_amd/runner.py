@@ -186,8 +186,9 @@ class BeamSelector:
         torch = _torch()
         self.R, self.prev_width, self.vocab, self.width = R, prev_width, vocab, width
         self.ws_bytes = ab.onela_select_workspace_bytes(R, prev_width, vocab, width)
-        # zero-filled once: the selection keeps its cross-workgroup counters
-        # here and returns them to zero after every call
+        # zero-filled once: the selection keeps its cross-workgroup state
+        # here (a call counter, bound words, tagged summaries) and leaves it
+        # ready for the next call
         self.workspace = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
         self.parents = torch.empty((R, width), dtype=torch.int32, device=device)
         self.tokens = torch.empty((R, width), dtype=torch.int32, device=device)

@@ -153,25 +153,27 @@ def test_binding_rejects_host_tensors():
 
 
 def _select_plan_bytes(R, P, V, W, chunk=16384):
-    """Workspace model of the beam selection: a 1 KiB control block (the
-    one-pass path's per-request counters), then either the two-pass regions
-    or a reduction tree whose workgroups each take `chunk` candidates and
-    write one slot of `cap` (key, index) pairs (8 bytes each) plus a 4-byte
-    count; stage outputs alternate between two buffers, every region
-    256-byte aligned."""
+    """Workspace model of the beam selection: a 1 KiB control block and a
+    128 KiB summary region (the one-pass path's state across calls: a call
+    counter, per-request bound words, 8192 16-byte wave summaries), then
+    either the two-pass regions or a reduction tree whose workgroups each
+    take `chunk` candidates and write one slot of `cap` (key, index) pairs
+    (8 bytes each) plus a 4-byte count; stage outputs alternate between two
+    buffers, every region 256-byte aligned."""
     p2 = lambda x: 1 << (x - 1).bit_length()
     cap = max(64, p2(2 * W))
     if cap > chunk // 4:
         cap = max(chunk // 4, p2(W))
     group = chunk // cap
     up = lambda x: -(-x // 256) * 256
+    head = 1024 + 8192 * 16
     n = P * V
     nchunks = -(-n // chunk)
     if n > chunk and n >= 2 * W * 2048 and nchunks <= 2048:
-        # two-pass / one-pass path: one 16-byte summary per wave of 2048
+        # two-pass / one-pass path: one 4-byte maximum per wave of 2048
         # candidates, one slot of `cap` pairs per chunk, one (count, largest
         # key) pair per chunk
-        return 1024 + up(R * nchunks * 8 * 16) + up(R * nchunks * cap * 8) + up(R * nchunks * 8)
+        return head + up(R * nchunks * 8 * 4) + up(R * nchunks * cap * 8) + up(R * nchunks * 8)
     pairs, counts = [0, 0], [0, 0]
     if n > chunk:
         slots = -(-n // chunk)
@@ -182,8 +184,7 @@ def _select_plan_bytes(R, P, V, W, chunk=16384):
             pairs[s % 2] = max(pairs[s % 2], R * slots * cap * 8)
             counts[s % 2] = max(counts[s % 2], R * slots * 4)
             s += 1
-    up = lambda x: -(-x // 256) * 256
-    return 1024 + sum(up(x) for x in pairs + counts)
+    return head + sum(up(x) for x in pairs + counts)
 
 
 @pytest.mark.parametrize("R,P,V,W", [(1, 3, 5, 7), (2, 8, 2048, 4096), (1, 512, 8192, 512),

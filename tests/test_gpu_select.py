@@ -160,6 +160,68 @@ def test_select_shared_workspace_across_shapes():
         _check(logp, beam, W, par.cpu().numpy(), tok.cpu().numpy(), sc.cpu().numpy())
 
 
+def _mix(M, m, km):
+    """The summary check word's mix (stated beside the one-pass summaries'
+    tags): products with odd constants, the second rotated left by 13."""
+    a = (M * 0x9E3779B1) & 0xFFFFFFFF
+    b = (m * 0x85EBCA77) & 0xFFFFFFFF
+    b = ((b << 13) | (b >> 19)) & 0xFFFFFFFF
+    return a ^ b ^ ((km * 0xC2B2AE3D) & 0xFFFFFFFF)
+
+
+def test_select_one_pass_tags_and_epoch_wrap():
+    """The one-pass path's cross-call state in the workspace: a call counter
+    (epoch, first word) and, from byte 1024, 8192 16-byte wave summaries
+    (M, m, kM, tag ^ mix).  Planted summaries of an earlier call (older tag)
+    with fields that would put the bound above every score, and summaries
+    whose check word names this call's tag but whose fields it does not
+    match, are not taken; the call matches the oracle and advances the
+    epoch.  At the largest tag the epoch starts again at 0 and the region is
+    cleared, and the call after it matches too.  Each call's survivor
+    counts show that a bound was used (without one every chunk keeps W)."""
+    import torch
+    from paper_2609_12399_amd.runner import BeamSelector
+    R, P, V, W = 1, 512, SELECT_CODEBOOK, 512
+    sel = BeamSelector(R, P, V, W)
+    ws = sel.workspace
+    nchunks = P * V // 16384
+    nseg, cap, nsum = nchunks * 8, 2 * W, 8192
+    up = lambda x: -(-x // 256) * 256
+    cnt_off = 1024 + nsum * 16 + up(R * nseg * 4) + up(R * nchunks * cap * 8)
+
+    def put_u32(off, vals):
+        b = torch.from_numpy(np.asarray(vals, dtype=np.uint32).reshape(-1).view(np.uint8).copy())
+        ws[off:off + b.numel()].copy_(b)
+
+    def epoch():
+        return int(ws[0:4].cpu().numpy().view(np.uint32)[0])
+
+    def call(seed):
+        logp, beam = make_select_inputs(R, P, V, seed, "logsoftmax", True)
+        print(f"tagged call seed={seed} epoch={epoch()}", flush=True)
+        sel(torch.from_numpy(logp).cuda(), torch.from_numpy(beam).cuda())
+        torch.cuda.synchronize()
+        _check(logp, beam, W, sel.parents.cpu().numpy(), sel.tokens.cpu().numpy(),
+               sel.scores.cpu().numpy())
+        cnt = ws[cnt_off:cnt_off + nchunks * 8].cpu().numpy().view(np.uint32)[0::2]
+        assert 0 < int(cnt.sum()) < 4096, int(cnt.sum())
+
+    E, top = 5, 0xFFFFFFFF
+    put_u32(0, [E])
+    planted = np.zeros((nsum, 4), dtype=np.uint32)
+    planted[:nseg] = [top, top, 64, E ^ _mix(top, top, 64)]              # an older call's
+    planted[1:nseg:2, 3] = (E + 1) ^ _mix(0x1234, top, 64)               # fields not its own
+    put_u32(1024, planted)
+    call(90)
+    assert epoch() == E + 1
+    put_u32(0, [0xFFFFFFFE])
+    call(91)
+    assert epoch() == 0
+    assert int(torch.count_nonzero(ws[1024:1024 + nsum * 16])) == 0
+    call(92)
+    assert epoch() == 1
+
+
 def test_select_graph_replays_with_new_scores():
     """The headline selection captured once in a HIP graph and replayed with
     new scores copied into its input buffers between replays (eager work
