@@ -1201,9 +1201,10 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
 //      the chunks' guaranteed counts at B, summed in index order, reach W:
 //      a candidate of a later chunk whose key equals B has W better ones
 //      (equal or higher keys at lower indices), so it cannot be kept (this
-//      keeps tied scores from surviving in every chunk).  The others wait
-//      for the bound word for a bounded time; one that gives up keeps its
-//      chunk's exact top W instead (slower, never wrong);
+//      keeps tied scores from surviving in every chunk).  B is published
+//      before c*, for which only chunks holding a key equal to B wait.  The
+//      others wait for the bound word for a bounded time; one that gives up
+//      keeps its chunk's exact top W instead (slower, never wrong);
 //   3. every workgroup keeps its candidates above B, or equal to B in a
 //      chunk up to c*, in its chunk's slot, in index order (the chunk's
 //      exact top W when they overflow it), with the count and the chunk's
@@ -1220,14 +1221,23 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(SelectParams p) {
 // with the beam (the top W all in the last rows): wave maxima alone then
 // guarantee only one candidate per wave.
 
-// Waits (thread 0) for the bound word of a request; 0 after `ticks`.
+// The bound word of a request: (h << 32) | B.  h = 0: nothing yet; h =
+// kCstarPending: B is known and c* is not; otherwise h = c* + 1.  A call
+// that gave up on the summaries publishes B = 0 with h = kNoBound (no chunk
+// above c*, so nothing is dropped).
+constexpr unsigned kCstarPending = ~0u;
+constexpr unsigned kNoBound = ~0u - 1u;
+
+// Waits (thread 0) for the bound word of a request, for B alone or (final)
+// also for c*; 0 after `ticks`.
 __device__ inline unsigned long long wait_bound(unsigned long long* word,
-                                                unsigned long long ticks) {
+                                                unsigned long long ticks, bool final) {
   const unsigned long long t0 = static_cast<unsigned long long>(wall_clock64());
   for (;;) {
     const unsigned long long v = __hip_atomic_load(word, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_AGENT);
-    if (v >> 32) return v;
+    const unsigned h = unsigned(v >> 32);
+    if (h != 0u && !(final && h == kCstarPending)) return v;
     if (static_cast<unsigned long long>(wall_clock64()) - t0 > ticks) return 0ull;
     __builtin_amdgcn_s_sleep(2);
   }
@@ -1308,7 +1318,8 @@ __device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned 
 }
 
 // Bound word of request r from every wave's summary (see step 2 above):
-// ((c* + 1) << 32) | B.  Thread t holds summaries i * kThreads + t in e[i]
+// ((c* + 1) << 32) | B, also published to `word` (thread 0): first with B
+// alone, then with c*.  Thread t holds summaries i * kThreads + t in e[i]
 // (nseg <= kOnePassSegPer * kThreads).
 //
 // Each live summary (M, m, kM) of a wave with nl live lanes is two weighted
@@ -1323,7 +1334,8 @@ __device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned 
 // as well, B is its smallest event key (its count still reaches W).
 __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
                                                    BoundShared& bs,
-                                                   const uint4 (&e)[kOnePassSegPer]) {
+                                                   const uint4 (&e)[kOnePassSegPer],
+                                                   unsigned long long* word) {
   const unsigned nseg = p.nwg * unsigned(kWaves);
   const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
   const unsigned W = p.W;
@@ -1440,6 +1452,10 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       for (int w2 = 0; w2 < kWaves; ++w2) B = min(B, bs.red[0][w2]);
     }
   }
+  // B alone first: only chunks holding a key equal to B wait for c*
+  if (t == 0)
+    __hip_atomic_store(word, (static_cast<unsigned long long>(kCstarPending) << 32) | B,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // c*: the chunks' guaranteed counts at B, summed in chunk order.  Thread t
   // holds summary i * kThreads + t, i.e. wave t % 8 of chunk i * 64 + t / 8:
   // a chunk's count is a sum over 8 adjacent lanes, stored by the first of
@@ -1468,7 +1484,9 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
     }
   }
   __syncthreads();
-  return (static_cast<unsigned long long>(sh.digit + 1u) << 32) | B;
+  const unsigned long long bw = (static_cast<unsigned long long>(sh.digit + 1u) << 32) | B;
+  if (t == 0) __hip_atomic_store(word, bw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return bw;
 }
 
 // LDS of the one-pass kernel.
@@ -1791,7 +1809,7 @@ template <bool BEAM>
 __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p) {
   __shared__ SelShared sh;
   __shared__ BoundShared bs;
-  __shared__ unsigned flag[1];
+  __shared__ unsigned long long bw_sh[1];
   __shared__ unsigned wmax[kWaves];
   const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
   const unsigned base = c * unsigned(kSelectChunk);
@@ -1815,24 +1833,36 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   // 2. the bound: computed by the request's first workgroup once every
   // summary is in, waited for by the others
   unsigned bound;  // keys below it are dropped
-  if (c == 0u) {
+  unsigned long long* const word = &p.ctl->bound[r];
+  if (c == 0u) {  // (chunk 0 is never above c*: its bound is B)
     uint4 e[kOnePassSegPer];
-    // (waited too long: B = 0 for every chunk, i.e. no bound)
-    const unsigned long long bw =
-        onepass_poll(p, r, tag, e) ? onepass_bound(p, sh, bs, e) : (~0ull << 32);
-    if (t == 0)
-      __hip_atomic_store(&p.ctl->bound[r], bw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (onepass_poll(p, r, tag, e)) {
+      bound = unsigned(onepass_bound(p, sh, bs, e, word));
+    } else {  // waited too long: no bound
+      if (t == 0)
+        __hip_atomic_store(word, static_cast<unsigned long long>(kNoBound) << 32, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      bound = 0u;
+    }
+  } else {
+    if (t == 0) bw_sh[0] = wait_bound(word, p.wait_ticks, false);
+    __syncthreads();
+    unsigned long long bw = bw_sh[0];  // 0 after a timeout: no bound
+    if (unsigned(bw >> 32) == kCstarPending) {
+      // c* decides only for keys equal to B: a chunk holding none keeps the
+      // keys >= B whichever side of c* it is on
+      const unsigned B = unsigned(bw);
+      int eq = 0;
+#pragma unroll
+      for (int i = 0; i < kNI; ++i) eq |= int(((vm >> i) & 1u) && key[i] == B);
+      if (__syncthreads_or(eq)) {
+        if (t == 0) bw_sh[0] = wait_bound(word, p.wait_ticks, true);
+        __syncthreads();
+        bw = bw_sh[0];
+      }
+    }
     const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
     bound = (c > cstar && B < ~0u) ? B + 1u : B;
-  } else {
-    if (t == 0) {
-      const unsigned long long bw = wait_bound(&p.ctl->bound[r], p.wait_ticks);
-      const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
-      // 0 after a timeout: no bound
-      flag[0] = bw == 0ull ? 0u : ((c > cstar && B < ~0u) ? B + 1u : B);
-    }
-    __syncthreads();
-    bound = flag[0];
   }
   // 3. survivors into the chunk's slot (as the filter kernel); the final
   // kernel reads them after this launch has ended
