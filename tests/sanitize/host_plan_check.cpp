@@ -79,10 +79,13 @@ static void select_plans() {
             continue;
           }
           EXPECT(rc == ONELA_OK);
-          EXPECT(plan.total % 256 == 0 && plan.total >= kSelectCtlBytes);
+          // the control block and the one-pass summary region come first in
+          // every plan, and nothing else is placed there
+          const size_t head = kSelectCtlBytes + kSelectSummaryBytes;
+          EXPECT(plan.total % 256 == 0 && plan.total >= head);
           EXPECT(plan.cap >= unsigned(W) && (plan.cap & (plan.cap - 1)) == 0);
           if (plan.two_pass) {
-            EXPECT(plan.seg_off == kSelectCtlBytes);
+            EXPECT(plan.seg_off == head);
             EXPECT(plan.seg_off < plan.slot_off && plan.slot_off < plan.cnt_off &&
                    plan.cnt_off < plan.total);
             EXPECT(plan.nseg == plan.nchunks * 8u);
@@ -90,7 +93,7 @@ static void select_plans() {
           } else {
             EXPECT(plan.stages >= 0 && plan.stages <= kSelectMaxStages);
             for (int b = 0; b < 2; ++b)
-              EXPECT(plan.pair_off[b] >= kSelectCtlBytes && plan.count_off[b] <= plan.total);
+              EXPECT(plan.pair_off[b] >= head && plan.count_off[b] <= plan.total);
           }
         }
 }
