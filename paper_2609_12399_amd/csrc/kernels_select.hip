@@ -299,6 +299,15 @@ __device__ inline unsigned ordered_plan_sparse(unsigned f, SelShared& sh) {
   return sh.tab[kNI * kWaves];
 }
 
+// ordered_plan_sparse again, for a new mask, after an earlier plan (or any
+// other use of sh.tab) in the same workgroup: the counts are zeroed first.
+__device__ inline unsigned replan_sparse(unsigned f, SelShared& sh) {
+  if (threadIdx.x < (kNI * kWaves + 4) / 4)
+    reinterpret_cast<uint4*>(sh.tab)[threadIdx.x] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  return ordered_plan_sparse(f, sh);
+}
+
 template <typename F>
 __device__ inline void ordered_apply_sparse(unsigned f, SelShared& sh, F&& fn) {
   const unsigned w = threadIdx.x >> 6;
@@ -879,9 +888,8 @@ __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p)
   if (total > p.cap) {  // rare: keep the chunk's exact top W of the survivors
     __syncthreads();
     keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
-    const Ordered o = ordered_plan(keep, sh);
-    ordered_apply(keep, o, sh, put);
-    total = o.total;
+    total = replan_sparse(keep, sh);
+    ordered_apply_sparse(keep, sh, put);
   } else {
     ordered_apply_sparse(keep, sh, put);
   }
@@ -1877,9 +1885,8 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   if (total > p.cap) {  // a chunk's exact top W of its survivors
     __syncthreads();
     keep = cut_mask(sh, key, keep, find_cut(sh, key, keep, p.W));
-    const Ordered o = ordered_plan(keep, sh);
-    ordered_apply(keep, o, sh, put);
-    total = o.total;
+    total = replan_sparse(keep, sh);
+    ordered_apply_sparse(keep, sh, put);
   } else {
     ordered_apply_sparse(keep, sh, put);
   }
