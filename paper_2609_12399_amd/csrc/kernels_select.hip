@@ -14,8 +14,8 @@
 // one-pass path (each chunk held in registers from its single read while a
 // bound forms across workgroups, then a placing launch; described at its
 // kernels below); other large calls the two-pass path (wave maxima, then one
-// filter pass, then ranking workgroups per request); smaller ones a reduction
-// tree.  A 512-thread workgroup holds 16384 candidates (32 per lane):
+// filter pass, then the one-pass path's placing launch, or ranking
+// workgroups per request beyond 512 chunks); smaller ones a reduction tree.  A 512-thread workgroup holds 16384 candidates (32 per lane):
 //   * stage kernel: keeps a superset of its candidates' top min(W, n) and
 //     writes it, in index order, to an output slot of `cap` (key, index)
 //     pairs plus a count.  A 2048-bin histogram of the maxima of groups of
