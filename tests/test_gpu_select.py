@@ -45,6 +45,10 @@ CASES = [
     ("one_pass_ties_w64", 1, 300, SELECT_CODEBOOK, 64, "ties", True),
     ("one_pass_r2_special", 2, 100, SELECT_CODEBOOK, 200, "special", True),
     ("one_pass_rising_w1024", 1, 1024, 4096, 1024, "rising", True),
+    # many requests in one launch: a polling workgroup and a bound word per
+    # request, one epoch (64 requests: every word of the control block)
+    ("one_pass_r32_ties", 32, 8, SELECT_CODEBOOK, 16, "ties", True),
+    ("one_pass_r64", 64, 4, SELECT_CODEBOOK, 8, "logsoftmax", True),
     # two-pass path ranked by the placing kernel of the one-pass path: more
     # chunks than fit at once, with heavy ties (more survivors than it
     # stages), and more requests than the one-pass control block has
