@@ -1294,15 +1294,16 @@ struct BoundShared {
   uint2 ev[kBoundList];          // (key, weight) of the events in the chosen bin
   unsigned nev;
   unsigned red[2][kWaves];
+  unsigned late[kWaves];         // threads of each wave whose poll gave up
   alignas(16) unsigned gc[kOnePassSegPer * kThreads / kWaves];  // guaranteed count at B per chunk
 };
 
-// Reads request r's wave summaries until every one carries `tag` (thread t:
-// summaries i * kThreads + t, all rows loaded in each round, the ones beyond
-// nseg outside the buffer, reading zeros); false when the waiting time passed
-// first (in any thread).
-__device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned tag,
-                                    uint4 (&e)[kOnePassSegPer]) {
+// Reads request r's wave summaries until every one of this thread's carries
+// `tag` (thread t: summaries i * kThreads + t, all rows loaded in each round,
+// the ones beyond nseg outside the buffer, reading zeros); 1 when the waiting
+// time passed first.  No barrier: onepass_bound's first one joins the threads.
+__device__ inline int onepass_poll(const SelectParams& p, unsigned r, unsigned tag,
+                                   uint4 (&e)[kOnePassSegPer]) {
   const unsigned nseg = p.nseg, t = threadIdx.x;
   const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(p.ex + size_t(r) * nseg, int(nseg * 16u));
   unsigned pending = 0u;
@@ -1322,13 +1323,14 @@ __device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned 
       break;
     }
   }
-  return __syncthreads_or(late) == 0;
+  return late;
 }
 
 // Bound word of request r from every wave's summary (see step 2 above):
 // ((c* + 1) << 32) | B, also published to `word` (thread 0): first with B
 // alone, then with c*.  Thread t holds summaries i * kThreads + t in e[i]
-// (nseg <= kOnePassSegPer * kThreads).
+// (nseg <= kOnePassSegPer * kThreads) from onepass_poll, which gave up when
+// `late` is set in any thread: then the word says no bound (B = 0).
 //
 // Each live summary (M, m, kM) of a wave with nl live lanes is two weighted
 // events: (M, kM) and (m, nl - kM).  The guaranteed count at a key x is the
@@ -1342,7 +1344,7 @@ __device__ inline bool onepass_poll(const SelectParams& p, unsigned r, unsigned 
 // as well, B is its smallest event key (its count still reaches W).
 __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
                                                    BoundShared& bs,
-                                                   const uint4 (&e)[kOnePassSegPer],
+                                                   const uint4 (&e)[kOnePassSegPer], int late,
                                                    unsigned long long* word) {
   const unsigned nseg = p.nwg * unsigned(kWaves);
   const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
@@ -1362,20 +1364,28 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       }
     }
   }
-  {
-    const Red3 wr = wave_reduce(0u, lo, hi);
+  {  // (with the poll's wait flags: one barrier for both)
+    const Red3 wr = wave_reduce(unsigned(late), lo, hi);
     if (lane == 0) {
       bs.red[0][w] = wr.lo;
       bs.red[1][w] = wr.hi;
+      bs.late[w] = wr.sum;
     }
   }
   __syncthreads();
   lo = ~0u;
   hi = 0u;
+  unsigned nlate = 0u;
 #pragma unroll
   for (int w2 = 0; w2 < kWaves; ++w2) {
     lo = min(lo, bs.red[0][w2]);
     hi = max(hi, bs.red[1][w2]);
+    nlate += bs.late[w2];
+  }
+  if (nlate != 0u) {
+    const unsigned long long none = static_cast<unsigned long long>(kNoBound) << 32;
+    if (t == 0) __hip_atomic_store(word, none, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return none;
   }
   unsigned B = lo;
   if (lo < hi) {
@@ -1844,14 +1854,8 @@ __global__ __launch_bounds__(kThreads) void select_onepass_kernel(SelectParams p
   unsigned long long* const word = &p.ctl->bound[r];
   if (c == 0u) {  // (chunk 0 is never above c*: its bound is B)
     uint4 e[kOnePassSegPer];
-    if (onepass_poll(p, r, tag, e)) {
-      bound = unsigned(onepass_bound(p, sh, bs, e, word));
-    } else {  // waited too long: no bound
-      if (t == 0)
-        __hip_atomic_store(word, static_cast<unsigned long long>(kNoBound) << 32, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      bound = 0u;
-    }
+    const int late = onepass_poll(p, r, tag, e);
+    bound = unsigned(onepass_bound(p, sh, bs, e, late, word));
   } else {
     if (t == 0) bw_sh[0] = wait_bound(word, p.wait_ticks, false);
     __syncthreads();
