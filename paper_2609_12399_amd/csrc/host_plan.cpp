@@ -107,8 +107,9 @@ bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan) {
     plan->two_pass = true;
     plan->nchunks = nchunks;
     plan->nseg = nchunks * (kSelectThreads / 64);
-    plan->seg_off = ctl;  // [R][nseg] wave maxima (two-pass)
-    plan->slot_off = ctl + up(size_t(R) * plan->nseg * 4);
+    plan->seg_off = ctl;  // [R][nseg] wave summaries (M, m, kM, 0), or uint32 maxima
+    plan->bound_off = ctl + up(size_t(R) * plan->nseg * 16);  // [R] bound words
+    plan->slot_off = plan->bound_off + up(size_t(R) * 8);
     plan->cnt_off = plan->slot_off + up(size_t(R) * nchunks * cap * 8 /* (key, index) */);
     plan->total = plan->cnt_off + up(size_t(R) * nchunks * 8 /* (count, largest key) */);
     return true;

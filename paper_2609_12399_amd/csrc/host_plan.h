@@ -76,11 +76,12 @@ struct SelectPlan {
   unsigned cap, group;
   size_t pair_off[2], count_off[2], total;
   // Two-pass and one-pass paths (see kernels_select.hip): per request nseg
-  // wave maxima (two-pass; the one-pass summaries have their own region),
-  // then nchunks slots of `cap` pairs and their counts.
+  // wave summaries or maxima (two-pass; the one-pass summaries have their own
+  // region), one bound word, then nchunks slots of `cap` pairs and their
+  // counts.
   bool two_pass;
   unsigned nchunks, nseg;
-  size_t seg_off, slot_off, cnt_off;
+  size_t seg_off, bound_off, slot_off, cnt_off;
 };
 bool select_plan(int R, unsigned N, unsigned W, SelectPlan* plan);
 // Size of the per-device scratch array of the allocation-free selection

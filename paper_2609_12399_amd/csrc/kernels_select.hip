@@ -84,6 +84,8 @@ struct SelectParams {
   uint4* ex;                // [R][nseg] per wave: (M, m, kM, check), see the one-pass path
   unsigned long long wait_ticks;  // how long a workgroup waits for the bound (wall clock)
   unsigned fparts;          // workgroups per request of the final kernel
+  // two-pass path with a bound word per request (see select_summary_kernel)
+  unsigned long long* tp_bound;  // [R] (c* + 1) << 32 | B, or null: the filter forms the bound
 };
 
 // Cross-workgroup state of the one-pass path, at the start of the workspace
@@ -94,6 +96,9 @@ struct OnePassCtl {
   unsigned epoch;     // this call's tag is epoch + 1
   unsigned pad_[3];
   unsigned long long bound[kSelectOnePassMaxRequests];  // (1 << 32) | bound, once known
+  // two-pass summary pass: workgroups of each request that have published
+  // their summaries (zero between calls: the last one returns it to zero)
+  unsigned arrive[kSelectOnePassMaxRequests];
 };
 static_assert(sizeof(OnePassCtl) <= kSelectCtlBytes, "control block fits its region");
 
@@ -844,7 +849,7 @@ __global__ __launch_bounds__(kThreads) void select_segmax_kernel(SelectParams p)
   if (lane_id() == 0) p.segmax[size_t(r) * p.nseg + c * kWaves + (threadIdx.x >> 6)] = w.hi;
 }
 
-template <bool BEAM>
+template <bool BEAM, bool WORD>
 __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p) {
   __shared__ SelShared sh;
   const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
@@ -852,28 +857,37 @@ __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p)
   const unsigned n = min(p.N - base, unsigned(kSelectChunk));
   unsigned key[kNI];
   const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
-  // wave maxima of the request; segment (chunk s / 8, wave s % 8) exists when
-  // its first candidate does
-  // (only the rows i * kThreads < nseg are read: a workgroup-uniform bound,
-  // so no load is issued for the empty tail of the lanes' slots)
-  unsigned mk[kNI], mvm = 0u;
-  const unsigned* seg = p.segmax + size_t(r) * p.nseg;
+  unsigned bound;
+  if constexpr (WORD) {
+    // the request's bound word, formed in the summary pass as the one-pass
+    // path forms it: keys below B are dropped, and keys equal to B beyond c*
+    const unsigned long long bw = p.tp_bound[r];
+    const unsigned B = unsigned(bw), cstar = unsigned(bw >> 32) - 1u;
+    bound = (c > cstar && B < ~0u) ? B + 1u : B;
+  } else {
+    // wave maxima of the request; segment (chunk s / 8, wave s % 8) exists
+    // when its first candidate does
+    // (only the rows i * kThreads < nseg are read: a workgroup-uniform
+    // bound, so no load is issued for the empty tail of the lanes' slots)
+    unsigned mk[kNI], mvm = 0u;
+    const unsigned* seg = p.segmax + size_t(r) * p.nseg;
 #pragma unroll
-  for (int i = 0; i < kNI; ++i) {
-    mk[i] = 0u;
-    if (unsigned(i) * kThreads < p.nseg) {
-      const unsigned s = unsigned(i) * kThreads + threadIdx.x;
-      const bool valid =
-          s < p.nseg && (s / kWaves) * unsigned(kSelectChunk) + (s % kWaves) * 64u < p.N;
-      mk[i] = seg[valid ? s : 0u];
-      mvm |= unsigned(valid) << i;
+    for (int i = 0; i < kNI; ++i) {
+      mk[i] = 0u;
+      if (unsigned(i) * kThreads < p.nseg) {
+        const unsigned s = unsigned(i) * kThreads + threadIdx.x;
+        const bool valid =
+            s < p.nseg && (s / kWaves) * unsigned(kSelectChunk) + (s % kWaves) * 64u < p.N;
+        mk[i] = seg[valid ? s : 0u];
+        mvm |= unsigned(valid) << i;
+      }
     }
-  }
 #pragma unroll
-  for (int i = 0; i < kNI; ++i) mk[i] = ((mvm >> i) & 1u) ? mk[i] : 0u;
-  // at least W maxima reach the bound (floor of the histogram bin where
-  // their count from the top reaches W)
-  const unsigned bound = group_bound(sh, mk, mvm, p.W, 1u);
+    for (int i = 0; i < kNI; ++i) mk[i] = ((mvm >> i) & 1u) ? mk[i] : 0u;
+    // at least W maxima reach the bound (floor of the histogram bin where
+    // their count from the top reaches W)
+    bound = group_bound(sh, mk, mvm, p.W, 1u);
+  }
   unsigned keep = vm;
 #pragma unroll
   for (int i = 0; i < kNI; ++i) keep &= ~(unsigned(key[i] < bound) << i);
@@ -895,7 +909,9 @@ __global__ __launch_bounds__(kThreads) void select_filter_kernel(SelectParams p)
   }
   if (threadIdx.x == 0) {  // (count, largest key of the chunk: its waves' maxima)
     unsigned top = 0u;
-    for (int w = 0; w < kWaves; ++w) top = max(top, seg[c * kWaves + unsigned(w)]);
+    const size_t s0 = size_t(r) * p.nseg + c * kWaves;
+    for (int w = 0; w < kWaves; ++w)
+      top = max(top, WORD ? p.ex[s0 + unsigned(w)].x : p.segmax[s0 + unsigned(w)]);
     reinterpret_cast<uint2*>(p.cnt_out)[size_t(r) * p.nwg + c] = make_uint2(total, top);
   }
 }
@@ -1266,6 +1282,10 @@ __device__ inline void st_agent4(void* base, unsigned off, uint4 v) {
 __device__ inline uint4 ld_agent4(__amdgpu_buffer_rsrc_t rs, unsigned off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kAgentScope));
 }
+// Waits for this wave's stores to complete (the vector memory counter also
+// covers stores on this architecture), before a counter tells others that
+// they are there.
+__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 // Tags of the one-pass wave summaries.  A summary (M, m, kM) is stored as one
 // 16-byte word whose last field is tag ^ mix(M, m, kM), tag = epoch + 1 of the
@@ -1342,18 +1362,18 @@ __device__ inline int onepass_poll(const SelectParams& p, unsigned r, unsigned t
 // each other directly.  A bin with more than kBoundList events is split by a
 // second histogram pass over the next 11 bits; should that one hold too many
 // as well, B is its smallest event key (its count still reaches W).
+template <int ROWS = kOnePassSegPer>
 __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelShared& sh,
-                                                   BoundShared& bs,
-                                                   const uint4 (&e)[kOnePassSegPer], int late,
-                                                   unsigned long long* word) {
+                                                   BoundShared& bs, const uint4 (&e)[ROWS],
+                                                   int late, unsigned long long* word) {
   const unsigned nseg = p.nwg * unsigned(kWaves);
   const unsigned t = threadIdx.x, lane = lane_id(), w = t >> 6;
   const unsigned W = p.W;
   reinterpret_cast<uint4*>(sh.hist)[t] = make_uint4(0u, 0u, 0u, 0u);
   if (t == 0) bs.nev = 0u;
-  unsigned nl[kOnePassSegPer], lo = ~0u, hi = 0u;
+  unsigned nl[ROWS], lo = ~0u, hi = 0u;
 #pragma unroll
-  for (int i = 0; i < kOnePassSegPer; ++i) {
+  for (int i = 0; i < ROWS; ++i) {
     nl[i] = 0u;
     if (unsigned(i) * kThreads < nseg) {
       const unsigned s = unsigned(i) * kThreads + t;
@@ -1403,7 +1423,7 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       }
       // weights by bin, among the events inside the bin chosen so far
 #pragma unroll
-      for (int i = 0; i < kOnePassSegPer; ++i)
+      for (int i = 0; i < ROWS; ++i)
         if (nl[i] > 0u) {
           const unsigned rm = e[i].x - lo, rl = e[i].y - lo;
           if (shr(rm, shift + bits) == prefix) atomicAdd(&sh.hist[(rm >> shift) & mask], e[i].z);
@@ -1416,7 +1436,7 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       need = sh.need;
       // the events of the chosen bin
 #pragma unroll
-      for (int i = 0; i < kOnePassSegPer; ++i)
+      for (int i = 0; i < ROWS; ++i)
         if (nl[i] > 0u) {
           const unsigned rm = e[i].x - lo, rl = e[i].y - lo;
           if (shr(rm, shift) == prefix) {
@@ -1457,7 +1477,7 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
       const unsigned floor = lo + (prefix << shift);
       unsigned nb = ~0u;
 #pragma unroll
-      for (int i = 0; i < kOnePassSegPer; ++i)
+      for (int i = 0; i < ROWS; ++i)
         if (nl[i] > 0u) {
           if (e[i].x >= floor) nb = min(nb, e[i].x);
           if (nl[i] > e[i].z && e[i].y >= floor) nb = min(nb, e[i].y);
@@ -1480,13 +1500,16 @@ __device__ inline unsigned long long onepass_bound(const SelectParams& p, SelSha
   // them (rows beyond nseg have no live lanes and store zeros); one wave
   // then scans the chunks in order.
 #pragma unroll
-  for (int i = 0; i < kOnePassSegPer; ++i) {
+  for (int i = 0; i < ROWS; ++i) {
     unsigned g = nl[i] > 0u ? (e[i].y >= B ? nl[i] : (e[i].x >= B ? e[i].z : 0u)) : 0u;
     g += dppu<0xB1>(g);   // quad_perm [1,0,3,2]
     g += dppu<0x4E>(g);   // quad_perm [2,3,0,1]
     g += dppu<0x141>(g);  // row_half_mirror: the other quad of the 8 lanes
     if ((lane & 7u) == 0u) bs.gc[unsigned(i) * 64u + t / 8u] = g;
   }
+#pragma unroll
+  for (int i = ROWS; i < kOnePassSegPer; ++i)  // chunks beyond the rows held: none
+    if ((lane & 7u) == 0u) bs.gc[unsigned(i) * 64u + t / 8u] = 0u;
   if (t == 0) sh.digit = ~0u;  // (c* always exists: the counts at B reach W)
   __syncthreads();
   if (w == 0) {  // lane l: chunks 8 l .. 8 l + 7
@@ -1933,6 +1956,45 @@ __global__ __launch_bounds__(kThreads) void select_onepass_final_kernel(SelectPa
 }
 
 
+// Two-pass path, first pass with a bound (R <= kSelectOnePassMaxRequests and
+// nseg <= kOnePassSegPer * kThreads): every wave publishes its one-pass
+// summary (M, m, kM); the last workgroup of a request to finish (an arrival
+// counter: no workgroup waits for another, so they need not all be resident
+// at once) reads the request's summaries and writes its bound word, formed as
+// in the one-pass path, for the filter pass.  The filter then compares with
+// one word instead of forming a bound from every wave maximum in each of its
+// workgroups.
+template <bool BEAM, int ROWS>
+__global__ __launch_bounds__(kThreads) void select_summary_kernel(SelectParams p) {
+  __shared__ SelShared sh;
+  __shared__ BoundShared bs;
+  __shared__ unsigned last[1];
+  const unsigned r = blockIdx.x / p.nwg, c = blockIdx.x - r * p.nwg;
+  const unsigned base = c * unsigned(kSelectChunk);
+  const unsigned n = min(p.N - base, unsigned(kSelectChunk));
+  const unsigned t = threadIdx.x, w = t >> 6;
+  unsigned key[kNI];
+  const unsigned vm = load_raw<BEAM>(p, r, base, n, key);
+  unsigned lmax = 0u;  // invalid slots hold key 0
+#pragma unroll
+  for (int i = 0; i < kNI; ++i) lmax = max(lmax, key[i]);
+  const Red3 wr = wave_reduce(0u, (vm & 1u) ? lmax : ~0u, lmax);
+  const unsigned km = unsigned(__popcll(__ballot((vm & 1u) && lmax == wr.hi)));
+  if (lane_id() == 0)
+    st_agent4(p.ex, (r * p.nseg + c * kWaves + w) * 16u, make_uint4(wr.hi, wr.lo, km, 0u));
+  wait_stores();
+  __syncthreads();
+  if (t == 0) last[0] = atomicAdd(&p.ctl->arrive[r], 1u) == p.nwg - 1u;
+  __syncthreads();
+  if (last[0] == 0u) return;  // workgroup-uniform
+  uint4 e[ROWS];  // (nseg <= ROWS * kThreads)
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(p.ex + size_t(r) * p.nseg, int(p.nseg * 16u));
+#pragma unroll
+  for (int i = 0; i < ROWS; ++i) e[i] = ld_agent4(rs, (unsigned(i) * kThreads + t) * 16u);
+  onepass_bound<ROWS>(p, sh, bs, e, 0, &p.tp_bound[r]);
+  if (t == 0) p.ctl->arrive[r] = 0u;
+}
+
 // Workgroups of the one-pass kernel that can be resident at once on the
 // current device (all of a call's workgroups must be, or they would wait on
 // ones that cannot start), and its wait for the bound in wall-clock ticks;
@@ -2018,18 +2080,47 @@ hipError_t launch_select(const SelectPlan& plan, int R, int prev_width, int voca
     return hipGetLastError();
   }
   if (plan.two_pass) {
-    p.segmax = reinterpret_cast<unsigned*>(ws + plan.seg_off);
     p.nseg = plan.nseg;
     p.nwg = plan.nchunks;
     p.cand_out = reinterpret_cast<uint2*>(ws + plan.slot_off);
     p.cnt_out = reinterpret_cast<unsigned*>(ws + plan.cnt_off);
     const unsigned blocks = unsigned(R) * plan.nchunks;
-    if (has_beam) select_segmax_kernel<true><<<blocks, kThreads, 0, st>>>(p);
-    else select_segmax_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    if (R <= kSelectOnePassMaxRequests && plan.nseg <= unsigned(kOnePassSegPer * kThreads) &&
+        unsigned(R) * plan.nchunks >= 4u * onepass_capacity()) {
+      // summaries and one bound word per request (the arrival counters are
+      // in the control block).  The summary pass costs about 10 us more than
+      // the wave maxima (each workgroup waits for its stores and its arrival
+      // before it leaves; the last request's bound ends the launch), and it
+      // saves the filter's per-workgroup bound (about 3.5 us per round of
+      // workgroups on the chip): it pays from four rounds on.
+      p.ctl = reinterpret_cast<OnePassCtl*>(ws);
+      p.ex = reinterpret_cast<uint4*>(ws + plan.seg_off);
+      p.tp_bound = reinterpret_cast<unsigned long long*>(ws + plan.bound_off);
+      // (the bound's rows of summaries per thread: as few as hold nseg)
+      if (plan.nseg <= 2u * kThreads) {
+        if (has_beam) select_summary_kernel<true, 2><<<blocks, kThreads, 0, st>>>(p);
+        else select_summary_kernel<false, 2><<<blocks, kThreads, 0, st>>>(p);
+      } else if (plan.nseg <= 4u * kThreads) {
+        if (has_beam) select_summary_kernel<true, 4><<<blocks, kThreads, 0, st>>>(p);
+        else select_summary_kernel<false, 4><<<blocks, kThreads, 0, st>>>(p);
+      } else {
+        if (has_beam) select_summary_kernel<true, kOnePassSegPer><<<blocks, kThreads, 0, st>>>(p);
+        else select_summary_kernel<false, kOnePassSegPer><<<blocks, kThreads, 0, st>>>(p);
+      }
+    } else {
+      p.segmax = reinterpret_cast<unsigned*>(ws + plan.seg_off);
+      if (has_beam) select_segmax_kernel<true><<<blocks, kThreads, 0, st>>>(p);
+      else select_segmax_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (has_beam) select_filter_kernel<true><<<blocks, kThreads, 0, st>>>(p);
-    else select_filter_kernel<false><<<blocks, kThreads, 0, st>>>(p);
+    if (p.tp_bound != nullptr) {
+      if (has_beam) select_filter_kernel<true, true><<<blocks, kThreads, 0, st>>>(p);
+      else select_filter_kernel<false, true><<<blocks, kThreads, 0, st>>>(p);
+    } else {
+      if (has_beam) select_filter_kernel<true, false><<<blocks, kThreads, 0, st>>>(p);
+      else select_filter_kernel<false, false><<<blocks, kThreads, 0, st>>>(p);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.nchunks <= unsigned(kThreads) && p.W <= unsigned(kOnePassRankMax)) {

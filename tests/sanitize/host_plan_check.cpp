@@ -86,8 +86,9 @@ static void select_plans() {
           EXPECT(plan.cap >= unsigned(W) && (plan.cap & (plan.cap - 1)) == 0);
           if (plan.two_pass) {
             EXPECT(plan.seg_off == head);
-            EXPECT(plan.seg_off < plan.slot_off && plan.slot_off < plan.cnt_off &&
-                   plan.cnt_off < plan.total);
+            EXPECT(plan.seg_off < plan.bound_off && plan.bound_off < plan.slot_off &&
+                   plan.slot_off < plan.cnt_off && plan.cnt_off < plan.total);
+            EXPECT(plan.bound_off - plan.seg_off >= size_t(R) * plan.nseg * 16);
             EXPECT(plan.nseg == plan.nchunks * 8u);
             EXPECT(uint64_t(plan.nchunks) * kSelectChunk >= N);
           } else {

@@ -170,10 +170,11 @@ def _select_plan_bytes(R, P, V, W, chunk=16384):
     n = P * V
     nchunks = -(-n // chunk)
     if n > chunk and n >= 2 * W * 2048 and nchunks <= 2048:
-        # two-pass / one-pass path: one 4-byte maximum per wave of 2048
-        # candidates, one slot of `cap` pairs per chunk, one (count, largest
-        # key) pair per chunk
-        return head + up(R * nchunks * 8 * 4) + up(R * nchunks * cap * 8) + up(R * nchunks * 8)
+        # two-pass / one-pass path: one 16-byte summary per wave of 2048
+        # candidates, one 8-byte bound word per request, one slot of `cap`
+        # pairs per chunk, one (count, largest key) pair per chunk
+        return (head + up(R * nchunks * 8 * 16) + up(R * 8) + up(R * nchunks * cap * 8)
+                + up(R * nchunks * 8))
     pairs, counts = [0, 0], [0, 0]
     if n > chunk:
         slots = -(-n // chunk)

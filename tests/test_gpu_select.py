@@ -54,6 +54,11 @@ CASES = [
     # stages), and more requests than the one-pass control block has
     ("two_pass_placed_r8_ties", 8, 256, SELECT_CODEBOOK, 256, "ties", True),
     ("two_pass_placed_r80", 80, 4, SELECT_CODEBOOK, 8, "ties", True),
+    # two-pass path whose first pass also forms each request's bound (four
+    # rounds of workgroups or more): 2, 4 and 8 rows of summaries per thread
+    ("two_pass_summary_rising_r8", 8, 256, SELECT_CODEBOOK, 256, "rising", True),
+    ("two_pass_summary_r4_w1024_ties", 4, 1024, 4096, 1024, "ties", True),
+    ("two_pass_summary_rows8", 2, 1024, SELECT_CODEBOOK, 256, "logsoftmax", True),
 ]
 
 
@@ -191,7 +196,7 @@ def test_select_one_pass_tags_and_epoch_wrap():
     nchunks = P * V // 16384
     nseg, cap, nsum = nchunks * 8, 2 * W, 8192
     up = lambda x: -(-x // 256) * 256
-    cnt_off = 1024 + nsum * 16 + up(R * nseg * 4) + up(R * nchunks * cap * 8)
+    cnt_off = 1024 + nsum * 16 + up(R * nseg * 16) + up(R * 8) + up(R * nchunks * cap * 8)
 
     def put_u32(off, vals):
         b = torch.from_numpy(np.asarray(vals, dtype=np.uint32).reshape(-1).view(np.uint8).copy())
